@@ -1,0 +1,241 @@
+/*
+ * hisparse.h -- C ABI of the HiSparse decode hot path on AMD Instinct MI355X (gfx950).
+ *
+ * HiSparse ("Scaling Sparse-Attention Decoding with Hierarchical KV Cache Management") keeps
+ * every request's full KV history in pinned host memory and gives each (request, layer) a
+ * small fixed-size GPU cache of B record slots (Section 3.2). Each decode step, the sparse
+ * indexer emits k selected logical records per request and layer; the library resolves them
+ * against the cache -- hit detection, LRU victim choice among the slots this step does not
+ * reference, fetch of the misses from pinned host memory into the freed HBM slots, and
+ * emission of the physical slot of every selected record in the selection's order
+ * (Section 3.4, phases 1-5) -- and then runs sparse decode attention over the k gathered
+ * records. For models whose layers share one indexer's selection, the anchor layer's miss
+ * plan is replayed into every shared layer's cache (Section 3.5, exact prefetch).
+ *
+ * Terms used below
+ *   unit   one independent cache: a (request, layer) for token-level selection, or a
+ *          (request, layer, kv head) for block/page selection. Unit u of a layer call is
+ *          request * units_per_request + head.
+ *   L      logical records per unit (tokens, blocks or pages), positions 0 .. L-1.
+ *   R      bytes per record.   k  selected records per unit per step.   B  slots per unit.
+ *
+ * Conventions
+ *   - Pointers prefixed d_ are device (HBM) pointers owned by the caller; the library reads or
+ *     writes them on the given stream and keeps no reference after the call returns.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *   - Calls marked [async] enqueue GPU work on `stream`, never synchronise the host, allocate
+ *     nothing and can be captured in a HIP graph. Calls marked [sync] block the host.
+ *   - Every call returns HISPARSE_OK or a negative hisparse_status_t; an argument error is
+ *     reported before any work is enqueued, and leaves all state untouched.
+ *   - Data errors found on the device (a selection entry >= L, or a repeated entry within one
+ *     unit's selection) do not fail the enqueueing call: that unit's state is left unchanged,
+ *     its k output slots are -1, its counts are (0, 0), and the error is latched for
+ *     hisparse_check_errors. Negative selection entries are padding: output slot -1, not
+ *     counted, never fetched.
+ *   - One handle must not be used by two host threads at once; calls on one handle that touch
+ *     the same layer must be ordered by the caller's streams.
+ */
+#ifndef HISPARSE_H
+#define HISPARSE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct hisparse_cache* hisparse_cache_t;
+
+typedef enum {
+  HISPARSE_OK = 0,
+  HISPARSE_ERR_INVALID_ARG = -1,   /* bad descriptor, layer index, pointer or size */
+  HISPARSE_ERR_OOM = -2,           /* device or pinned host allocation failed */
+  HISPARSE_ERR_HIP = -3,           /* a HIP runtime call failed */
+  HISPARSE_ERR_UNSUPPORTED = -4,   /* valid request this build does not implement */
+  HISPARSE_ERR_BAD_SELECTION = -5  /* latched device-side selection error (see above) */
+} hisparse_status_t;
+
+/* How missed records travel from the host pool to the GPU cache (Section 3.4 Phase 4). */
+typedef enum {
+  /* GPU threads load the missed records straight from mapped pinned host memory with 16-byte
+   * vector loads and store them into their slots: the GPU-assisted IO the paper adopts. */
+  HISPARSE_FETCH_ZERO_COPY = 0,
+  /* Timing mode (Section 4.6's "no-IO oracle"): tables and slot outputs are exact, but no
+   * record is copied, so the cache holds stale data and attention outputs are not valid. */
+  HISPARSE_FETCH_NONE = 2
+} hisparse_fetch_t;
+
+/* Kind of pinned host memory backing the pool. */
+typedef enum {
+  HISPARSE_HOST_COHERENT = 0,      /* fine-grained, mapped (hipHostMallocCoherent|Mapped) */
+  HISPARSE_HOST_NONCOHERENT = 1,   /* coarse-grained, mapped (hipHostMallocNonCoherent|Mapped) */
+  HISPARSE_HOST_UNCACHED = 2       /* fine-grained uncached (hipHostMallocUncached|Mapped) */
+} hisparse_host_memory_t;
+
+/* Cache descriptor (the paper's configuration: top_k, device buffer size B, transfer block
+ * size; Appendix A "Configuration", Section 3.2 "Sizing the cache"). */
+typedef struct {
+  int32_t num_requests;          /* >= 1 */
+  int32_t num_layers;            /* >= 1 */
+  int32_t units_per_request;     /* 1 (token-level) or kv heads (block/page selection) */
+  int32_t capacity;              /* B: slots per unit; top_k <= B <= 16384 */
+  int64_t num_records;           /* L: records per unit, 1 .. 2^31-1 */
+  int32_t top_k;                 /* k: 1 .. 4096 */
+  int32_t record_bytes;          /* R: multiple of 16, 16 .. 1 MiB */
+  int32_t share_group;           /* G >= 1: layers with layer % G == 0 are anchors that resolve;
+                                    layer l with l % G != 0 shares the selection of anchor
+                                    l - l % G (Section 3.5) */
+  int32_t fetch;                 /* hisparse_fetch_t */
+  int32_t host_memory;           /* hisparse_host_memory_t */
+  int32_t transfer_block_bytes;  /* bytes each fetch thread keeps in flight: 16, 32, 64, 128
+                                    or 256 (the paper's swap-in transfer block size); 0 = 64 */
+  int32_t reserved;              /* must be 0 */
+} hisparse_cache_desc_t;
+
+/* Sparse decode attention descriptor. The token layout inside a record is
+ * [tokens_per_record][token_elems] bf16 with token_elems = record_bytes / 2 / tokens_per_record;
+ * the key is the token's first d_qk elements and the value its d_v elements from v_offset.
+ * Supported shapes: (d_qk, d_v, v_offset) = (576, 512, 0), latent MLA where the value is the
+ * first 512 dims of the 576-dim latent record; and (128, 128, 128), GQA with K then V. */
+typedef struct {
+  int32_t q_heads;               /* query heads attending to one unit: 1 .. 256 */
+  int32_t d_qk;
+  int32_t d_v;
+  int32_t v_offset;
+  int32_t tokens_per_record;     /* 1 (token records), 16 (pages), 64 (blocks), ... */
+  int32_t num_splits;            /* partitions of the token sequence reduced in a fixed order;
+                                    0 = chosen from the shape alone */
+  float scale;                   /* softmax scale applied to q.k */
+  int32_t reserved;              /* must be 0 */
+} hisparse_attn_desc_t;
+
+/* Human-readable name of a status code (static storage). */
+const char* hisparse_status_string(hisparse_status_t status);
+
+/* [pure host] Check a cache descriptor without touching any device. */
+hisparse_status_t hisparse_validate_desc(const hisparse_cache_desc_t* desc);
+
+/* [pure host] Check an attention descriptor against a cache descriptor's record layout. */
+hisparse_status_t hisparse_validate_attn(int32_t record_bytes, int32_t top_k,
+                                         const hisparse_attn_desc_t* attn);
+
+/* [sync] Create a cache on HIP device `device`. Allocates, and owns until destroy:
+ *   - per layer, a pinned mapped host pool [units][L][R] (the authoritative full KV,
+ *     Section 3.2 "host KV pool"), uninitialised -- the caller stages prefill KV into it
+ *     (hisparse_host_pool) before resolving;
+ *   - per layer, the GPU cache [units][B][R] in HBM;
+ *   - per anchor layer, the page table [units][L] int32 (-1 = host-only), slot map [units][B]
+ *     int32 (-1 = empty), LRU timestamps [units][B] uint32, recency index [units][B], step clock
+ *     [units] and miss plan [units][k] -- all initialised to the cold state.
+ * On failure nothing stays allocated and *out is NULL. */
+hisparse_status_t hisparse_cache_create(const hisparse_cache_desc_t* desc, int32_t device,
+                                        hisparse_cache_t* out);
+
+/* [sync] Release everything the handle owns. NULL is accepted. */
+hisparse_status_t hisparse_cache_destroy(hisparse_cache_t cache);
+
+/* Host address and size of layer `layer`'s pinned host pool, laid out [units][L][R]: record r
+ * of unit u starts at host + (u * L + r) * R. The caller may write it whenever no GPU work
+ * that reads it is in flight. */
+hisparse_status_t hisparse_host_pool(hisparse_cache_t cache, int32_t layer, void** host,
+                                     size_t* bytes);
+
+/* Device address and size of layer `layer`'s GPU cache, laid out [units][B][R]. */
+hisparse_status_t hisparse_layer_cache(hisparse_cache_t cache, int32_t layer, void** device,
+                                       size_t* bytes);
+
+/* [async] Return every anchor layer's units to the cold state (all slots empty, clocks 0). */
+hisparse_status_t hisparse_reset(hisparse_cache_t cache, void* stream);
+
+/* [async] Resolve one step of an anchor layer (Section 3.4 phases 1-5).
+ *   d_sel    int32 [units][k]: selected positions per unit, in the indexer's order.
+ *   d_slots  int32 [units][k]: out; d_slots[u][i] is the slot of unit u now holding record
+ *            d_sel[u][i] (Section 3.3 (3): aligned with the selection's order); -1 for padding.
+ *   d_counts int32 [units][2]: out, {hits, misses} per unit; may be NULL.
+ * Replacement is LRU among the slots the step does not reference, with this step's hits
+ * promoted above its newly fetched misses (Section 3.2 "Replacement policy"). Ties are
+ * canonical: misses of step t are stamped 2t-1 and hits 2t (t = the unit's valid steps so
+ * far + 1); victims are taken in ascending (timestamp, slot) order, empty slots first, and
+ * the i-th miss in ascending position order takes the i-th victim. Misses are fetched from
+ * this layer's host pool (unless fetch = HISPARSE_FETCH_NONE), and the miss plan is kept for
+ * hisparse_prefetch_layer. Returns INVALID_ARG for a shared (non-anchor) layer. */
+hisparse_status_t hisparse_resolve(hisparse_cache_t cache, int32_t layer, const int32_t* d_sel,
+                                   int32_t* d_slots, int32_t* d_counts, void* stream);
+
+/* [async] The two halves of hisparse_resolve, for callers that schedule or time them apart
+ * (the paper's breakdown of a resolve into metadata phases and IO, Section 4.4):
+ * hisparse_resolve_tables runs phases 1-3 and 5 -- every output of hisparse_resolve and the
+ * miss plan, but no record is copied; hisparse_fetch then runs phase 4, copying the records of
+ * the anchor layer's latest miss plan from its host pool into its GPU cache (a no-op under
+ * HISPARSE_FETCH_NONE). hisparse_resolve == hisparse_resolve_tables + hisparse_fetch. */
+hisparse_status_t hisparse_resolve_tables(hisparse_cache_t cache, int32_t layer,
+                                          const int32_t* d_sel, int32_t* d_slots,
+                                          int32_t* d_counts, void* stream);
+hisparse_status_t hisparse_fetch(hisparse_cache_t cache, int32_t layer, void* stream);
+
+/* [async] Exact prefetch (Section 3.5): replay the miss plan recorded by the latest resolve of
+ * `anchor_layer` into the cache of `shared_layer` (anchor < shared < anchor + share_group),
+ * copying each planned record from shared_layer's own host pool into the same slot. After the
+ * replay, shared_layer's cache holds its records for the anchor's selection in the anchor's
+ * slots, so its attention reads through the anchor's d_slots. The caller orders it after that
+ * resolve (e.g. an event) and before the shared layer's attention, and must not start the
+ * anchor's next resolve before the replay has completed. */
+hisparse_status_t hisparse_prefetch_layer(hisparse_cache_t cache, int32_t anchor_layer,
+                                          int32_t shared_layer, void* stream);
+
+/* Bytes of device workspace hisparse_sparse_decode(_pool) needs for `units` units of top_k
+ * records each; 0 if the descriptor is invalid. */
+size_t hisparse_decode_workspace_bytes(int32_t units, int32_t top_k, int32_t record_bytes,
+                                       const hisparse_attn_desc_t* attn);
+
+/* [async] Sparse decode attention of one layer over its GPU cache (the consumer of Section 3.4
+ * Phase 5's slot vector).
+ *   d_q     bf16 [units][q_heads][d_qk] query.
+ *   d_slots int32 [units][k]: slots from hisparse_resolve (the anchor's, for a shared layer);
+ *           -1 entries are skipped.
+ *   d_out   float32 [units][q_heads][d_v]: out_h = sum_j softmax_j(scale * q_h . key_j) value_j
+ *           over the tokens of the selected records. A unit with no valid record gets zeros.
+ *   d_workspace / workspace_bytes: caller-owned scratch of at least
+ *           hisparse_decode_workspace_bytes(units, k, R, attn) bytes.
+ * The reduction order depends only on the position of a record in the slot vector, never on
+ * the slot value, so the result is bit-identical to hisparse_sparse_decode_pool over any other
+ * placement of the same records. */
+hisparse_status_t hisparse_sparse_decode(hisparse_cache_t cache, int32_t layer, const void* d_q,
+                                         const int32_t* d_slots, float* d_out,
+                                         const hisparse_attn_desc_t* attn, void* d_workspace,
+                                         size_t workspace_bytes, void* stream);
+
+/* [async] The same attention over an explicit device pool [units][records_per_unit][R], with
+ * d_idx int32 [units][k] record indices into each unit's part of the pool (-1 = skip). Used for
+ * a fully resident KV (indices = positions), or any other placement. */
+hisparse_status_t hisparse_sparse_decode_pool(const void* d_pool, int64_t records_per_unit,
+                                              int32_t record_bytes, int32_t units, int32_t top_k,
+                                              const void* d_q, const int32_t* d_idx, float* d_out,
+                                              const hisparse_attn_desc_t* attn,
+                                              void* d_workspace, size_t workspace_bytes,
+                                              void* stream);
+
+/* [sync] Copy an anchor layer's resolve state into host buffers (any may be NULL):
+ * slot_pos int32 [units][B], slot_ts uint32 [units][B], page_table int32 [units][L],
+ * order int32 [units][B] (slots by ascending (timestamp, slot)), clock uint32 [units]. */
+hisparse_status_t hisparse_read_state(hisparse_cache_t cache, int32_t layer, int32_t* slot_pos,
+                                      uint32_t* slot_ts, int32_t* page_table, int32_t* order,
+                                      uint32_t* clock);
+
+/* [sync] Copy an anchor layer's latest miss plan into host buffers (either may be NULL):
+ * plan int32 [units][k][2] = (position, slot) for the first count[u] entries, in ascending
+ * position order; count int32 [units]. */
+hisparse_status_t hisparse_read_plan(hisparse_cache_t cache, int32_t layer, int32_t* plan,
+                                     int32_t* count);
+
+/* [sync] Return HISPARSE_ERR_BAD_SELECTION if a device-side selection error was latched since
+ * the last check (info, if not NULL, receives {layer, unit, number of failing unit-steps}),
+ * clearing the latch; otherwise HISPARSE_OK. */
+hisparse_status_t hisparse_check_errors(hisparse_cache_t cache, int32_t* info);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HISPARSE_H */

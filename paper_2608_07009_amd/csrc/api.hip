@@ -1,0 +1,413 @@
+// C ABI of the HiSparse library: descriptor validation, allocation of the host pool, GPU
+// cache and resolve state, and the enqueueing entry points (declared in include/hisparse.h).
+#include <string.h>
+
+#include <algorithm>
+#include <new>
+
+#include "internal.h"
+
+using hisparse::kMaxCapacity;
+using hisparse::kMaxRecordBytes;
+using hisparse::kMaxTopK;
+
+namespace {
+
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+bool is_anchor(const hisparse_cache* c, int32_t layer) {
+  return layer >= 0 && layer < c->desc.num_layers && layer % c->desc.share_group == 0;
+}
+
+int transfer_block(const hisparse_cache_desc_t& d) {
+  return d.transfer_block_bytes == 0 ? 64 : d.transfer_block_bytes;
+}
+
+void free_all(hisparse_cache* c) {
+  if (!c) return;
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(c->device);
+  (void)hipDeviceSynchronize();
+  for (void* h : c->host)
+    if (h) (void)hipHostFree(h);
+  for (uint8_t* p : c->cache)
+    if (p) (void)hipFree(p);
+  for (auto& a : c->anchors) {
+    (void)hipFree(a.pt);
+    (void)hipFree(a.slot_pos);
+    (void)hipFree(a.slot_ts);
+    (void)hipFree(a.order);
+    (void)hipFree(a.clock);
+    (void)hipFree(a.plan);
+    (void)hipFree(a.plan_count);
+    (void)hipFree(a.counts);
+  }
+  if (c->err) (void)hipFree(c->err);
+  (void)hipSetDevice(prev);
+  delete c;
+}
+
+template <typename T>
+hisparse_status_t dmalloc(T** p, size_t bytes) {
+  *p = nullptr;
+  if (hipMalloc(reinterpret_cast<void**>(p), bytes) != hipSuccess) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    return HISPARSE_ERR_OOM;
+  }
+  return HISPARSE_OK;
+}
+
+hisparse::StateArgs state_args(const hisparse_cache* c, const hisparse_cache::Anchor& a) {
+  hisparse::StateArgs s{};
+  s.pt = a.pt;
+  s.slot_pos = a.slot_pos;
+  s.slot_ts = a.slot_ts;
+  s.order = a.order;
+  s.clock = a.clock;
+  s.plan_count = a.plan_count;
+  s.L = c->desc.num_records;
+  s.B = c->desc.capacity;
+  s.units = c->units;
+  return s;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* hisparse_status_string(hisparse_status_t s) {
+  switch (s) {
+    case HISPARSE_OK: return "HISPARSE_OK";
+    case HISPARSE_ERR_INVALID_ARG: return "HISPARSE_ERR_INVALID_ARG";
+    case HISPARSE_ERR_OOM: return "HISPARSE_ERR_OOM";
+    case HISPARSE_ERR_HIP: return "HISPARSE_ERR_HIP";
+    case HISPARSE_ERR_UNSUPPORTED: return "HISPARSE_ERR_UNSUPPORTED";
+    case HISPARSE_ERR_BAD_SELECTION: return "HISPARSE_ERR_BAD_SELECTION";
+  }
+  return "HISPARSE_ERR_UNKNOWN";
+}
+
+hisparse_status_t hisparse_validate_desc(const hisparse_cache_desc_t* d) {
+  if (!d) return HISPARSE_ERR_INVALID_ARG;
+  if (d->num_requests < 1 || d->num_layers < 1 || d->units_per_request < 1)
+    return HISPARSE_ERR_INVALID_ARG;
+  const int64_t units = (int64_t)d->num_requests * d->units_per_request;
+  if (units > 65535) return HISPARSE_ERR_INVALID_ARG;
+  if (d->top_k < 1 || d->top_k > kMaxTopK) return HISPARSE_ERR_INVALID_ARG;
+  if (d->capacity < d->top_k || d->capacity > kMaxCapacity) return HISPARSE_ERR_INVALID_ARG;
+  if (d->num_records < 1 || d->num_records > 0x7FFFFFFFLL) return HISPARSE_ERR_INVALID_ARG;
+  if (d->record_bytes < 16 || d->record_bytes > kMaxRecordBytes || d->record_bytes % 16 != 0)
+    return HISPARSE_ERR_INVALID_ARG;
+  if (d->share_group < 1) return HISPARSE_ERR_INVALID_ARG;
+  if (d->fetch != HISPARSE_FETCH_ZERO_COPY && d->fetch != HISPARSE_FETCH_NONE)
+    return HISPARSE_ERR_UNSUPPORTED;
+  if (d->host_memory < HISPARSE_HOST_COHERENT || d->host_memory > HISPARSE_HOST_UNCACHED)
+    return HISPARSE_ERR_INVALID_ARG;
+  const int tb = d->transfer_block_bytes;
+  if (!(tb == 0 || tb == 16 || tb == 32 || tb == 64 || tb == 128 || tb == 256))
+    return HISPARSE_ERR_INVALID_ARG;
+  if (d->reserved != 0) return HISPARSE_ERR_INVALID_ARG;
+  // the resolve kernel keeps the sorted misses, the slot outputs and two slot bitmaps in LDS
+  if (hisparse::resolve_lds_bytes(d->top_k, d->capacity) > 64 * 1024)
+    return HISPARSE_ERR_INVALID_ARG;
+  // per-unit host pool and cache offsets must fit comfortably in 64-bit byte offsets
+  if ((double)d->num_records * d->record_bytes * units > 4.0e18) return HISPARSE_ERR_INVALID_ARG;
+  return HISPARSE_OK;
+}
+
+hisparse_status_t hisparse_validate_attn(int32_t record_bytes, int32_t top_k,
+                                         const hisparse_attn_desc_t* a) {
+  if (!a) return HISPARSE_ERR_INVALID_ARG;
+  if (a->reserved != 0 || a->q_heads < 1 || a->q_heads > 256 || a->num_splits < 0)
+    return HISPARSE_ERR_INVALID_ARG;
+  if (top_k < 1 || top_k > kMaxTopK) return HISPARSE_ERR_INVALID_ARG;
+  const int tpr = a->tokens_per_record;
+  if (tpr < 1 || tpr > 4096 || (tpr & (tpr - 1)) != 0) return HISPARSE_ERR_INVALID_ARG;
+  if (record_bytes < 16 || record_bytes % (2 * tpr) != 0) return HISPARSE_ERR_INVALID_ARG;
+  if ((int64_t)top_k * tpr > (1 << 24)) return HISPARSE_ERR_INVALID_ARG;
+  const int token_elems = record_bytes / 2 / tpr;
+  const bool mla = a->d_qk == 576 && a->d_v == 512 && a->v_offset == 0;
+  const bool gqa = a->d_qk == 128 && a->d_v == 128 && a->v_offset == 128;
+  if (!mla && !gqa) return HISPARSE_ERR_UNSUPPORTED;
+  if (token_elems < std::max(a->d_qk, a->v_offset + a->d_v)) return HISPARSE_ERR_INVALID_ARG;
+  if ((record_bytes / tpr) % 16 != 0) return HISPARSE_ERR_INVALID_ARG;  // 16-byte token rows
+  if (!(a->scale > 0.f) || a->scale > 1e6f) return HISPARSE_ERR_INVALID_ARG;
+  return HISPARSE_OK;
+}
+
+hisparse_status_t hisparse_cache_create(const hisparse_cache_desc_t* desc, int32_t device,
+                                        hisparse_cache_t* out) {
+  if (!out) return HISPARSE_ERR_INVALID_ARG;
+  *out = nullptr;
+  hisparse_status_t st = hisparse_validate_desc(desc);
+  if (st != HISPARSE_OK) return st;
+  int n_dev = 0;
+  if (hipGetDeviceCount(&n_dev) != hipSuccess || device < 0 || device >= n_dev) {
+    (void)hipGetLastError();
+    return HISPARSE_ERR_INVALID_ARG;
+  }
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  if (hipSetDevice(device) != hipSuccess) return HISPARSE_ERR_HIP;
+
+  hisparse_cache* c = new (std::nothrow) hisparse_cache();
+  if (!c) return HISPARSE_ERR_OOM;
+  c->desc = *desc;
+  c->device = device;
+  c->units = desc->num_requests * desc->units_per_request;
+  c->n_anchors = (desc->num_layers + desc->share_group - 1) / desc->share_group;
+  const size_t U = (size_t)c->units, L = (size_t)desc->num_records, B = (size_t)desc->capacity;
+  const size_t R = (size_t)desc->record_bytes, K = (size_t)desc->top_k;
+  c->host_layer_bytes = U * L * R;
+  c->cache_layer_bytes = U * B * R;
+  c->host.assign(desc->num_layers, nullptr);
+  c->host_dev.assign(desc->num_layers, nullptr);
+  c->cache.assign(desc->num_layers, nullptr);
+  c->anchors.assign(c->n_anchors, hisparse_cache::Anchor{});
+
+  unsigned flags = hipHostMallocMapped;
+  if (desc->host_memory == HISPARSE_HOST_COHERENT) flags |= hipHostMallocCoherent;
+  else if (desc->host_memory == HISPARSE_HOST_NONCOHERENT) flags |= hipHostMallocNonCoherent;
+  else flags |= hipHostMallocUncached;
+
+  st = HISPARSE_OK;
+  for (int l = 0; l < desc->num_layers && st == HISPARSE_OK; ++l) {
+    if (hipHostMalloc(&c->host[l], c->host_layer_bytes, flags) != hipSuccess) {
+      c->host[l] = nullptr;
+      (void)hipGetLastError();
+      st = HISPARSE_ERR_OOM;
+      break;
+    }
+    if (hipHostGetDevicePointer(&c->host_dev[l], c->host[l], 0) != hipSuccess) {
+      (void)hipGetLastError();
+      st = HISPARSE_ERR_HIP;
+      break;
+    }
+    st = dmalloc(&c->cache[l], c->cache_layer_bytes);
+  }
+  for (int a = 0; a < c->n_anchors && st == HISPARSE_OK; ++a) {
+    auto& an = c->anchors[a];
+    if ((st = dmalloc(&an.pt, U * L * 4)) != HISPARSE_OK) break;
+    if ((st = dmalloc(&an.slot_pos, U * B * 4)) != HISPARSE_OK) break;
+    if ((st = dmalloc(&an.slot_ts, U * B * 4)) != HISPARSE_OK) break;
+    if ((st = dmalloc(&an.order, U * B * 4)) != HISPARSE_OK) break;
+    if ((st = dmalloc(&an.clock, U * 4)) != HISPARSE_OK) break;
+    if ((st = dmalloc(&an.plan, U * K * sizeof(int2))) != HISPARSE_OK) break;
+    if ((st = dmalloc(&an.plan_count, U * 4)) != HISPARSE_OK) break;
+    if ((st = dmalloc(&an.counts, U * 2 * 4)) != HISPARSE_OK) break;
+  }
+  if (st == HISPARSE_OK) st = dmalloc(&c->err, hisparse::kErrWords * 4);
+  if (st == HISPARSE_OK) {
+    if (hipMemset(c->err, 0, hisparse::kErrWords * 4) != hipSuccess) st = HISPARSE_ERR_HIP;
+    for (int l = 0; l < desc->num_layers && st == HISPARSE_OK; ++l)
+      if (hipMemset(c->cache[l], 0, c->cache_layer_bytes) != hipSuccess) st = HISPARSE_ERR_HIP;
+    for (int a = 0; a < c->n_anchors && st == HISPARSE_OK; ++a) {
+      if (hipMemset(c->anchors[a].plan, 0xFF, U * K * sizeof(int2)) != hipSuccess ||
+          hisparse::launch_reset_state(state_args(c, c->anchors[a]), nullptr) != hipSuccess)
+        st = HISPARSE_ERR_HIP;
+    }
+    if (st == HISPARSE_OK && hipDeviceSynchronize() != hipSuccess) st = HISPARSE_ERR_HIP;
+  }
+  (void)hipSetDevice(prev);
+  if (st != HISPARSE_OK) {
+    (void)hipGetLastError();
+    free_all(c);
+    return st;
+  }
+  *out = c;
+  return HISPARSE_OK;
+}
+
+hisparse_status_t hisparse_cache_destroy(hisparse_cache_t c) {
+  free_all(c);
+  return HISPARSE_OK;
+}
+
+hisparse_status_t hisparse_host_pool(hisparse_cache_t c, int32_t layer, void** host,
+                                     size_t* bytes) {
+  if (!c || layer < 0 || layer >= c->desc.num_layers) return HISPARSE_ERR_INVALID_ARG;
+  if (host) *host = c->host[layer];
+  if (bytes) *bytes = c->host_layer_bytes;
+  return HISPARSE_OK;
+}
+
+hisparse_status_t hisparse_layer_cache(hisparse_cache_t c, int32_t layer, void** device,
+                                       size_t* bytes) {
+  if (!c || layer < 0 || layer >= c->desc.num_layers) return HISPARSE_ERR_INVALID_ARG;
+  if (device) *device = c->cache[layer];
+  if (bytes) *bytes = c->cache_layer_bytes;
+  return HISPARSE_OK;
+}
+
+hisparse_status_t hisparse_reset(hisparse_cache_t c, void* stream) {
+  if (!c) return HISPARSE_ERR_INVALID_ARG;
+  for (auto& a : c->anchors)
+    if (hisparse::launch_reset_state(state_args(c, a), as_stream(stream)) != hipSuccess)
+      return HISPARSE_ERR_HIP;
+  return HISPARSE_OK;
+}
+
+hisparse_status_t hisparse_resolve_tables(hisparse_cache_t c, int32_t layer,
+                                          const int32_t* d_sel, int32_t* d_slots,
+                                          int32_t* d_counts, void* stream) {
+  if (!c || !d_sel || !d_slots || !is_anchor(c, layer)) return HISPARSE_ERR_INVALID_ARG;
+  auto& an = c->anchors[layer / c->desc.share_group];
+  hisparse::ResolveArgs a{};
+  a.sel = d_sel;
+  a.pt = an.pt;
+  a.slot_pos = an.slot_pos;
+  a.slot_ts = an.slot_ts;
+  a.order = an.order;
+  a.clock = an.clock;
+  a.slots_out = d_slots;
+  a.counts_out = d_counts ? d_counts : an.counts;
+  a.plan = an.plan;
+  a.plan_count = an.plan_count;
+  a.err = c->err;
+  a.L = c->desc.num_records;
+  a.B = c->desc.capacity;
+  a.k = c->desc.top_k;
+  a.layer = layer;
+  a.units = c->units;
+  if (hisparse::launch_resolve(a, as_stream(stream)) != hipSuccess) return HISPARSE_ERR_HIP;
+  return HISPARSE_OK;
+}
+
+namespace {
+// Copy the records of `anchor`'s latest miss plan from `target`'s host pool into `target`'s
+// GPU cache (target == anchor: the demand fetch; target a shared layer: the prefetch replay).
+hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t target,
+                                hipStream_t stream) {
+  if (c->desc.fetch == HISPARSE_FETCH_NONE) return HISPARSE_OK;
+  auto& an = c->anchors[anchor / c->desc.share_group];
+  hisparse::FetchArgs f{};
+  f.plan = an.plan;
+  f.plan_count = an.plan_count;
+  f.host = reinterpret_cast<const uint8_t*>(c->host_dev[target]);
+  f.cache = c->cache[target];
+  f.L = c->desc.num_records;
+  f.B = c->desc.capacity;
+  f.k = c->desc.top_k;
+  f.R = c->desc.record_bytes;
+  f.units = c->units;
+  if (hisparse::launch_fetch(f, transfer_block(c->desc), stream) != hipSuccess)
+    return HISPARSE_ERR_HIP;
+  return HISPARSE_OK;
+}
+}  // namespace
+
+hisparse_status_t hisparse_fetch(hisparse_cache_t c, int32_t layer, void* stream) {
+  if (!c || !is_anchor(c, layer)) return HISPARSE_ERR_INVALID_ARG;
+  return enqueue_fetch(c, layer, layer, as_stream(stream));
+}
+
+hisparse_status_t hisparse_resolve(hisparse_cache_t c, int32_t layer, const int32_t* d_sel,
+                                   int32_t* d_slots, int32_t* d_counts, void* stream) {
+  hisparse_status_t st = hisparse_resolve_tables(c, layer, d_sel, d_slots, d_counts, stream);
+  if (st != HISPARSE_OK) return st;
+  return enqueue_fetch(c, layer, layer, as_stream(stream));
+}
+
+hisparse_status_t hisparse_prefetch_layer(hisparse_cache_t c, int32_t anchor_layer,
+                                          int32_t shared_layer, void* stream) {
+  if (!c || !is_anchor(c, anchor_layer)) return HISPARSE_ERR_INVALID_ARG;
+  if (shared_layer <= anchor_layer || shared_layer >= c->desc.num_layers ||
+      shared_layer - anchor_layer >= c->desc.share_group)
+    return HISPARSE_ERR_INVALID_ARG;
+  return enqueue_fetch(c, anchor_layer, shared_layer, as_stream(stream));
+}
+
+size_t hisparse_decode_workspace_bytes(int32_t units, int32_t top_k, int32_t record_bytes,
+                                       const hisparse_attn_desc_t* attn) {
+  hisparse::AttnPlan p{};
+  if (hisparse::plan_attention(units, top_k, record_bytes, attn, &p) != HISPARSE_OK) return 0;
+  return p.workspace_bytes;
+}
+
+hisparse_status_t hisparse_sparse_decode_pool(const void* d_pool, int64_t records_per_unit,
+                                              int32_t record_bytes, int32_t units, int32_t top_k,
+                                              const void* d_q, const int32_t* d_idx, float* d_out,
+                                              const hisparse_attn_desc_t* attn,
+                                              void* d_workspace, size_t workspace_bytes,
+                                              void* stream) {
+  if (!d_pool || !d_q || !d_idx || !d_out || !d_workspace || records_per_unit < 1)
+    return HISPARSE_ERR_INVALID_ARG;
+  hisparse::AttnPlan p{};
+  hisparse_status_t st = hisparse::plan_attention(units, top_k, record_bytes, attn, &p);
+  if (st != HISPARSE_OK) return st;
+  if (workspace_bytes < p.workspace_bytes) return HISPARSE_ERR_INVALID_ARG;
+  if (hisparse::launch_attention(p, *attn, reinterpret_cast<const uint8_t*>(d_pool),
+                                 records_per_unit, record_bytes, units, top_k,
+                                 reinterpret_cast<const uint16_t*>(d_q), d_idx, d_out, d_workspace,
+                                 as_stream(stream)) != hipSuccess)
+    return HISPARSE_ERR_HIP;
+  return HISPARSE_OK;
+}
+
+hisparse_status_t hisparse_sparse_decode(hisparse_cache_t c, int32_t layer, const void* d_q,
+                                         const int32_t* d_slots, float* d_out,
+                                         const hisparse_attn_desc_t* attn, void* d_workspace,
+                                         size_t workspace_bytes, void* stream) {
+  if (!c || layer < 0 || layer >= c->desc.num_layers) return HISPARSE_ERR_INVALID_ARG;
+  return hisparse_sparse_decode_pool(c->cache[layer], c->desc.capacity, c->desc.record_bytes,
+                                     c->units, c->desc.top_k, d_q, d_slots, d_out, attn,
+                                     d_workspace, workspace_bytes, stream);
+}
+
+hisparse_status_t hisparse_read_state(hisparse_cache_t c, int32_t layer, int32_t* slot_pos,
+                                      uint32_t* slot_ts, int32_t* page_table, int32_t* order,
+                                      uint32_t* clock) {
+  if (!c || !is_anchor(c, layer)) return HISPARSE_ERR_INVALID_ARG;
+  auto& an = c->anchors[layer / c->desc.share_group];
+  const size_t U = (size_t)c->units, B = (size_t)c->desc.capacity;
+  const size_t L = (size_t)c->desc.num_records;
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(c->device);
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess && slot_pos) e = hipMemcpy(slot_pos, an.slot_pos, U * B * 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess && slot_ts) e = hipMemcpy(slot_ts, an.slot_ts, U * B * 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess && page_table) e = hipMemcpy(page_table, an.pt, U * L * 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess && order) e = hipMemcpy(order, an.order, U * B * 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess && clock) e = hipMemcpy(clock, an.clock, U * 4, hipMemcpyDeviceToHost);
+  (void)hipSetDevice(prev);
+  return e == hipSuccess ? HISPARSE_OK : HISPARSE_ERR_HIP;
+}
+
+hisparse_status_t hisparse_read_plan(hisparse_cache_t c, int32_t layer, int32_t* plan,
+                                     int32_t* count) {
+  if (!c || !is_anchor(c, layer)) return HISPARSE_ERR_INVALID_ARG;
+  auto& an = c->anchors[layer / c->desc.share_group];
+  const size_t U = (size_t)c->units, K = (size_t)c->desc.top_k;
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(c->device);
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess && plan) e = hipMemcpy(plan, an.plan, U * K * sizeof(int2), hipMemcpyDeviceToHost);
+  if (e == hipSuccess && count) e = hipMemcpy(count, an.plan_count, U * 4, hipMemcpyDeviceToHost);
+  (void)hipSetDevice(prev);
+  return e == hipSuccess ? HISPARSE_OK : HISPARSE_ERR_HIP;
+}
+
+hisparse_status_t hisparse_check_errors(hisparse_cache_t c, int32_t* info) {
+  if (!c) return HISPARSE_ERR_INVALID_ARG;
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(c->device);
+  int32_t w[hisparse::kErrWords] = {0, 0, 0, 0};
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess) e = hipMemcpy(w, c->err, sizeof(w), hipMemcpyDeviceToHost);
+  if (e == hipSuccess && w[0] != 0) e = hipMemset(c->err, 0, sizeof(w));
+  (void)hipSetDevice(prev);
+  if (e != hipSuccess) return HISPARSE_ERR_HIP;
+  if (info) {
+    info[0] = w[1];
+    info[1] = w[2];
+    info[2] = w[3];
+  }
+  return w[0] != 0 ? (hisparse_status_t)w[0] : HISPARSE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,101 @@
+// Internal declarations shared by the HiSparse HIP library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <vector>
+
+#include "hisparse.h"
+
+namespace hisparse {
+
+constexpr int kMaxTopK = 4096;
+constexpr int kMaxCapacity = 16384;
+constexpr int kMaxRecordBytes = 1 << 20;
+
+// Error word layout: [0] first error code, [1] layer, [2] unit, [3] failing unit-steps.
+constexpr int kErrWords = 4;
+
+struct ResolveArgs {
+  const int32_t* sel;   // [units][k]
+  int32_t* pt;          // [units][L]
+  int32_t* slot_pos;    // [units][B]
+  uint32_t* slot_ts;    // [units][B]
+  int32_t* order;       // [units][B], slots by ascending (ts, slot)
+  uint32_t* clock;      // [units]
+  int32_t* slots_out;   // [units][k]
+  int32_t* counts_out;  // [units][2]
+  int2* plan;           // [units][k] (position, slot)
+  int32_t* plan_count;  // [units]
+  int32_t* err;         // [kErrWords]
+  int64_t L;
+  int32_t B, k, layer, units;
+};
+
+struct FetchArgs {
+  const int2* plan;         // [units][k]
+  const int32_t* plan_count;  // [units]
+  const uint8_t* host;      // device-visible address of the layer's host pool [units][L][R]
+  uint8_t* cache;           // layer's GPU cache [units][B][R]
+  int64_t L;
+  int32_t B, k, R, units;
+};
+
+struct StateArgs {
+  int32_t* pt;
+  int32_t* slot_pos;
+  uint32_t* slot_ts;
+  int32_t* order;
+  uint32_t* clock;
+  int32_t* plan_count;
+  int64_t L;
+  int32_t B, units;
+};
+
+hipError_t launch_resolve(const ResolveArgs& a, hipStream_t stream);
+hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, hipStream_t stream);
+hipError_t launch_reset_state(const StateArgs& a, hipStream_t stream);
+size_t resolve_lds_bytes(int32_t k, int32_t B);
+
+// Attention over records addressed by idx[unit][k] (entries outside [0, records_per_unit) are skipped) into pool[unit][records_per_unit][R].
+struct AttnPlan {
+  int32_t hw, tw, hb;        // head waves, token waves, head blocks
+  int32_t n_tok;             // tokens per unit = k * tokens_per_record
+  int32_t split_tokens;      // tokens per workgroup split (multiple of 32 * tw)
+  int32_t n_wg_splits;       // workgroup splits per unit
+  int32_t n_parts;           // partial results per (unit, head) = n_wg_splits * tw
+  size_t workspace_bytes;
+};
+hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_bytes,
+                                 const hisparse_attn_desc_t* attn, AttnPlan* plan);
+hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
+                            const uint8_t* pool, int64_t records_per_unit, int32_t record_bytes,
+                            int32_t units, int32_t top_k, const uint16_t* q, const int32_t* idx,
+                            float* out, void* workspace, hipStream_t stream);
+
+}  // namespace hisparse
+
+struct hisparse_cache {
+  hisparse_cache_desc_t desc;
+  int device = 0;
+  int32_t units = 0;
+  int32_t n_anchors = 0;
+  size_t host_layer_bytes = 0;
+  size_t cache_layer_bytes = 0;
+  std::vector<void*> host;       // per layer, host address of the pinned pool
+  std::vector<void*> host_dev;   // per layer, device-visible address of the same pool
+  std::vector<uint8_t*> cache;   // per layer, GPU cache
+  struct Anchor {
+    int32_t* pt = nullptr;
+    int32_t* slot_pos = nullptr;
+    uint32_t* slot_ts = nullptr;
+    int32_t* order = nullptr;
+    uint32_t* clock = nullptr;
+    int2* plan = nullptr;
+    int32_t* plan_count = nullptr;
+    int32_t* counts = nullptr;   // used when the caller passes no counts buffer
+  };
+  std::vector<Anchor> anchors;   // per anchor layer (layer / share_group)
+  int32_t* err = nullptr;        // device error word
+};

@@ -1,0 +1,130 @@
+"""Exact layer-wise prefetch (Section 3.5) on the GPU.
+
+Shared layers reuse their anchor's selection and slot table; the anchor's miss plan is replayed
+into each shared layer's cache on a side stream. Checks:
+  * equivalence: replaying the plan gives the same cache contents as resolving the shared layer
+    itself with the same selection (the canonical LRU is a deterministic function of the
+    selection stream);
+  * every resident slot of every shared layer holds that layer's own host record;
+  * shared-layer attention through the anchor's slots equals attention over the fully resident
+    KV of that layer (bit-identical) and the oracle (tolerance);
+  * the side-stream/event ordering: the anchor's next resolve never runs before the previous
+    replays finish (checked by results, over many steps).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workload as W
+from hs_harness import Run, attn_desc, d2h, layer_cache_host, log
+from paper_2608_07009_amd import HiSparseCache, hisparse as hs
+
+pytestmark = pytest.mark.gpu
+
+
+def test_replay_equals_independent_resolve():
+    w = W.workload(1, num_layers=2, share_group=2)
+    steps = 24
+    dev = torch.device("cuda:0")
+    shared = HiSparseCache.for_workload(w)
+    indep = HiSparseCache.for_workload(w.__class__(**{**w.__dict__, "share_group": 1}))
+    try:
+        for c in (shared, indep):
+            for l in range(2):
+                W.fill_kv(c.host_pool(l)[0], w, l)
+        sel = torch.from_numpy(W.selection_streams(w, steps=steps)).to(dev)  # [steps][1][k]
+        s_a = torch.empty((1, w.k), dtype=torch.int32, device=dev)
+        s_b0 = torch.empty_like(s_a)
+        s_b1 = torch.empty_like(s_a)
+        st = torch.cuda.current_stream()
+        for t in range(steps):
+            hs.hisparse_resolve(shared.handle, 0, sel[t], s_a, None, st)
+            hs.hisparse_prefetch_layer(shared.handle, 0, 1, st)
+            hs.hisparse_resolve(indep.handle, 0, sel[t], s_b0, None, st)
+            hs.hisparse_resolve(indep.handle, 1, sel[t], s_b1, None, st)
+            assert torch.equal(s_a, s_b0) and torch.equal(s_a, s_b1)
+            pa, na = shared.layer_cache(1)
+            pb, nb = indep.layer_cache(1)
+            assert (d2h(pa, na) == d2h(pb, nb)).all(), f"step {t}"
+    finally:
+        shared.close()
+        indep.close()
+
+
+@pytest.mark.parametrize("cfg,steps", [(1, 16), (5, 6)])
+def test_prefetch_side_stream(cfg, steps):
+    base = W.workload(cfg)
+    if cfg == 1:
+        base = W.workload(1, num_layers=7, share_group=4)  # anchors 0 and 4
+    run = Run(base, steps)
+    w = run.w
+    log(f"test_prefetch_side_stream {w.name} layers={w.num_layers} anchors={w.anchors}")
+    try:
+        main = torch.cuda.current_stream()
+        side = torch.cuda.Stream()
+        ad = attn_desc(w)
+        ws = torch.empty(hs.hisparse_decode_workspace_bytes(w.units, w.k, w.record_bytes, ad),
+                         dtype=torch.uint8, device=run.dev)
+        outs = {l: torch.empty((w.units, w.q_heads, w.d_v), dtype=torch.float32,
+                               device=run.dev) for l in range(w.num_layers)}
+        orcs = {l: oracle.OracleCache(w.units, w.L, w.B, w.k) for l in w.anchors}
+        check_layers = sorted({1, w.num_layers - 1} - set(w.anchors))
+        for t in range(steps):
+            q = {l: torch.from_numpy(W.queries(w, t, l).view(np.int16)).to(run.dev)
+                 for l in check_layers}
+            for a in w.anchors:
+                hs.hisparse_resolve(run.cache.handle, a, run.sel_ptr(t, a), run.slots[a],
+                                    run.counts[a], main)
+                ev = torch.cuda.Event()
+                ev.record(main)
+                side.wait_event(ev)
+                done = {}
+                for s in range(a + 1, min(a + w.share_group, w.num_layers)):
+                    hs.hisparse_prefetch_layer(run.cache.handle, a, s, side)
+                    done[s] = torch.cuda.Event()
+                    done[s].record(side)
+                for s, e in done.items():
+                    main.wait_event(e)
+                    if s in check_layers:
+                        hs.hisparse_sparse_decode(run.cache.handle, s, q[s], run.slots[a],
+                                                  outs[s], ad, ws, ws.numel(), main)
+            torch.cuda.synchronize()
+            for a in w.anchors:
+                sel = run.sel_host[t, (a // w.share_group) * w.units:
+                                   (a // w.share_group + 1) * w.units]
+                e_slots, _, _, _, bad = orcs[a].resolve(sel)
+                assert bad == 0 and (run.slots[a].cpu().numpy() == e_slots).all()
+            if t in (0, steps - 1):
+                for s in check_layers:
+                    a = s - s % w.share_group
+                    img = layer_cache_host(run, s)
+                    host = run.cache.host_view(s)
+                    sp = orcs[a].slot_pos
+                    for u in range(w.units):
+                        res = np.nonzero(sp[u] >= 0)[0]
+                        assert (img[u, res] == host[u, sp[u, res]]).all(), f"layer {s} step {t}"
+                    # attention of the shared layer vs its resident KV and the oracle
+                    resident = torch.from_numpy(host.reshape(-1)).to(run.dev)
+                    sel_dev = run.sel[t, (a // w.share_group) * w.units:
+                                      (a // w.share_group + 1) * w.units]
+                    ref_dev = torch.empty_like(outs[s])
+                    hs.hisparse_sparse_decode_pool(resident, w.L, w.record_bytes, w.units, w.k,
+                                                   q[s], sel_dev, ref_dev, ad, ws, ws.numel(),
+                                                   main)
+                    torch.cuda.synchronize()
+                    assert torch.equal(ref_dev, outs[s])
+                    del resident
+                    qh = W.queries(w, t, s)
+                    sel0 = run.sel_host[t, (a // w.share_group) * w.units]
+                    ref = oracle.sparse_decode(qh[0], host[0].view(np.uint16).reshape(w.L, -1),
+                                               sel0, d_qk=w.d_qk, d_v=w.d_v, v_off=w.v_offset,
+                                               token_elems=w.token_elems,
+                                               tokens_per_record=w.tokens_per_record,
+                                               scale=w.scale)
+                    o = outs[s].cpu().numpy()[0]
+                    assert np.abs(o - ref).max() <= 1e-2
+                    assert np.linalg.norm(o - ref) / np.linalg.norm(ref) <= 5e-3
+                    log(f"  step {t} shared layer {s}: ok")
+    finally:
+        run.close()

@@ -1,0 +1,89 @@
+"""GPU parity of the resolve path (Section 3.4 phases 1-5) against the CPU oracle.
+
+Bit-exact on every step: the slot vector of every unit, (hits, misses), and the miss plan;
+at checkpoints: the full LRU state (slot map, timestamps, page table, clock, recency index)
+and the bytes of every resident slot against the host record it claims to hold."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workload as W
+from hs_harness import Run, expected_order, layer_cache_host, log
+from paper_2608_07009_amd import hisparse as hs
+
+pytestmark = pytest.mark.gpu
+
+# full shapes; steps trimmed so every config finishes in well under a minute
+STEPS = {1: 64, 2: 40, 3: 128, 4: 64, 5: 24}
+
+
+def check_state(run, layer, orc, full_pt=True):
+    st = run.cache.read_state(layer, page_table=full_pt)
+    assert (st["slot_pos"] == orc.slot_pos).all()
+    assert (st["slot_ts"] == orc.slot_ts).all()
+    assert (st["clock"] == orc.clock).all()
+    assert (st["order"] == expected_order(orc.slot_ts)).all()
+    if full_pt:
+        assert (st["page_table"] == orc.pt).all()
+
+
+def check_resident_bytes(run, layer, orc):
+    """Every resident slot holds exactly the host record its slot map names."""
+    img = layer_cache_host(run, layer)
+    host = run.cache.host_view(layer)
+    for u in range(run.w.units):
+        res = np.nonzero(orc.slot_pos[u] >= 0)[0]
+        assert (img[u, res] == host[u, orc.slot_pos[u, res]]).all(), f"unit {u}"
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_resolve_matches_oracle(cfg):
+    steps = STEPS[cfg]
+    log(f"test_resolve_matches_oracle cfg={cfg} steps={steps}")
+    run = Run(W.workload(cfg), steps)
+    w = run.w
+    try:
+        orcs = {l: oracle.OracleCache(w.units, w.L, w.B, w.k) for l in w.anchors}
+        checkpoints = {0, 1, steps // 2, steps - 1}
+        for t in range(steps):
+            run.resolve_step(t)
+            slots = run.slots.cpu().numpy()
+            counts = run.counts.cpu().numpy()
+            for l in w.anchors:
+                a = l // w.share_group
+                sel = run.sel_host[t, a * w.units:(a + 1) * w.units]
+                e_slots, e_counts, pp, ps, bad = orcs[l].resolve(sel)
+                assert bad == 0
+                assert (slots[l] == e_slots).all(), f"slots step {t} layer {l}"
+                assert (counts[l] == e_counts).all(), f"counts step {t} layer {l}"
+                if t in checkpoints and l in (w.anchors[0], w.anchors[-1]):
+                    plan, cnt = run.cache.read_plan(l)
+                    assert (cnt == e_counts[:, 1]).all()
+                    for u in range(w.units):
+                        m = cnt[u]
+                        assert (plan[u, :m, 0] == pp[u, :m]).all()
+                        assert (plan[u, :m, 1] == ps[u, :m]).all()
+                    check_state(run, l, orcs[l], full_pt=(w.units * w.L <= 1 << 24))
+                    check_resident_bytes(run, l, orcs[l])
+            if t in checkpoints:
+                log(f"  step {t}: hits/misses unit0 layer0 = {counts[0, 0].tolist()}")
+        st, info = run.cache.check_errors()
+        assert st == hs.HISPARSE_OK
+    finally:
+        run.close()
+
+
+def test_resolve_fetch_none_same_tables():
+    """FETCH_NONE (no-IO timing mode) publishes the same slot tables and counts."""
+    w = W.workload(1)
+    a = Run(w, 32)
+    b = Run(w, 32, fill=False, fetch=hs.HISPARSE_FETCH_NONE)
+    try:
+        for t in range(32):
+            a.resolve_step(t)
+            b.resolve_step(t)
+            assert torch.equal(a.slots, b.slots) and torch.equal(a.counts, b.counts)
+    finally:
+        a.close()
+        b.close()

@@ -222,3 +222,18 @@ def normal_table() -> np.ndarray:
 def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
     """Exact widening of bf16 bit patterns."""
     return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def pinned_budget_bytes() -> int:
+    """Pinned host memory the harness may use (HISPARSE_PINNED_BUDGET_GIB, default 63 GiB: the
+    MI355X boxes this was measured on refuse to pin more than about 65 GiB per process)."""
+    return int(float(os.environ.get("HISPARSE_PINNED_BUDGET_GIB", "63")) * 2**30)
+
+
+def fit_pinned(w: Workload, budget: int | None = None) -> Workload:
+    """The workload with as many of its layers as fit the pinned-memory budget (all other shapes
+    unchanged). Per-layer work is identical, so per-layer metrics are unaffected."""
+    budget = pinned_budget_bytes() if budget is None else budget
+    per_layer = w.units * w.L * w.record_bytes
+    n = min(w.num_layers, max(1, budget // per_layer))
+    return w if n == w.num_layers else replace(w, num_layers=int(n))
