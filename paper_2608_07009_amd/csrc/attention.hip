@@ -30,12 +30,19 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kChunk = 32;            // tokens per wave per iteration
-constexpr int kKPad = 8;              // bf16 padding per K row in LDS
-constexpr int kVtRow = kChunk + 8;    // bf16 per V^T row in LDS (32 tokens + padding)
-constexpr int kTargetWorkgroups = 512;
+constexpr int kTargetWorkgroups = 256;
+constexpr int kMaxSplitRecords = 1024;  // record indices of one split staged in LDS
+constexpr int kMaxSplitTokens = 8192;   // tokens of one split (validity bitmask in LDS)
+// Rescale the running output only when a head's running max grows by more than this (log2
+// units): exponentials are taken against a slightly stale max (values up to 2^8), which is
+// exact softmax arithmetic with a different reference point and keeps fp32/bf16 far from
+// overflow; the final normalisation uses the same reference.
+constexpr float kRescaleSlack = 8.0f;
+
+// 16-byte loads of padding tokens and padding slots read zeros from here.
+__device__ __attribute__((aligned(16))) uint8_t g_zero_token[2048];
 
 struct AttnArgs {
   const uint8_t* pool;
@@ -57,30 +64,54 @@ __device__ inline uint16_t f32_to_bf16_rne(float f) {
 __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
 __device__ inline u32x4 lds_load16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
-__device__ inline u32x2 lds_load8(const uint16_t* p) { return *reinterpret_cast<const u32x2*>(p); }
 __device__ inline void lds_store16(uint16_t* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
 
-// Key chunks (8 bf16 each) that the value range does not already cover.
-template <int DQK, int DV, int VOFF>
-struct KeyOnly {
-  static_assert(VOFF == 0 || VOFF >= DQK, "value range must start the token or follow the key");
-  static constexpr int start = VOFF == 0 ? DV / 8 : 0;
-  static constexpr int count = VOFF == 0 ? DQK / 8 - DV / 8 : DQK / 8;
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Wait until at most N direct-to-LDS loads of this wave are outstanding and its LDS writes are
+// done, then synchronise the workgroup. (A workgroup fence would also drain the younger
+// prefetches, which is exactly what the pipeline must not do.)
+template <int N>
+__device__ inline void wait_loads_and_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+// LDS tile of one 32-token chunk: token t's 16-byte piece c at slot t * PP + c, PP >= P pieces
+// per row. The padding makes consecutive rows start 36 (MLA: PP = 73) or 20 (GQA: PP = 37)
+// banks apart, so the 16 rows read by one MFMA operand load hit distinct banks, and the
+// transpose reads (4 rows x 4 column pairs per 16 lanes) do too.
+template <int P>
+struct TileRow {
+  static constexpr int PP = (P == 72) ? 73 : (P == 32 ? 37 : P + 1);
 };
 
-template <int DQK, int DV, int VOFF, int HW, int TW>
-__global__ __launch_bounds__(64 * HW * TW) void attn_partial_kernel(AttnArgs a) {
-  constexpr int GT = 64 * HW;                 // threads per token group
-  constexpr int KROW = DQK + kKPad;
-  constexpr int K_TILE = kChunk * KROW;
-  constexpr int VT_TILE = DV * kVtRow;
-  constexpr int TG_ELEMS = K_TILE + VT_TILE;
+// Row order of a 32-token chunk inside the MFMA tiles: operand row m of tile h reads token
+// 16h + perm(m) with perm(4g + s) = 8 (g >> 1) + 2s + (g & 1). A lane's S^T accumulator then
+// holds tokens perm(4g + j) (+16), and the PV transpose reads touch rows two apart, which
+// with the padded row stride keeps both access patterns free of bank conflicts.
+__device__ inline int tile_row(int m) { return 8 * (m >> 3) + 2 * (m & 3) + ((m >> 2) & 1); }
+
+template <int DQK, int DV, int VOFF, int HW, int TW, int NST>
+__global__ __launch_bounds__(64 * HW * TW, (HW * TW >= 8) ? 2 : 1)
+void attn_partial_kernel(AttnArgs a) {
+  constexpr int TE = (DQK > VOFF + DV) ? DQK : VOFF + DV;  // bf16 per token used here
+  constexpr int P = TE / 8;                                 // 16-byte pieces per token
+  constexpr int PP = TileRow<P>::PP;                        // pieces per LDS row
+  constexpr int NL = ((kChunk - 1) * PP + P + 63) / 64;     // 64-lane loads per chunk
+  constexpr int TILE = NL * 64 * 8;                         // bf16 per chunk tile
+  constexpr int LPW_MAX = (NL + HW - 1) / HW;               // loads per wave (first waves)
+  constexpr int LPW_MIN = NL / HW;                          // loads per wave (last waves)
+  constexpr int NL_REM = NL % HW;                           // waves doing LPW_MAX loads
   constexpr int NKK = DQK / 32;
   constexpr int NOUT = DV / 16;
-  constexpr int VCH = DV / 8;                 // value chunks per token
-  using KO = KeyOnly<DQK, DV, VOFF>;
-  static_assert(DQK % 32 == 0 && DV % 16 == 0, "shape");
-  __shared__ __align__(16) uint16_t s_kv[TW * TG_ELEMS];
+  static_assert(DQK % 32 == 0 && DV % 16 == 0 && VOFF % 8 == 0, "shape");
+  static_assert(NST >= 2 && NST <= 4 && (NST - 2) * LPW_MAX < 64, "pipeline depth");
+  __shared__ __align__(16) uint16_t s_kv[TW * NST * TILE];
+  __shared__ int32_t s_idx[kMaxSplitRecords];  // the split's record indices, -1 = skip
+  __shared__ uint32_t s_valid[kMaxSplitTokens / 32];  // bit t of word c: token 32c+t attends
 
   // XCD-aware mapping: consecutive workgroup ids go round-robin over the 8 XCDs, so give each
   // XCD a contiguous range of work items; the head blocks of one (unit, split) then share the
@@ -94,10 +125,22 @@ __global__ __launch_bounds__(64 * HW * TW) void attn_partial_kernel(AttnArgs a) 
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hg = wave % HW, tg = wave / HW;
-  const int gtid = tid - tg * GT;
   const int g = lane >> 4;
-  uint16_t* s_k = s_kv + tg * TG_ELEMS;
-  uint16_t* s_vt = s_k + K_TILE;
+  uint16_t* s_tiles = s_kv + tg * NST * TILE;
+
+  const int tok_begin = split * a.split_tokens;
+  const int tok_end = min(a.n_tok, tok_begin + a.split_tokens);
+  const int rec_begin = tok_begin >> a.tpr_shift;
+  const int n_rec = ((tok_end - 1) >> a.tpr_shift) - rec_begin + 1;
+  const int tpr_mask = (1 << a.tpr_shift) - 1;
+  {
+    const int32_t* idx_u = a.idx + (int64_t)unit * a.k + rec_begin;
+    for (int i = tid; i < n_rec; i += 64 * HW * TW) {
+      const int32_t s = idx_u[i];
+      s_idx[i] = (s >= 0 && s < a.rec_per_unit) ? s : -1;
+    }
+  }
+  const uint8_t* pool_u = a.pool + (int64_t)unit * a.rec_per_unit * a.R;
 
   const int head = hb * 16 * HW + hg * 16 + (lane & 15);
   const bool head_ok = head < a.H;
@@ -117,103 +160,89 @@ __global__ __launch_bounds__(64 * HW * TW) void attn_partial_kernel(AttnArgs a) 
   for (int n = 0; n < NOUT; ++n) o[n] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
-  const int tok_begin = split * a.split_tokens;
-  const int tok_end = min(a.n_tok, tok_begin + a.split_tokens);
-  const int32_t* idx_u = a.idx + (int64_t)unit * a.k;
-  const uint8_t* pool_u = a.pool + (int64_t)unit * a.rec_per_unit * a.R;
-  const int tpr_mask = (1 << a.tpr_shift) - 1;
-
-  for (int c0 = tok_begin; c0 < tok_end; c0 += kChunk * TW) {
-    const int cbase = c0 + tg * kChunk;
-    __syncthreads();  // the previous chunk's LDS reads are done
-
-    // ---- stage: K rows natural, V transposed to [dim][token] ----
-    for (int item = gtid; item < (kChunk / 8) * VCH; item += GT) {
-      const int oct = item / VCH, c = item % VCH;
-      u32x4 in[8];
-#pragma unroll
-      for (int t8 = 0; t8 < 8; ++t8) {
-        const int tk = cbase + oct * 8 + t8;
-        in[t8] = u32x4{0u, 0u, 0u, 0u};
-        if (tk < tok_end) {
-          const int32_t s = idx_u[tk >> a.tpr_shift];
-          if (s >= 0 && s < a.rec_per_unit)
-            in[t8] = *reinterpret_cast<const u32x4*>(pool_u + (int64_t)s * a.R +
-                                                     (int64_t)(tk & tpr_mask) * a.token_bytes +
-                                                     (VOFF + c * 8) * 2);
-        }
-      }
-      if (VOFF + c * 8 < DQK) {
-#pragma unroll
-        for (int t8 = 0; t8 < 8; ++t8) lds_store16(s_k + (oct * 8 + t8) * KROW + VOFF + c * 8, in[t8]);
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        u32x4 r;
-#pragma unroll
-        for (int w2 = 0; w2 < 4; ++w2) {
-          const uint32_t x = in[2 * w2][j >> 1], y = in[2 * w2 + 1][j >> 1];
-          r[w2] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
-        }
-        lds_store16(s_vt + (c * 8 + j) * kVtRow + oct * 8, r);
+  __syncthreads();  // s_idx is ready
+  const int n_it = (tok_end - tok_begin + kChunk * TW - 1) / (kChunk * TW);
+  {
+    // every chunk the token groups iterate over gets its word, including chunks that lie
+    // wholly past the split end (all zero)
+    const int span = n_it * kChunk * TW;
+    for (int base = wave * 64; base < span; base += 64 * HW * TW) {
+      const int tk = tok_begin + base + lane;
+      const bool ok = tk < tok_end && s_idx[(tk >> a.tpr_shift) - rec_begin] >= 0;
+      const uint64_t m = __ballot(ok);
+      if (lane == 0) {
+        s_valid[base >> 5] = (uint32_t)m;
+        if (base + 32 < span) s_valid[(base >> 5) + 1] = (uint32_t)(m >> 32);
       }
     }
-    for (int item = gtid; item < kChunk * KO::count; item += GT) {
-      const int tok = item / KO::count, c = KO::start + item % KO::count;
-      const int tk = cbase + tok;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (tk < tok_end) {
-        const int32_t s = idx_u[tk >> a.tpr_shift];
-        if (s >= 0 && s < a.rec_per_unit)
-          v = *reinterpret_cast<const u32x4*>(pool_u + (int64_t)s * a.R +
-                                              (int64_t)(tk & tpr_mask) * a.token_bytes + c * 16);
-      }
-      lds_store16(s_k + tok * KROW + c * 8, v);
-    }
-    __syncthreads();
+  }
 
-    // ---- scores: S^T tiles for tokens [0,16) and [16,32) of the chunk ----
-    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
-    const uint16_t* k0 = s_k + (lane & 15) * KROW + 8 * g;
-    const uint16_t* k1 = k0 + 16 * KROW;
+  // Direct global->LDS staging of chunk `it` of this token group into pipeline buffer `buf`.
+  // Load j (64 lanes) fills slots 64j .. 64j+63; wave hg issues loads [j0, j0 + n_loads).
+  // Padding slots are skipped; padding tokens and tokens past the split end get zeros (their
+  // scores are masked to -inf, so they carry P = 0).
+  const int n_loads = hg < NL_REM ? LPW_MAX : LPW_MIN;
+  const int j0 = hg * LPW_MIN + min(hg, NL_REM);
+  auto issue = [&](int it, int buf) {
+    const int cbase = tok_begin + it * kChunk * TW + tg * kChunk;
+    uint16_t* tile = s_tiles + buf * TILE;
+    // recompute the per-lane slot arithmetic here instead of keeping it live across the loop
+    int lane = threadIdx.x & 63;
+    asm volatile("" : "+v"(lane));
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) {
-      const bf16x8_t a0 = __builtin_bit_cast(bf16x8_t, lds_load16(k0 + kk * 32));
-      const bf16x8_t a1 = __builtin_bit_cast(bf16x8_t, lds_load16(k1 + kk * 32));
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qreg[kk], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, qreg[kk], s1, 0, 0, 0);
-    }
-
-    // ---- online softmax for this lane's head over its 8 tokens ----
-    float sc[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int tk = cbase + (j < 4 ? 4 * g + j : 16 + 4 * g + (j - 4));
-      bool ok = tk < tok_end;
-      if (ok) {
-        const int32_t s = idx_u[tk >> a.tpr_shift];
-        ok = s >= 0 && s < a.rec_per_unit;
+    for (int jj = 0; jj < LPW_MAX; ++jj) {
+      if (jj < n_loads) {  // wave-uniform
+        const int j = j0 + jj;
+        const int p = 64 * j + lane;
+        const int t = p / PP, c = p % PP;
+        const int tk = cbase + t;
+        const bool real = t < kChunk && c < P && tk < tok_end;
+        const int32_t s = real ? s_idx[(tk >> a.tpr_shift) - rec_begin] : -1;
+        const uint8_t* src = s >= 0 ? pool_u + (int64_t)s * a.R +
+                                          (int64_t)(tk & tpr_mask) * a.token_bytes + 16 * c
+                                    : g_zero_token + 16 * (c < P ? c : 0);
+        __builtin_amdgcn_global_load_lds(src, (lds_void*)(tile + 64 * j * 8), 16, 0, 0);
       }
-      const float raw = j < 4 ? s0[j] : s1[j - 4];
-      sc[j] = ok ? raw * a.scale_log2 : -INFINITY;
     }
-    float cmax = sc[0];
+  };
+  // this wave's loads for the current chunk are done once at most `younger` later chunks'
+  // loads are outstanding
+  auto wait_chunk = [&](int younger) {
+    if constexpr (NST == 2) {
+      wait_loads_and_barrier<0>();
+    } else if (hg < NL_REM) {
+      if (younger >= 2) wait_loads_and_barrier<(NST - 2) * LPW_MAX>();
+      else if (younger == 1) wait_loads_and_barrier<LPW_MAX>();
+      else wait_loads_and_barrier<0>();
+    } else {
+      if (younger >= 2) wait_loads_and_barrier<(NST - 2) * LPW_MIN>();
+      else if (younger == 1) wait_loads_and_barrier<LPW_MIN>();
+      else wait_loads_and_barrier<0>();
+    }
+  };
+
 #pragma unroll
-    for (int j = 1; j < 8; ++j) cmax = fmaxf(cmax, sc[j]);
-    cmax = fmaxf(cmax, __shfl_xor(cmax, 16, 64));
-    cmax = fmaxf(cmax, __shfl_xor(cmax, 32, 64));
-    const float m_new = fmaxf(m_run, cmax);
-    float alpha = 1.f;
+  for (int st = 0; st < NST - 1; ++st)
+    if (st < n_it) issue(st, st);
+
+  // Per chunk: scores (QK), softmax against the running reference max, then P.V. O is touched
+  // only by MFMAs inside the loop; the rare move of a head's reference max (growth beyond the
+  // slack) leaves the loop, rescales, finishes that chunk and re-enters.
+  f32x4 s0, s1;
+  float sc[8];
+  float cmax = -INFINITY;
+  int it = 0;
+
+  auto finish_chunk = [&](const uint16_t* tile) {
     uint32_t pw[4];
     float psum = 0.f;
-    if (m_new == -INFINITY) {
+    if (m_run == -INFINITY) {
       pw[0] = pw[1] = pw[2] = pw[3] = 0u;
     } else {
-      alpha = exp2f(m_run - m_new);
 #pragma unroll
       for (int j = 0; j < 8; j += 2) {
-        const uint16_t b0 = f32_to_bf16_rne(exp2f(sc[j] - m_new));
-        const uint16_t b1 = f32_to_bf16_rne(exp2f(sc[j + 1] - m_new));
+        const uint16_t b0 = f32_to_bf16_rne(exp2f(sc[j] - m_run));
+        const uint16_t b1 = f32_to_bf16_rne(exp2f(sc[j + 1] - m_run));
         psum += bf16_to_f32(b0);
         psum += bf16_to_f32(b1);
         pw[j >> 1] = (uint32_t)b0 | ((uint32_t)b1 << 16);
@@ -221,10 +250,89 @@ __global__ __launch_bounds__(64 * HW * TW) void attn_partial_kernel(AttnArgs a) 
     }
     psum += __shfl_xor(psum, 16, 64);
     psum += __shfl_xor(psum, 32, 64);
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
+    l_run += psum;
+    const bf16x8_t pa = __builtin_bit_cast(bf16x8_t, u32x4{pw[0], pw[1], pw[2], pw[3]});
+    // V operand by transpose reads: in each 16-lane group, lane 4s+q addresses
+    // V[token][16n + 4q .. +3] of token perm(4g+s) (first read) or 16+perm(4g+s) (second
+    // read); lane t then holds V[those tokens][16n + t], i.e. B[k = 8g .. 8g+7][n = t], in the
+    // token order of this lane's P values.
+    const int ts = (lane & 15) >> 2, q4 = (lane & 3) * 4;
+    const uint16_t* vrow0 = tile + tile_row(4 * g + ts) * PP * 8 + VOFF + q4;
+    const uint16_t* vrow1 = vrow0 + 16 * PP * 8;
+#pragma unroll
+    for (int n = 0; n < NOUT; ++n) {
+      const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vrow0 + 16 * n));
+      const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vrow1 + 16 * n));
+      const bf16x8_t vb = __builtin_bit_cast(
+          bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[n], 0, 0, 0);
+    }
+    // transpose reads two output tiles ahead of their MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int n = 0; n < NOUT - 2; ++n) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+  };
 
-    // ---- rescale O rows (heads 4g..4g+3) and accumulate P . V ----
+  for (;;) {
+    for (; it < n_it; ++it) {
+      // chunks it+1 .. it+NST-2 were issued earlier and may still be in flight
+      wait_chunk(min(NST - 2, n_it - 1 - it));
+      // every wave is past its reads of buffer (it-1) % NST: refill it with chunk it+NST-1
+      if (it + NST - 1 < n_it) issue(it + NST - 1, (it + NST - 1) % NST);
+
+      const uint16_t* tile = s_tiles + (it % NST) * TILE;
+      const int cbase = tok_begin + it * kChunk * TW + tg * kChunk;
+
+      // ---- scores: S^T tiles for tokens [0,16) and [16,32) of the chunk ----
+      s0 = f32x4{0.f, 0.f, 0.f, 0.f};
+      s1 = f32x4{0.f, 0.f, 0.f, 0.f};
+      const uint16_t* k0 = tile + (tile_row(lane & 15) * PP + g) * 8;
+      const uint16_t* k1 = k0 + 16 * PP * 8;
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk) {
+        const bf16x8_t a0 = __builtin_bit_cast(bf16x8_t, lds_load16(k0 + kk * 32));
+        const bf16x8_t a1 = __builtin_bit_cast(bf16x8_t, lds_load16(k1 + kk * 32));
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qreg[kk], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, qreg[kk], s1, 0, 0, 0);
+      }
+      // keep operand reads two k-steps ahead of the MFMAs instead of all hoisted up front
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+      for (int kk = 0; kk < NKK - 2; ++kk) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+      const uint32_t vmask = s_valid[(cbase - tok_begin) >> 5];
+      int gq = g;
+      asm volatile("" : "+v"(gq));
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int bit = j < 4 ? tile_row(4 * gq + j) : 16 + tile_row(4 * gq + (j - 4));
+        const float raw = j < 4 ? s0[j] : s1[j - 4];
+        sc[j] = ((vmask >> bit) & 1u) ? raw * a.scale_log2 : -INFINITY;
+      }
+      cmax = sc[0];
+#pragma unroll
+      for (int j = 1; j < 8; ++j) cmax = fmaxf(cmax, sc[j]);
+      cmax = fmaxf(cmax, __shfl_xor(cmax, 16, 64));
+      cmax = fmaxf(cmax, __shfl_xor(cmax, 32, 64));
+      // Validity is per token, so every head of the wave agrees on whether m_run is -inf.
+      // While it is, O and l are exactly zero and the reference max can simply be set.
+      if (m_run == -INFINITY) m_run = cmax;
+      else if (__ballot(cmax > m_run + kRescaleSlack)) break;
+      finish_chunk(tile);
+    }
+    if (it >= n_it) break;
+    // rare path: move the reference max of the heads whose scores outgrew it
+    const float m_new = fmaxf(m_run, cmax);
+    const float alpha = exp2f(m_run - m_new);
+    l_run *= alpha;
+    m_run = m_new;
     float al[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) al[j] = __shfl(alpha, 4 * g + j, 64);
@@ -233,15 +341,8 @@ __global__ __launch_bounds__(64 * HW * TW) void attn_partial_kernel(AttnArgs a) 
 #pragma unroll
       for (int j = 0; j < 4; ++j) o[n][j] *= al[j];
     }
-    const bf16x8_t pa = __builtin_bit_cast(bf16x8_t, u32x4{pw[0], pw[1], pw[2], pw[3]});
-    const uint16_t* vt = s_vt + (lane & 15) * kVtRow + 4 * g;
-#pragma unroll
-    for (int n = 0; n < NOUT; ++n) {
-      const uint16_t* r = vt + n * 16 * kVtRow;
-      const u32x2 lo = lds_load8(r), hi = lds_load8(r + 16);
-      const bf16x8_t vb = __builtin_bit_cast(bf16x8_t, u32x4{lo[0], lo[1], hi[0], hi[1]});
-      o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[n], 0, 0, 0);
-    }
+    finish_chunk(s_tiles + (it % NST) * TILE);
+    ++it;
   }
 
   // ---- partial results of this (split, token group) ----
@@ -290,10 +391,10 @@ __global__ __launch_bounds__(DV / 4) void attn_combine_kernel(CombineArgs a) {
   *reinterpret_cast<f32x4*>(a.out + ((int64_t)unit * a.H + h) * DV + d) = r;
 }
 
-template <int DQK, int DV, int VOFF, int HW, int TW>
+template <int DQK, int DV, int VOFF, int HW, int TW, int NST>
 void launch_partial(const AttnArgs& args, hipStream_t stream) {
   const int nwg_pad = (args.n_wg + 7) & ~7;
-  hipLaunchKernelGGL((attn_partial_kernel<DQK, DV, VOFF, HW, TW>), dim3(nwg_pad),
+  hipLaunchKernelGGL((attn_partial_kernel<DQK, DV, VOFF, HW, TW, NST>), dim3(nwg_pad),
                      dim3(64 * HW * TW), 0, stream, args);
 }
 
@@ -311,8 +412,13 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
   if (units <= 0 || (int64_t)units * 256 > (1LL << 30)) return HISPARSE_ERR_INVALID_ARG;
   const int H = attn->q_heads;
   AttnPlan p{};
-  p.hw = H <= 16 ? 1 : (H <= 32 ? 2 : 4);
-  p.tw = is_mla(*attn) ? 1 : 4 / p.hw;
+  if (is_mla(*attn)) {  // up to 64 heads per workgroup (Q and O of 16 heads fill a wave)
+    p.hw = H <= 16 ? 1 : (H <= 32 ? 2 : 4);
+    p.tw = 1;
+  } else {
+    p.hw = H > 32 ? 4 : (H > 16 ? 2 : 1);
+    p.tw = 4 / p.hw;
+  }
   p.hb = (H + 16 * p.hw - 1) / (16 * p.hw);
   p.n_tok = top_k * attn->tokens_per_record;
   const int chunk = kChunk * p.tw;
@@ -321,12 +427,18 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
   if (attn->num_splits > 0) {
     splits = std::min(attn->num_splits, max_splits);
   } else {
+    // about one workgroup per CU, but at least four chunks per token group in every split so
+    // the load pipeline reaches steady state
     const int per_split = units * p.hb;
     splits = (kTargetWorkgroups + per_split - 1) / per_split;
-    splits = std::max(1, std::min(splits, max_splits));
+    const int min_work_splits = std::max(1, p.n_tok / (4 * chunk));
+    splits = std::max(1, std::min({splits, max_splits, min_work_splits}));
   }
+  const int max_split_tokens = std::min(kMaxSplitRecords * attn->tokens_per_record, kMaxSplitTokens);
+  splits = std::max(splits, (p.n_tok + max_split_tokens - 1) / max_split_tokens);
   const int per = (p.n_tok + splits - 1) / splits;
   p.split_tokens = (per + chunk - 1) / chunk * chunk;
+  if (p.split_tokens > max_split_tokens) p.split_tokens = max_split_tokens / chunk * chunk;
   p.n_wg_splits = (p.n_tok + p.split_tokens - 1) / p.split_tokens;
   p.n_parts = p.n_wg_splits * p.tw;
   const int64_t n_wg = (int64_t)units * p.n_wg_splits * p.hb;
@@ -368,15 +480,15 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
 
   if (is_mla(attn)) {
     switch (p.hw) {
-      case 1: launch_partial<576, 512, 0, 1, 1>(a, stream); break;
-      case 2: launch_partial<576, 512, 0, 2, 1>(a, stream); break;
-      default: launch_partial<576, 512, 0, 4, 1>(a, stream); break;
+      case 1: launch_partial<576, 512, 0, 1, 1, 2>(a, stream); break;
+      case 2: launch_partial<576, 512, 0, 2, 1, 4>(a, stream); break;
+      default: launch_partial<576, 512, 0, 4, 1, 4>(a, stream); break;
     }
   } else {
     switch (p.hw) {
-      case 1: launch_partial<128, 128, 128, 1, 4>(a, stream); break;
-      case 2: launch_partial<128, 128, 128, 2, 2>(a, stream); break;
-      default: launch_partial<128, 128, 128, 4, 1>(a, stream); break;
+      case 1: launch_partial<128, 128, 128, 1, 4, 2>(a, stream); break;
+      case 2: launch_partial<128, 128, 128, 2, 2, 3>(a, stream); break;
+      default: launch_partial<128, 128, 128, 4, 1, 4>(a, stream); break;
     }
   }
   hipError_t e = hipGetLastError();
