@@ -1,0 +1,102 @@
+"""The C ABI without a GPU: the library loads, exports every function include/hisparse.h
+declares, and its pure-host validation accepts the five workloads and rejects bad descriptors."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import workload as W
+from paper_2608_07009_amd import hisparse as hs
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "hisparse.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(hisparse_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_what_binding_lists():
+    assert declared_functions() == sorted(hs.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(hs.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def desc_for(w, **kw):
+    d = dict(num_requests=w.num_requests, num_layers=w.num_layers,
+             units_per_request=w.units_per_request, capacity=w.B, num_records=w.L, top_k=w.k,
+             record_bytes=w.record_bytes, share_group=w.share_group, fetch=0, host_memory=0,
+             transfer_block_bytes=0, reserved=0)
+    d.update(kw)
+    return hs.CacheDesc(**d)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_workload_descriptors_are_valid(cfg):
+    w = W.workload(cfg)
+    assert hs.hisparse_validate_desc(desc_for(w)) == hs.HISPARSE_OK
+    ad = hs.AttnDesc(w.q_heads, w.d_qk, w.d_v, w.v_offset, w.tokens_per_record, 0, w.scale, 0)
+    assert hs.hisparse_validate_attn(w.record_bytes, w.k, ad) == hs.HISPARSE_OK
+    assert hs.hisparse_decode_workspace_bytes(w.units, w.k, w.record_bytes, ad) > 0
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("capacity", 100, hs.HISPARSE_ERR_INVALID_ARG),          # B < k (Section 3.2 needs B >= k)
+    ("top_k", 0, hs.HISPARSE_ERR_INVALID_ARG),
+    ("top_k", 5000, hs.HISPARSE_ERR_INVALID_ARG),
+    ("record_bytes", 1000, hs.HISPARSE_ERR_INVALID_ARG),     # not a multiple of 16
+    ("num_records", 0, hs.HISPARSE_ERR_INVALID_ARG),
+    ("share_group", 0, hs.HISPARSE_ERR_INVALID_ARG),
+    ("num_requests", 0, hs.HISPARSE_ERR_INVALID_ARG),
+    ("units_per_request", 70000, hs.HISPARSE_ERR_INVALID_ARG),
+    ("fetch", 1, hs.HISPARSE_ERR_UNSUPPORTED),
+    ("host_memory", 7, hs.HISPARSE_ERR_INVALID_ARG),
+    ("transfer_block_bytes", 48, hs.HISPARSE_ERR_INVALID_ARG),
+    ("reserved", 1, hs.HISPARSE_ERR_INVALID_ARG),
+    ("capacity", 20000, hs.HISPARSE_ERR_INVALID_ARG),        # beyond the LDS-resident maximum
+])
+def test_invalid_descriptors(field, value, status):
+    w = W.workload(1)
+    assert hs.hisparse_validate_desc(desc_for(w, **{field: value})) == status
+
+
+@pytest.mark.parametrize("change,status", [
+    (dict(d_qk=256), hs.HISPARSE_ERR_UNSUPPORTED),
+    (dict(tokens_per_record=3), hs.HISPARSE_ERR_INVALID_ARG),
+    (dict(q_heads=0), hs.HISPARSE_ERR_INVALID_ARG),
+    (dict(scale=0.0), hs.HISPARSE_ERR_INVALID_ARG),
+    (dict(num_splits=-1), hs.HISPARSE_ERR_INVALID_ARG),
+    (dict(reserved=2), hs.HISPARSE_ERR_INVALID_ARG),
+])
+def test_invalid_attention_descriptors(change, status):
+    w = W.workload(2)
+    d = dict(q_heads=w.q_heads, d_qk=w.d_qk, d_v=w.d_v, v_offset=w.v_offset,
+             tokens_per_record=w.tokens_per_record, num_splits=0, scale=w.scale, reserved=0)
+    d.update(change)
+    assert hs.hisparse_validate_attn(w.record_bytes, w.k, hs.AttnDesc(**d)) == status
+    assert hs.hisparse_decode_workspace_bytes(w.units, w.k, w.record_bytes, hs.AttnDesc(**d)) == 0
+
+
+def test_record_too_small_for_attention():
+    ad = hs.AttnDesc(16, 576, 512, 0, 1, 0, 0.07, 0)
+    assert hs.hisparse_validate_attn(512, 64, ad) == hs.HISPARSE_ERR_INVALID_ARG
+
+
+def test_status_strings():
+    for code, name in [(0, "HISPARSE_OK"), (-1, "HISPARSE_ERR_INVALID_ARG"),
+                       (-5, "HISPARSE_ERR_BAD_SELECTION")]:
+        assert hs.hisparse_status_string(code) == name
+
+
+def test_create_fails_cleanly_without_a_device_or_with_bad_args():
+    w = W.workload(1)
+    with pytest.raises(hs.HisparseError) as e:
+        hs.hisparse_cache_create(desc_for(w, capacity=1))
+    assert e.value.status == hs.HISPARSE_ERR_INVALID_ARG
