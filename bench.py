@@ -2,15 +2,18 @@
 """Benchmark of the HiSparse decode hot path on one MI355X.
 
 One step = one decode step of every layer: resolve (phases 1-3, 5) + miss fetch (phase 4) for
-each anchor layer, exact-prefetch replays for shared layers (side stream), and sparse decode
-attention for every layer, over seeded synthetic inputs already resident in HBM / pinned host
-memory. Default workload: 32 requests x 8 layers, 32K-token context, k=2048, B=4096 slots,
-128 latent-attention heads.
+each anchor layer, exact-prefetch replays into shared layers on a side stream, and sparse
+decode attention for every layer, over seeded synthetic inputs already resident in HBM and
+pinned host memory. Default workload: 32 requests x 8 layers, 32K-token context, k=2048,
+B=4096 slots, 128 latent-attention heads.
 
 Prints one JSON line: value = selections served per second (layers x units x k per step over
-wall time), with the miss-fetch GB/s against the in-process pinned hipMemcpy H2D peak, decode
-tokens/s, per-kernel event timings, the roofline of the dominant kernel and the CPU oracle
-baseline.
+the wall time of the timed steps), with miss-fetch GB/s against the in-process pinned
+hipMemcpy H2D peak, decode tokens/s, per-kernel HIP-event timings, the roofline of the dominant
+kernel, the same step replayed from a captured HIP graph, and the CPU oracle baseline.
+
+The timed steps are launched eagerly with every argument precomputed, so the host stays ahead
+of the GPU and each kernel's start/end events bracket the kernel itself.
 """
 from __future__ import annotations
 
@@ -40,11 +43,12 @@ def parse():
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
-    ap.add_argument("--fetch", choices=["zero_copy", "none"], default="zero_copy")
+    ap.add_argument("--fetch", choices=["zero_copy", "none", "sdma"], default="zero_copy")
     ap.add_argument("--host-memory", choices=["coherent", "noncoherent", "uncached"],
                     default="coherent")
     ap.add_argument("--transfer-block", type=int, default=0)
     ap.add_argument("--splits", type=int, default=0, help="attention splits (0 = auto)")
+    ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-sweep", action="store_true")
@@ -52,63 +56,71 @@ def parse():
 
 
 class Hip:
-    """Raw hipMemcpyAsync for the pinned H2D sweep."""
+    """Raw HIP runtime calls (the runtime torch already loaded)."""
 
     def __init__(self):
-        self.lib = ctypes.CDLL("libamdhip64.so")
-        self.lib.hipMemcpyAsync.restype = ctypes.c_int
-        self.lib.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
-                                            ctypes.c_int, ctypes.c_void_p]
+        L = ctypes.CDLL("libamdhip64.so")
+        V, P = ctypes.c_void_p, ctypes.POINTER(ctypes.c_void_p)
+        L.hipEventCreateWithFlags.argtypes = [P, ctypes.c_uint]
+        L.hipEventRecord.argtypes = [V, V]
+        L.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), V, V]
+        L.hipEventSynchronize.argtypes = [V]
+        L.hipEventDestroy.argtypes = [V]
+        L.hipStreamWaitEvent.argtypes = [V, V, ctypes.c_uint]
+        L.hipMemcpyAsync.argtypes = [V, V, ctypes.c_size_t, ctypes.c_int, V]
+        for f in ("hipEventCreateWithFlags", "hipEventRecord", "hipEventElapsedTime",
+                  "hipEventSynchronize", "hipEventDestroy", "hipStreamWaitEvent",
+                  "hipMemcpyAsync"):
+            getattr(L, f).restype = ctypes.c_int
+        self.L = L
 
-    def h2d_async(self, dst: int, src: int, n: int, stream: int) -> None:
-        rc = self.lib.hipMemcpyAsync(dst, src, n, 1, stream)  # hipMemcpyHostToDevice
+    def event(self, timing: bool = True) -> int:
+        e = ctypes.c_void_p()
+        rc = self.L.hipEventCreateWithFlags(ctypes.byref(e), 0 if timing else 0x2)
         if rc != 0:
-            raise RuntimeError(f"hipMemcpyAsync failed ({rc})")
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
+        return e.value
+
+    def ms(self, e0: int, e1: int) -> float:
+        out = ctypes.c_float()
+        rc = self.L.hipEventElapsedTime(ctypes.byref(out), e0, e1)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return out.value
 
 
-def pinned_sweep(torch, host_ptr: int, host_bytes: int, dev, stream) -> dict:
+def pinned_sweep(torch, hip: Hip, host_ptr: int, host_bytes: int, dev, stream: int) -> dict:
     """H2D bandwidth of hipMemcpyAsync from the library's pinned pool, 4 KiB .. 1 GiB."""
-    hip = Hip()
     top = min(1 << 30, host_bytes)
     dst = torch.empty(top, dtype=torch.uint8, device=dev)
+    e0, e1 = hip.event(), hip.event()
     res = {}
     size = 4096
     while size <= top:
         reps = max(3, min(2000, (256 << 20) // size))
-        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        hip.h2d_async(dst.data_ptr(), host_ptr, size, stream.cuda_stream)  # warm
-        s.record(stream)
+        hip.L.hipMemcpyAsync(dst.data_ptr(), host_ptr, size, 1, stream)  # warm
+        hip.L.hipEventRecord(e0, stream)
         for _ in range(reps):
-            hip.h2d_async(dst.data_ptr(), host_ptr, size, stream.cuda_stream)
-        e.record(stream)
-        e.synchronize()
-        res[size] = size * reps / (s.elapsed_time(e) * 1e-3) / 1e9
+            if hip.L.hipMemcpyAsync(dst.data_ptr(), host_ptr, size, 1, stream) != 0:
+                raise RuntimeError("hipMemcpyAsync failed")
+        hip.L.hipEventRecord(e1, stream)
+        hip.L.hipEventSynchronize(e1)
+        res[size] = size * reps / (hip.ms(e0, e1) * 1e-3) / 1e9
         size *= 4
     del dst
     return res
 
 
-class Events:
-    """Per-kernel HIP event pairs recorded on the kernel's own stream."""
-
-    def __init__(self, torch):
-        self.torch = torch
-        self.spans = []  # (name, start, end)
-
-    def span(self, name, stream, fn):
-        s = self.torch.cuda.Event(enable_timing=True)
-        e = self.torch.cuda.Event(enable_timing=True)
-        s.record(stream)
-        fn()
-        e.record(stream)
-        self.spans.append((name, s, e))
-
-    def totals(self) -> dict:
-        out = {}
-        for name, s, e in self.spans:
-            t, n = out.get(name, (0.0, 0))
-            out[name] = (t + s.elapsed_time(e) * 1e-3, n + 1)
-        return out
+def union_length(intervals) -> float:
+    total, end = 0.0, None
+    for a, b in sorted(intervals):
+        if end is None or a > end:
+            total += b - a
+            end = b
+        elif b > end:
+            total += b - end
+            end = b
+    return total
 
 
 def cpu_baseline(w, cache, sel_host, budget_s: float) -> dict:
@@ -162,7 +174,8 @@ def main() -> int:
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}))
         return 1
-    hs.lib()  # fails loudly if the HIP library is missing
+    L = hs.lib()  # fails loudly if the HIP library is missing
+    hip = Hip()
     w0 = W.workload(args.config)
     w = W.fit_pinned(w0)
     steps_needed = args.warmup + args.steps
@@ -171,9 +184,12 @@ def main() -> int:
                           f"{w.steps} steps"}))
         return 2
     dev = torch.device("cuda:0")
-    main_s = torch.cuda.current_stream()
-    side_s = torch.cuda.Stream()
-    fetch = hs.HISPARSE_FETCH_NONE if args.fetch == "none" else hs.HISPARSE_FETCH_ZERO_COPY
+    main_t = torch.cuda.Stream()  # a capturable stream (not the legacy null stream)
+    torch.cuda.set_stream(main_t)
+    side_t = torch.cuda.Stream()
+    main_s, side_s = main_t.cuda_stream, side_t.cuda_stream
+    fetch = {"none": hs.HISPARSE_FETCH_NONE, "sdma": hs.HISPARSE_FETCH_SDMA,
+             "zero_copy": hs.HISPARSE_FETCH_ZERO_COPY}[args.fetch]
     hmem = {"coherent": hs.HISPARSE_HOST_COHERENT, "noncoherent": hs.HISPARSE_HOST_NONCOHERENT,
             "uncached": hs.HISPARSE_HOST_UNCACHED}[args.host_memory]
 
@@ -190,74 +206,119 @@ def main() -> int:
     log(f"{w.name}: layers {w.num_layers} (of {w0.num_layers}), host pool "
         f"{w.host_pool_bytes() / 2**30:.1f} GiB, set up in {time.time() - t0:.1f}s")
 
-    U, k = w.units, w.k
+    U, k, G = w.units, w.k, w.share_group
     slots = torch.empty((w.num_layers, U, k), dtype=torch.int32, device=dev)
     counts = torch.zeros((steps_needed, w.num_layers, U, 2), dtype=torch.int32, device=dev)
     ad = hs.AttnDesc(w.q_heads, w.d_qk, w.d_v, w.v_offset, w.tokens_per_record, args.splits,
                      w.scale, 0)
+    ad_ref = ctypes.byref(ad)
     ws_bytes = hs.hisparse_decode_workspace_bytes(U, k, w.record_bytes, ad)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     out = torch.empty((w.num_layers, U, w.q_heads, w.d_v), dtype=torch.float32, device=dev)
     h = cache.handle
-    G = w.share_group
 
-    def step(t: int, ev: Events | None):
-        def span(name, stream, fn):
-            if ev is None:
-                fn()
+    # every pointer of every step, precomputed
+    sel_p = [[sel[t, (a // G) * U:(a // G + 1) * U].data_ptr() for a in range(w.num_layers)]
+             for t in range(steps_needed)]
+    cnt_p = [[counts[t, a].data_ptr() for a in range(w.num_layers)] for t in range(steps_needed)]
+    slot_p = [slots[a].data_ptr() for a in range(w.num_layers)]
+    q_p = [[q_all[v, l].data_ptr() for l in range(w.num_layers)] for v in range(n_qv)]
+    out_p = [out[l].data_ptr() for l in range(w.num_layers)]
+    ws_p = ws.data_ptr()
+    groups = [(a, list(range(a + 1, min(a + G, w.num_layers)))) for a in w.anchors]
+    f_tables, f_fetch = L.hisparse_resolve_tables, L.hisparse_fetch
+    f_prefetch, f_decode = L.hisparse_prefetch_layer, L.hisparse_sparse_decode
+    rec = hip.L.hipEventRecord
+    wait = hip.L.hipStreamWaitEvent
+    sync_events = [hip.event(timing=False) for _ in range(2 * G)]
+
+    def check(rc, what):
+        if rc != 0:
+            raise RuntimeError(f"{what} -> {hs.hisparse_status_string(rc)}")
+
+    def step(t, ev=None, spans=None, sel_override=None, q_override=None):
+        """Enqueue decode step t. With ev (a list of timing events, consumed in order) every
+        kernel call is bracketed by events and (name, e0, e1) appended to spans."""
+        qv = q_override or q_p[t % n_qv]
+        for a, shared in groups:
+            sp = sel_override[a] if sel_override else sel_p[t][a]
+            cp = 0 if sel_override else cnt_p[t][a]
+            if ev is not None:
+                e0, e1 = ev.pop(), ev.pop()
+                rec(e0, main_s)
+                check(f_tables(h, a, sp, slot_p[a], cp or None, main_s), "resolve_tables")
+                rec(e1, main_s)
+                spans.append(("resolve_tables", e0, e1))
             else:
-                ev.span(name, stream, fn)
-
-        qv = q_all[t % n_qv]
-        for a in w.anchors:
-            ai = a // G
-            sel_a = sel[t, ai * U:(ai + 1) * U]
-            span("resolve_tables", main_s,
-                 lambda: hs.hisparse_resolve_tables(h, a, sel_a, slots[a], counts[t, a], main_s))
-            shared = list(range(a + 1, min(a + G, w.num_layers)))
-            done = {}
+                check(f_tables(h, a, sp, slot_p[a], cp or None, main_s), "resolve_tables")
             if shared:
-                fork = torch.cuda.Event()
-                fork.record(main_s)
-                side_s.wait_event(fork)
-                for s in shared:
-                    span("prefetch_replay", side_s,
-                         lambda s=s: hs.hisparse_prefetch_layer(h, a, s, side_s))
-                    done[s] = torch.cuda.Event()
-                    done[s].record(side_s)
-            span("fetch", main_s, lambda: hs.hisparse_fetch(h, a, main_s))
-            span("sparse_decode", main_s,
-                 lambda: hs.hisparse_sparse_decode(h, a, qv[a], slots[a], out[a], ad, ws,
-                                                   ws_bytes, main_s))
-            for s in shared:
-                main_s.wait_event(done[s])
-                span("sparse_decode", main_s,
-                     lambda s=s: hs.hisparse_sparse_decode(h, s, qv[s], slots[a], out[s], ad, ws,
-                                                           ws_bytes, main_s))
+                fork = sync_events[0]
+                rec(fork, main_s)
+                wait(side_s, fork, 0)
+                for i, s in enumerate(shared):
+                    if ev is not None:
+                        e0, e1 = ev.pop(), ev.pop()
+                        rec(e0, side_s)
+                        check(f_prefetch(h, a, s, side_s), "prefetch_layer")
+                        rec(e1, side_s)
+                        spans.append(("prefetch_replay", e0, e1))
+                    else:
+                        check(f_prefetch(h, a, s, side_s), "prefetch_layer")
+                    rec(sync_events[1 + i], side_s)
+            if ev is not None:
+                e0, e1, e2 = ev.pop(), ev.pop(), ev.pop()
+                rec(e0, main_s)
+                check(f_fetch(h, a, main_s), "fetch")
+                rec(e1, main_s)
+                check(f_decode(h, a, qv[a], slot_p[a], out_p[a], ad_ref, ws_p, ws_bytes, main_s),
+                      "sparse_decode")
+                rec(e2, main_s)
+                spans.append(("fetch", e0, e1))
+                spans.append(("sparse_decode", e1, e2))
+            else:
+                check(f_fetch(h, a, main_s), "fetch")
+                check(f_decode(h, a, qv[a], slot_p[a], out_p[a], ad_ref, ws_p, ws_bytes, main_s),
+                      "sparse_decode")
+            for i, s in enumerate(shared):
+                wait(main_s, sync_events[1 + i], 0)
+                if ev is not None:
+                    e0, e1 = ev.pop(), ev.pop()
+                    rec(e0, main_s)
+                    check(f_decode(h, s, qv[s], slot_p[a], out_p[s], ad_ref, ws_p, ws_bytes,
+                                   main_s), "sparse_decode")
+                    rec(e1, main_s)
+                    spans.append(("sparse_decode", e0, e1))
+                else:
+                    check(f_decode(h, s, qv[s], slot_p[a], out_p[s], ad_ref, ws_p, ws_bytes,
+                                   main_s), "sparse_decode")
 
     # pinned H2D sweep over the same pool (hipMemcpyAsync), before the timed region
     sweep = {}
     if not args.no_sweep:
-        sweep = pinned_sweep(torch, *cache.host_pool(0), dev, main_s)
+        sweep = pinned_sweep(torch, hip, *cache.host_pool(0), dev, main_s)
         log("pinned H2D sweep GB/s: " + ", ".join(f"{s >> 10}K:{v:.1f}" for s, v in sweep.items()))
     pinned_peak = max(sweep.values()) if sweep else None
 
     # warmup (step 0 is the cold step)
     torch.cuda.synchronize()
     tc = time.perf_counter()
-    step(0, None)
+    step(0)
     torch.cuda.synchronize()
     cold_ms = (time.perf_counter() - tc) * 1e3
     for t in range(1, args.warmup):
-        step(t, None)
+        step(t)
     torch.cuda.synchronize()
 
     # timed region
-    ev = Events(torch)
+    per_step_events = sum(6 + 5 * len(sh) for _, sh in groups)
+    events = [hip.event() for _ in range(per_step_events * args.steps + 1)]
+    ref = events.pop()
+    spans = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    rec(ref, main_s)
     for t in range(args.warmup, steps_needed):
-        step(t, ev)
+        step(t, events, spans)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     st, info = cache.check_errors()
@@ -265,21 +326,33 @@ def main() -> int:
         print(json.dumps({"error": f"device-side selection error {info}"}))
         return 1
 
-    tot = ev.totals()
+    tot = {}
+    io_intervals = []
+    for name, e0, e1 in spans:
+        d = hip.ms(e0, e1) * 1e-3
+        t_sum, n = tot.get(name, (0.0, 0))
+        tot[name] = (t_sum + d, n + 1)
+        if name in ("fetch", "prefetch_replay"):
+            io_intervals.append((hip.ms(ref, e0) * 1e-3, hip.ms(ref, e1) * 1e-3))
+    for e in events:
+        hip.L.hipEventDestroy(e)
+    for _, e0, e1 in spans:
+        hip.L.hipEventDestroy(e0)
+        hip.L.hipEventDestroy(e1)
+    hip.L.hipEventDestroy(ref)
+
     c = counts[args.warmup:steps_needed].cpu().numpy().astype(np.int64)  # [K][layers][U][2]
     K = args.steps
     anchor_calls = K * len(w.anchors)
     misses_anchor = int(c[:, w.anchors, :, 1].sum())
     hits_anchor = int(c[:, w.anchors, :, 0].sum())
-    shared_per_anchor = {a: len(range(a + 1, min(a + G, w.num_layers))) for a in w.anchors}
-    misses_replay = int(sum(c[:, a, :, 1].sum() * n for a, n in shared_per_anchor.items()))
+    misses_replay = int(sum(c[:, a, :, 1].sum() * len(sh) for a, sh in groups))
     R = w.record_bytes
     served = K * w.num_layers * U * k
     value = served / wall
 
     def kernel(name):
-        t, n = tot.get(name, (0.0, 0))
-        return t, n
+        return tot.get(name, (0.0, 0))
 
     t_tab, n_tab = kernel("resolve_tables")
     t_fet, n_fet = kernel("fetch")
@@ -287,6 +360,7 @@ def main() -> int:
     t_att, n_att = kernel("sparse_decode")
     fetch_bytes = misses_anchor * R
     replay_bytes = misses_replay * R
+    moves_data = fetch != hs.HISPARSE_FETCH_NONE
     kernels = {}
     # resolve tables: integer metadata work per unit (algorithmic bytes):
     # sel 4k + page-table probes 4k + slot outputs 4k + recency index read+write 8B
@@ -297,11 +371,11 @@ def main() -> int:
             "launches": n_tab, "avg_us": t_tab / n_tab * 1e6, "bound": "latency",
             "hbm_GBps": tab_bytes / t_tab / 1e9,
             "selections_per_s_no_io": anchor_calls * U * k / t_tab}
-    if n_fet and fetch != hs.HISPARSE_FETCH_NONE:
+    if n_fet and moves_data:
         kernels["fetch"] = {"launches": n_fet, "avg_us": t_fet / n_fet * 1e6,
                             "bytes_per_launch": fetch_bytes / n_fet,
                             "GBps": fetch_bytes / t_fet / 1e9}
-    if n_rep and fetch != hs.HISPARSE_FETCH_NONE:
+    if n_rep and moves_data:
         kernels["prefetch_replay"] = {"launches": n_rep, "avg_us": t_rep / n_rep * 1e6,
                                       "bytes_per_launch": replay_bytes / n_rep,
                                       "GBps": replay_bytes / t_rep / 1e9}
@@ -320,8 +394,8 @@ def main() -> int:
             "mfma_frac": att_flops_call / a_time / 1e12 / MFMA_BF16_PEAK_TFLOPS}
 
     # dominant kernel by total event time
-    totals = {"resolve_tables": t_tab, "fetch": t_fet, "prefetch_replay": t_rep,
-              "sparse_decode": t_att}
+    totals = {"resolve_tables": t_tab, "fetch": t_fet if moves_data else 0.0,
+              "prefetch_replay": t_rep if moves_data else 0.0, "sparse_decode": t_att}
     dom = max(totals, key=totals.get)
     if dom in ("fetch", "prefetch_replay"):
         kd = kernels[dom]
@@ -347,7 +421,43 @@ def main() -> int:
         roof = {"kernel": dom, "bound": "hbm", "achieved": kd["hbm_GBps"], "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": kd["hbm_GBps"] / HBM_PEAK_GBPS, "traffic": None}
 
-    miss_gbps = (fetch_bytes + replay_bytes) / (t_fet + t_rep) / 1e9 if (t_fet + t_rep) else None
+    io_busy = union_length(io_intervals)
+    miss_gbps = (fetch_bytes + replay_bytes) / io_busy / 1e9 if (io_busy and moves_data) else None
+
+    # the same steps replayed from one captured HIP graph (cold reset, same warmup)
+    graph = None
+    if not args.no_graph and fetch != hs.HISPARSE_FETCH_SDMA:
+        stage_sel = torch.empty_like(sel[0])
+        stage_q = torch.empty_like(q_all[0])
+        tidx = torch.zeros(1, dtype=torch.int64, device=dev)
+        sel_stage_p = [stage_sel[(a // G) * U:(a // G + 1) * U].data_ptr()
+                       for a in range(w.num_layers)]
+        q_stage_p = [stage_q[l].data_ptr() for l in range(w.num_layers)]
+        g = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=main_t):
+            stage_sel.copy_(sel.index_select(0, tidx).squeeze(0))
+            stage_q.copy_(q_all.index_select(0, torch.remainder(tidx, n_qv)).squeeze(0))
+            tidx.add_(1)
+            step(0, sel_override=sel_stage_p, q_override=q_stage_p)
+        torch.cuda.synchronize()
+        hs.hisparse_reset(h, main_s)
+        tidx.zero_()
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        tg = time.perf_counter()
+        for _ in range(args.steps):
+            g.replay()
+        torch.cuda.synchronize()
+        gwall = time.perf_counter() - tg
+        graph = {"ms_per_step": gwall / K * 1e3, "selections_per_s": served / gwall,
+                 "decode_tokens_per_s": w.num_requests * K / gwall}
+        st, info = cache.check_errors()
+        if st != hs.HISPARSE_OK:
+            print(json.dumps({"error": f"device-side selection error in graph replay {info}"}))
+            return 1
+
     result = {
         "metric": "resolved selections/s + miss-fetch GB/s (% host-link peak), decode tokens/s",
         "value": value,
@@ -377,11 +487,14 @@ def main() -> int:
         "cold_step_ms": cold_ms,
         "kernels": kernels,
         "roofline": roof,
+        "graph_replay": graph,
         "hbm_footprint_GiB": (w0.num_layers * U * w.B * R) / 2**30,
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle baseline")
         result["cpu_baseline"] = cpu_baseline(w, cache, sel_host[:, :U], args.cpu_budget)
+    for e in sync_events:
+        hip.L.hipEventDestroy(e)
     cache.close()
     print(json.dumps(result), flush=True)
     return 0

@@ -24,7 +24,9 @@
  *     writes them on the given stream and keeps no reference after the call returns.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *   - Calls marked [async] enqueue GPU work on `stream`, never synchronise the host, allocate
- *     nothing and can be captured in a HIP graph. Calls marked [sync] block the host.
+ *     nothing and can be captured in a HIP graph (with HISPARSE_FETCH_SDMA, the calls that
+ *     fetch synchronise `stream` once to read the miss plan back, and cannot be captured).
+ *     Calls marked [sync] block the host.
  *   - Every call returns HISPARSE_OK or a negative hisparse_status_t; an argument error is
  *     reported before any work is enqueued, and leaves all state untouched.
  *   - Data errors found on the device (a selection entry >= L, or a repeated entry within one
@@ -61,6 +63,10 @@ typedef enum {
   /* GPU threads load the missed records straight from mapped pinned host memory with 16-byte
    * vector loads and store them into their slots: the GPU-assisted IO the paper adopts. */
   HISPARSE_FETCH_ZERO_COPY = 0,
+  /* The host reads the miss plan back (a stream synchronisation) and issues one batched DMA
+   * copy (hipMemcpyBatchAsync) of the missed records. Not capturable in a HIP graph: calls
+   * that fetch return HISPARSE_ERR_UNSUPPORTED while `stream` is capturing. */
+  HISPARSE_FETCH_SDMA = 1,
   /* Timing mode (Section 4.6's "no-IO oracle"): tables and slot outputs are exact, but no
    * record is copied, so the cache holds stale data and attention outputs are not valid. */
   HISPARSE_FETCH_NONE = 2

@@ -1,5 +1,6 @@
 // C ABI of the HiSparse library: descriptor validation, allocation of the host pool, GPU
 // cache and resolve state, and the enqueueing entry points (declared in include/hisparse.h).
+#include <dlfcn.h>
 #include <string.h>
 
 #include <algorithm>
@@ -14,6 +15,16 @@ using hisparse::kMaxTopK;
 namespace {
 
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+// hipMemcpyBatchAsync exists only in newer HIP runtimes; the process may run an older one
+// (whichever libamdhip64 was loaded first), so it is looked up at run time.
+typedef hipError_t (*batch_copy_fn)(void**, void**, size_t*, size_t, hipMemcpyAttributes*,
+                                    size_t*, size_t, size_t*, hipStream_t);
+batch_copy_fn batch_copy() {
+  static batch_copy_fn fn =
+      reinterpret_cast<batch_copy_fn>(dlsym(RTLD_DEFAULT, "hipMemcpyBatchAsync"));
+  return fn;
+}
 
 bool is_anchor(const hisparse_cache* c, int32_t layer) {
   return layer >= 0 && layer < c->desc.num_layers && layer % c->desc.share_group == 0;
@@ -44,6 +55,8 @@ void free_all(hisparse_cache* c) {
     (void)hipFree(a.counts);
   }
   if (c->err) (void)hipFree(c->err);
+  if (c->h_plan_count) (void)hipHostFree(c->h_plan_count);
+  if (c->h_plan) (void)hipHostFree(c->h_plan);
   (void)hipSetDevice(prev);
   delete c;
 }
@@ -101,7 +114,8 @@ hisparse_status_t hisparse_validate_desc(const hisparse_cache_desc_t* d) {
   if (d->record_bytes < 16 || d->record_bytes > kMaxRecordBytes || d->record_bytes % 16 != 0)
     return HISPARSE_ERR_INVALID_ARG;
   if (d->share_group < 1) return HISPARSE_ERR_INVALID_ARG;
-  if (d->fetch != HISPARSE_FETCH_ZERO_COPY && d->fetch != HISPARSE_FETCH_NONE)
+  if (d->fetch != HISPARSE_FETCH_ZERO_COPY && d->fetch != HISPARSE_FETCH_SDMA &&
+      d->fetch != HISPARSE_FETCH_NONE)
     return HISPARSE_ERR_UNSUPPORTED;
   if (d->host_memory < HISPARSE_HOST_COHERENT || d->host_memory > HISPARSE_HOST_UNCACHED)
     return HISPARSE_ERR_INVALID_ARG;
@@ -199,6 +213,18 @@ hisparse_status_t hisparse_cache_create(const hisparse_cache_desc_t* desc, int32
     if ((st = dmalloc(&an.counts, U * 2 * 4)) != HISPARSE_OK) break;
   }
   if (st == HISPARSE_OK) st = dmalloc(&c->err, hisparse::kErrWords * 4);
+  if (st == HISPARSE_OK && desc->fetch == HISPARSE_FETCH_SDMA) {
+    if (hipHostMalloc(reinterpret_cast<void**>(&c->h_plan_count), U * 4, 0) != hipSuccess ||
+        hipHostMalloc(reinterpret_cast<void**>(&c->h_plan), U * K * sizeof(int2), 0) !=
+            hipSuccess) {
+      (void)hipGetLastError();
+      st = HISPARSE_ERR_OOM;
+    } else {
+      c->dma_dst.resize(U * K);
+      c->dma_src.resize(U * K);
+      c->dma_size.resize(U * K);
+    }
+  }
   if (st == HISPARSE_OK) {
     if (hipMemset(c->err, 0, hisparse::kErrWords * 4) != hipSuccess) st = HISPARSE_ERR_HIP;
     for (int l = 0; l < desc->num_layers && st == HISPARSE_OK; ++l)
@@ -282,6 +308,54 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
                                 hipStream_t stream) {
   if (c->desc.fetch == HISPARSE_FETCH_NONE) return HISPARSE_OK;
   auto& an = c->anchors[anchor / c->desc.share_group];
+  if (c->desc.fetch == HISPARSE_FETCH_SDMA) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &cs) != hipSuccess) return HISPARSE_ERR_HIP;
+    if (cs != hipStreamCaptureStatusNone) return HISPARSE_ERR_UNSUPPORTED;
+    const size_t U = (size_t)c->units, K = (size_t)c->desc.top_k;
+    if (hipMemcpyAsync(c->h_plan_count, an.plan_count, U * 4, hipMemcpyDeviceToHost, stream) !=
+            hipSuccess ||
+        hipMemcpyAsync(c->h_plan, an.plan, U * K * sizeof(int2), hipMemcpyDeviceToHost,
+                       stream) != hipSuccess ||
+        hipStreamSynchronize(stream) != hipSuccess)
+      return HISPARSE_ERR_HIP;
+    const size_t R = (size_t)c->desc.record_bytes, L = (size_t)c->desc.num_records;
+    const size_t B = (size_t)c->desc.capacity;
+    uint8_t* host = reinterpret_cast<uint8_t*>(c->host[target]);
+    uint8_t* cache = c->cache[target];
+    size_t n = 0;
+    for (size_t u = 0; u < U; ++u) {
+      const int2* pl = c->h_plan + u * K;
+      for (int32_t i = 0; i < c->h_plan_count[u]; ++i) {
+        uint8_t* src = host + (u * L + (size_t)pl[i].x) * R;
+        uint8_t* dst = cache + (u * B + (size_t)pl[i].y) * R;
+        if (n && (uint8_t*)c->dma_src[n - 1] + c->dma_size[n - 1] == src &&
+            (uint8_t*)c->dma_dst[n - 1] + c->dma_size[n - 1] == dst) {
+          c->dma_size[n - 1] += R;  // adjacent positions into adjacent slots: one copy
+        } else {
+          c->dma_src[n] = src;
+          c->dma_dst[n] = dst;
+          c->dma_size[n] = R;
+          ++n;
+        }
+      }
+    }
+    if (n == 0) return HISPARSE_OK;
+    if (batch_copy_fn fn = batch_copy()) {
+      size_t fail = 0;
+      if (fn(c->dma_dst.data(), c->dma_src.data(), c->dma_size.data(), n, nullptr, nullptr, 0,
+             &fail, stream) != hipSuccess) {
+        (void)hipGetLastError();
+        return HISPARSE_ERR_HIP;
+      }
+      return HISPARSE_OK;
+    }
+    for (size_t i = 0; i < n; ++i)
+      if (hipMemcpyAsync(c->dma_dst[i], c->dma_src[i], c->dma_size[i], hipMemcpyHostToDevice,
+                         stream) != hipSuccess)
+        return HISPARSE_ERR_HIP;
+    return HISPARSE_OK;
+  }
   hisparse::FetchArgs f{};
   f.plan = an.plan;
   f.plan_count = an.plan_count;

@@ -64,7 +64,6 @@ __device__ inline uint16_t f32_to_bf16_rne(float f) {
 __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
 __device__ inline u32x4 lds_load16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
-__device__ inline void lds_store16(uint16_t* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;

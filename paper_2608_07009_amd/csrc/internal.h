@@ -98,4 +98,9 @@ struct hisparse_cache {
   };
   std::vector<Anchor> anchors;   // per anchor layer (layer / share_group)
   int32_t* err = nullptr;        // device error word
+  // HISPARSE_FETCH_SDMA: pinned readback of a plan and the host-side copy lists
+  int32_t* h_plan_count = nullptr;
+  int2* h_plan = nullptr;
+  std::vector<void*> dma_dst, dma_src;
+  std::vector<size_t> dma_size;
 };

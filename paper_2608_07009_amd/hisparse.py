@@ -24,6 +24,7 @@ HISPARSE_ERR_UNSUPPORTED = -4
 HISPARSE_ERR_BAD_SELECTION = -5
 
 HISPARSE_FETCH_ZERO_COPY = 0
+HISPARSE_FETCH_SDMA = 1
 HISPARSE_FETCH_NONE = 2
 
 HISPARSE_HOST_COHERENT = 0

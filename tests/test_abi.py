@@ -56,7 +56,7 @@ def test_workload_descriptors_are_valid(cfg):
     ("share_group", 0, hs.HISPARSE_ERR_INVALID_ARG),
     ("num_requests", 0, hs.HISPARSE_ERR_INVALID_ARG),
     ("units_per_request", 70000, hs.HISPARSE_ERR_INVALID_ARG),
-    ("fetch", 1, hs.HISPARSE_ERR_UNSUPPORTED),
+    ("fetch", 3, hs.HISPARSE_ERR_UNSUPPORTED),
     ("host_memory", 7, hs.HISPARSE_ERR_INVALID_ARG),
     ("transfer_block_bytes", 48, hs.HISPARSE_ERR_INVALID_ARG),
     ("reserved", 1, hs.HISPARSE_ERR_INVALID_ARG),
@@ -100,3 +100,12 @@ def test_create_fails_cleanly_without_a_device_or_with_bad_args():
     with pytest.raises(hs.HisparseError) as e:
         hs.hisparse_cache_create(desc_for(w, capacity=1))
     assert e.value.status == hs.HISPARSE_ERR_INVALID_ARG
+
+
+def test_loads_in_a_process_that_imported_torch_first():
+    """torch brings its own HIP runtime; the library must not need symbols newer than it has."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = "import torch; from paper_2608_07009_amd import hisparse as hs; hs.lib()"
+    subprocess.check_call([sys.executable, "-c", code], cwd=root)

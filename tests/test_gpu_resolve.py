@@ -87,3 +87,21 @@ def test_resolve_fetch_none_same_tables():
     finally:
         a.close()
         b.close()
+
+
+@pytest.mark.parametrize("cfg,steps", [(1, 24), (3, 24)])
+def test_sdma_fetch_matches_zero_copy(cfg, steps):
+    """The host-issued DMA fetch path moves exactly the bytes the zero-copy kernel moves."""
+    w = W.workload(cfg, num_layers=1)
+    a = Run(w, steps)
+    b = Run(w, steps, fetch=hs.HISPARSE_FETCH_SDMA)
+    try:
+        for t in range(steps):
+            a.resolve_step(t)
+            b.resolve_step(t)
+            assert torch.equal(a.slots, b.slots) and torch.equal(a.counts, b.counts)
+            if t in (0, steps // 2, steps - 1):
+                assert (layer_cache_host(a, 0) == layer_cache_host(b, 0)).all(), f"step {t}"
+    finally:
+        a.close()
+        b.close()
