@@ -214,7 +214,9 @@ hisparse_status_t hisparse_sparse_decode(hisparse_cache_t cache, int32_t layer, 
 
 /* [async] The same attention over an explicit device pool [units][records_per_unit][R], with
  * d_idx int32 [units][k] record indices into each unit's part of the pool (-1 = skip). Used for
- * a fully resident KV (indices = positions), or any other placement. */
+ * a fully resident KV (indices = positions), or any other placement. One unit's part of the
+ * pool, records_per_unit * R bytes, must stay below 2 GiB (HISPARSE_ERR_UNSUPPORTED otherwise;
+ * the same holds for B * R of a cache). */
 hisparse_status_t hisparse_sparse_decode_pool(const void* d_pool, int64_t records_per_unit,
                                               int32_t record_bytes, int32_t units, int32_t top_k,
                                               const void* d_q, const int32_t* d_idx, float* d_out,

@@ -412,6 +412,8 @@ hisparse_status_t hisparse_sparse_decode_pool(const void* d_pool, int64_t record
   hisparse_status_t st = hisparse::plan_attention(units, top_k, record_bytes, attn, &p);
   if (st != HISPARSE_OK) return st;
   if (workspace_bytes < p.workspace_bytes) return HISPARSE_ERR_INVALID_ARG;
+  // the kernel addresses a unit's records with 32-bit byte offsets
+  if (records_per_unit * (int64_t)record_bytes > (int64_t)INT32_MAX) return HISPARSE_ERR_UNSUPPORTED;
   if (hisparse::launch_attention(p, *attn, reinterpret_cast<const uint8_t*>(d_pool),
                                  records_per_unit, record_bytes, units, top_k,
                                  reinterpret_cast<const uint16_t*>(d_q), d_idx, d_out, d_workspace,

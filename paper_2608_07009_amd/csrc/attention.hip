@@ -177,29 +177,41 @@ void attn_partial_kernel(AttnArgs a) {
   }
 
   // Direct global->LDS staging of chunk `it` of this token group into pipeline buffer `buf`.
-  // Load j (64 lanes) fills slots 64j .. 64j+63; wave hg issues loads [j0, j0 + n_loads).
-  // Padding slots are skipped; padding tokens and tokens past the split end get zeros (their
-  // scores are masked to -inf, so they carry P = 0).
-  const int n_loads = hg < NL_REM ? LPW_MAX : LPW_MIN;
-  const int j0 = hg * LPW_MIN + min(hg, NL_REM);
+  // Lane t < kChunk first resolves token t of the chunk to its byte offset in the unit's pool
+  // (-1: padding token, padding slot or past the split end; such rows read zeros, and their
+  // scores are masked to -inf so they carry P = 0). Load j (64 lanes) fills tile slots
+  // 64j .. 64j+63, which span at most three tile rows: each lane takes its row's offset from
+  // the lane that resolved it (scalar lane reads) and adds its 16-byte piece. Wave hg issues
+  // loads [j0, j0 + n_loads).
+  const int hg_s = __builtin_amdgcn_readfirstlane(hg);
+  const int n_loads = hg_s < NL_REM ? LPW_MAX : LPW_MIN;
+  const int j0 = hg_s * LPW_MIN + min(hg_s, NL_REM);
+  const uint8_t* zero_page = g_zero_token;
   auto issue = [&](int it, int buf) {
     const int cbase = tok_begin + it * kChunk * TW + tg * kChunk;
     uint16_t* tile = s_tiles + buf * TILE;
-    // recompute the per-lane slot arithmetic here instead of keeping it live across the loop
+    // recompute the per-lane arithmetic here instead of keeping it live across the loop
     int lane = threadIdx.x & 63;
     asm volatile("" : "+v"(lane));
+    const int tk = cbase + lane;
+    const bool in_chunk = lane < kChunk && tk < tok_end;
+    const int32_t s = s_idx[in_chunk ? (tk >> a.tpr_shift) - rec_begin : 0];
+    const int toff = (in_chunk && s >= 0) ? s * a.R + (tk & tpr_mask) * a.token_bytes : -1;
 #pragma unroll
     for (int jj = 0; jj < LPW_MAX; ++jj) {
       if (jj < n_loads) {  // wave-uniform
         const int j = j0 + jj;
-        const int p = 64 * j + lane;
-        const int t = p / PP, c = p % PP;
-        const int tk = cbase + t;
-        const bool real = t < kChunk && c < P && tk < tok_end;
-        const int32_t s = real ? s_idx[(tk >> a.tpr_shift) - rec_begin] : -1;
-        const uint8_t* src = s >= 0 ? pool_u + (int64_t)s * a.R +
-                                          (int64_t)(tk & tpr_mask) * a.token_bytes + 16 * c
-                                    : g_zero_token + 16 * (c < P ? c : 0);
+        const int t0 = (64 * j) / PP;
+        int c = 64 * j - t0 * PP + lane;
+        int o = __builtin_amdgcn_readlane(toff, t0);
+        const int o1 = __builtin_amdgcn_readlane(toff, t0 + 1);
+        if (c >= PP) { c -= PP; o = o1; }
+        if constexpr (PP < 64) {  // a load of 64 slots can reach a third row
+          const int o2 = __builtin_amdgcn_readlane(toff, t0 + 2);
+          if (c >= PP) { c -= PP; o = o2; }
+        }
+        const bool real = o >= 0 && c < P;
+        const uint8_t* src = real ? pool_u + (uint32_t)o + 16 * c : zero_page + 16 * (c < P ? c : 0);
         __builtin_amdgcn_global_load_lds(src, (lds_void*)(tile + 64 * j * 8), 16, 0, 0);
       }
     }
