@@ -376,30 +376,74 @@ struct CombineArgs {
   const float* part_o;
   const float2* part_ml;
   float* out;
-  int32_t H, n_parts;
+  int32_t H, n_parts, n_rows;  // n_rows = units * H
 };
 
+// One wave per (unit, head): the largest partial reference max M, the weights
+// w_p = 2^(m_p - M), then out = sum_p w_p o_p / sum_p w_p l_p, over the parts in split order.
+// Lane j holds the weight of part j of each group of 64 parts; eight parts' outputs are in
+// flight at a time.
 template <int DV>
-__global__ __launch_bounds__(DV / 4) void attn_combine_kernel(CombineArgs a) {
-  const int uh = blockIdx.x;
-  const int unit = uh / a.H, h = uh % a.H;
-  const float2* ml = a.part_ml + (int64_t)unit * a.n_parts * a.H + h;
+__global__ __launch_bounds__(256) void attn_combine_kernel(CombineArgs a) {
+  constexpr int E = DV / 64;  // output floats per lane
+  static_assert(E == 2 || E == 8, "d_v");
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= a.n_rows) return;
+  const int unit = row / a.H, h = row % a.H;
+  const int np = a.n_parts;
+  const int64_t pstride = (int64_t)a.H * DV;
+  const float2* ml = a.part_ml + (int64_t)unit * np * a.H + h;
+  const float* po = a.part_o + (int64_t)unit * np * pstride + (int64_t)h * DV + lane * E;
+
   float M = -INFINITY;
-  for (int p = 0; p < a.n_parts; ++p) M = fmaxf(M, ml[(int64_t)p * a.H].x);
+  for (int pb = lane; pb < np; pb += 64) M = fmaxf(M, ml[(int64_t)pb * a.H].x);
+#pragma unroll
+  for (int x = 32; x >= 1; x >>= 1) M = fmaxf(M, __shfl_xor(M, x, 64));
+
+  float acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
   float lsum = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  const int d = threadIdx.x * 4;
-  for (int p = 0; p < a.n_parts; ++p) {
-    const float2 v = ml[(int64_t)p * a.H];
-    const float wgt = v.x == -INFINITY ? 0.f : exp2f(v.x - M);
-    lsum += wgt * v.y;
-    const f32x4 po = *reinterpret_cast<const f32x4*>(
-        a.part_o + (((int64_t)unit * a.n_parts + p) * a.H + h) * DV + d);
-    acc += wgt * po;
+  for (int pb = 0; pb < np; pb += 64) {
+    float w = 0.f;
+    if (pb + lane < np) {
+      const float2 v = ml[(int64_t)(pb + lane) * a.H];
+      w = v.x == -INFINITY ? 0.f : exp2f(v.x - M);
+      lsum += w * v.y;
+    }
+    const int n = min(64, np - pb);
+    for (int i = 0; i < n; i += 8) {
+      float val[8][E];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (i + u < n) {
+          const float* src = po + (int64_t)(pb + i + u) * pstride;
+#pragma unroll
+          for (int e = 0; e < E; e += 2) {
+            const float2 t = *reinterpret_cast<const float2*>(src + e);
+            val[u][e] = t.x;
+            val[u][e + 1] = t.y;
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (i + u < n) {
+          const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), i + u));
+#pragma unroll
+          for (int e = 0; e < E; ++e) acc[e] += wu * val[u][e];
+        }
+      }
+    }
   }
-  f32x4 r = {0.f, 0.f, 0.f, 0.f};
-  if (lsum > 0.f) r = acc / lsum;
-  *reinterpret_cast<f32x4*>(a.out + ((int64_t)unit * a.H + h) * DV + d) = r;
+#pragma unroll
+  for (int x = 32; x >= 1; x >>= 1) lsum += __shfl_xor(lsum, x, 64);
+  const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+  float* dst = a.out + (int64_t)row * DV + lane * E;
+#pragma unroll
+  for (int e = 0; e < E; e += 2)
+    *reinterpret_cast<float2*>(dst + e) = make_float2(acc[e] * inv, acc[e + 1] * inv);
 }
 
 template <int DQK, int DV, int VOFF, int HW, int TW, int NST>
@@ -504,11 +548,12 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  CombineArgs c{a.part_o, a.part_ml, out, attn.q_heads, p.n_parts};
+  CombineArgs c{a.part_o, a.part_ml, out, attn.q_heads, p.n_parts, units * attn.q_heads};
+  const int n_cwg = (units * attn.q_heads + 3) / 4;
   if (attn.d_v == 512)
-    hipLaunchKernelGGL(attn_combine_kernel<512>, dim3(units * attn.q_heads), dim3(128), 0, stream, c);
+    hipLaunchKernelGGL(attn_combine_kernel<512>, dim3(n_cwg), dim3(256), 0, stream, c);
   else
-    hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(units * attn.q_heads), dim3(32), 0, stream, c);
+    hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(n_cwg), dim3(256), 0, stream, c);
   return hipGetLastError();
 }
 
