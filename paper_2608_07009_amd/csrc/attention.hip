@@ -29,6 +29,7 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kChunk = 32;            // tokens per wave per iteration
@@ -53,8 +54,17 @@ struct AttnArgs {
   int64_t rec_per_unit;
   int32_t R, token_bytes, tpr_shift, k, H, n_tok;
   int32_t split_tokens, n_wg_splits, hb, n_parts, n_wg;
+  int32_t Hp;  // latent attention: heads rounded up to 32 (partial-output block layout)
   float scale_log2;
 };
+
+// Latent-attention partial outputs are stored in the PV accumulators' own layout, so every
+// lane writes 16 contiguous bytes: per part, 32-head block b, output tile n (dims 32n..32n+31),
+// group q and lane L hold heads 32b + 8q + 4(L >> 5) + e, e = 0..3, of dim 32n + (L & 31).
+__device__ __host__ inline int64_t mla_part_offset(int head, int dim) {
+  const int hl = head & 31, q = hl >> 3, e = hl & 3, ln = ((hl >> 2) & 1) * 32 + (dim & 31);
+  return (int64_t)(head >> 5) * 32 * 512 + ((((dim >> 5) * 4 + q) * 64 + ln) * 4 + e);
+}
 
 __device__ inline uint16_t f32_to_bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
@@ -92,6 +102,64 @@ struct TileRow {
 // holds tokens perm(4g + j) (+16), and the PV transpose reads touch rows two apart, which
 // with the padded row stride keeps both access patterns free of bank conflicts.
 __device__ inline int tile_row(int m) { return 8 * (m >> 3) + 2 * (m & 3) + ((m >> 2) & 1); }
+
+// Direct global->LDS staging of one 32-token chunk starting at token cbase into `tile`.
+// Lane t < kChunk first resolves token t of the chunk to its byte offset in the unit's pool
+// (-1: padding token, padding slot or past the split end; such rows read zeros, and their
+// scores are masked to -inf so they carry P = 0). Load j (64 lanes) fills tile slots
+// 64j .. 64j+63, which span at most three tile rows: each lane takes its row's offset from the
+// lane that resolved it (scalar lane reads) and adds its 16-byte piece. The calling wave
+// issues loads [j0, j0 + n_loads) of the chunk.
+template <int P, int PP, int LPW_MAX>
+__device__ __forceinline__ void stage_chunk(uint16_t* tile, const int32_t* s_idx,
+                                            const uint8_t* pool_u, int cbase, int tok_end,
+                                            int rec_begin, int tpr_shift, int R, int token_bytes,
+                                            int j0, int n_loads) {
+  // recompute the per-lane arithmetic here instead of keeping it live across the loop
+  int lane = threadIdx.x & 63;
+  asm volatile("" : "+v"(lane));
+  const int tk = cbase + lane;
+  const bool in_chunk = lane < kChunk && tk < tok_end;
+  const int32_t s = s_idx[in_chunk ? (tk >> tpr_shift) - rec_begin : 0];
+  const int toff =
+      (in_chunk && s >= 0) ? s * R + (tk & ((1 << tpr_shift) - 1)) * token_bytes : -1;
+#pragma unroll
+  for (int jj = 0; jj < LPW_MAX; ++jj) {
+    if (jj < n_loads) {  // wave-uniform
+      const int j = j0 + jj;
+      const int t0 = (64 * j) / PP;
+      int c = 64 * j - t0 * PP + lane;
+      int o = __builtin_amdgcn_readlane(toff, t0);
+      const int o1 = __builtin_amdgcn_readlane(toff, t0 + 1);
+      if (c >= PP) { c -= PP; o = o1; }
+      if constexpr (PP < 64) {  // a load of 64 slots can reach a third row
+        const int o2 = __builtin_amdgcn_readlane(toff, t0 + 2);
+        if (c >= PP) { c -= PP; o = o2; }
+      }
+      const bool real = o >= 0 && c < P;
+      const uint8_t* src =
+          real ? pool_u + (uint32_t)o + 16 * c : g_zero_token + 16 * (c < P ? c : 0);
+      __builtin_amdgcn_global_load_lds(src, (lds_void*)(tile + 64 * j * 8), 16, 0, 0);
+    }
+  }
+}
+
+// The calling wave's loads of the current chunk are done once at most `younger` later chunks'
+// loads (n_loads each) are outstanding; then the workgroup synchronises.
+template <int NST, int LPW_MAX, int LPW_MIN>
+__device__ __forceinline__ void wait_chunk(int younger, bool max_loads) {
+  if constexpr (NST == 2) {
+    wait_loads_and_barrier<0>();
+  } else if (max_loads) {
+    if (younger >= 2) wait_loads_and_barrier<(NST - 2) * LPW_MAX>();
+    else if (younger == 1) wait_loads_and_barrier<LPW_MAX>();
+    else wait_loads_and_barrier<0>();
+  } else {
+    if (younger >= 2) wait_loads_and_barrier<(NST - 2) * LPW_MIN>();
+    else if (younger == 1) wait_loads_and_barrier<LPW_MIN>();
+    else wait_loads_and_barrier<0>();
+  }
+}
 
 template <int DQK, int DV, int VOFF, int HW, int TW, int NST>
 __global__ __launch_bounds__(64 * HW * TW, (HW * TW >= 8) ? 2 : 1)
@@ -131,7 +199,6 @@ void attn_partial_kernel(AttnArgs a) {
   const int tok_end = min(a.n_tok, tok_begin + a.split_tokens);
   const int rec_begin = tok_begin >> a.tpr_shift;
   const int n_rec = ((tok_end - 1) >> a.tpr_shift) - rec_begin + 1;
-  const int tpr_mask = (1 << a.tpr_shift) - 1;
   {
     const int32_t* idx_u = a.idx + (int64_t)unit * a.k + rec_begin;
     for (int i = tid; i < n_rec; i += 64 * HW * TW) {
@@ -176,61 +243,16 @@ void attn_partial_kernel(AttnArgs a) {
     }
   }
 
-  // Direct global->LDS staging of chunk `it` of this token group into pipeline buffer `buf`.
-  // Lane t < kChunk first resolves token t of the chunk to its byte offset in the unit's pool
-  // (-1: padding token, padding slot or past the split end; such rows read zeros, and their
-  // scores are masked to -inf so they carry P = 0). Load j (64 lanes) fills tile slots
-  // 64j .. 64j+63, which span at most three tile rows: each lane takes its row's offset from
-  // the lane that resolved it (scalar lane reads) and adds its 16-byte piece. Wave hg issues
-  // loads [j0, j0 + n_loads).
+  // wave hg stages loads [j0, j0 + n_loads) of each chunk of its token group
   const int hg_s = __builtin_amdgcn_readfirstlane(hg);
   const int n_loads = hg_s < NL_REM ? LPW_MAX : LPW_MIN;
   const int j0 = hg_s * LPW_MIN + min(hg_s, NL_REM);
-  const uint8_t* zero_page = g_zero_token;
   auto issue = [&](int it, int buf) {
-    const int cbase = tok_begin + it * kChunk * TW + tg * kChunk;
-    uint16_t* tile = s_tiles + buf * TILE;
-    // recompute the per-lane arithmetic here instead of keeping it live across the loop
-    int lane = threadIdx.x & 63;
-    asm volatile("" : "+v"(lane));
-    const int tk = cbase + lane;
-    const bool in_chunk = lane < kChunk && tk < tok_end;
-    const int32_t s = s_idx[in_chunk ? (tk >> a.tpr_shift) - rec_begin : 0];
-    const int toff = (in_chunk && s >= 0) ? s * a.R + (tk & tpr_mask) * a.token_bytes : -1;
-#pragma unroll
-    for (int jj = 0; jj < LPW_MAX; ++jj) {
-      if (jj < n_loads) {  // wave-uniform
-        const int j = j0 + jj;
-        const int t0 = (64 * j) / PP;
-        int c = 64 * j - t0 * PP + lane;
-        int o = __builtin_amdgcn_readlane(toff, t0);
-        const int o1 = __builtin_amdgcn_readlane(toff, t0 + 1);
-        if (c >= PP) { c -= PP; o = o1; }
-        if constexpr (PP < 64) {  // a load of 64 slots can reach a third row
-          const int o2 = __builtin_amdgcn_readlane(toff, t0 + 2);
-          if (c >= PP) { c -= PP; o = o2; }
-        }
-        const bool real = o >= 0 && c < P;
-        const uint8_t* src = real ? pool_u + (uint32_t)o + 16 * c : zero_page + 16 * (c < P ? c : 0);
-        __builtin_amdgcn_global_load_lds(src, (lds_void*)(tile + 64 * j * 8), 16, 0, 0);
-      }
-    }
+    stage_chunk<P, PP, LPW_MAX>(s_tiles + buf * TILE, s_idx, pool_u,
+                                tok_begin + it * kChunk * TW + tg * kChunk, tok_end, rec_begin,
+                                a.tpr_shift, a.R, a.token_bytes, j0, n_loads);
   };
-  // this wave's loads for the current chunk are done once at most `younger` later chunks'
-  // loads are outstanding
-  auto wait_chunk = [&](int younger) {
-    if constexpr (NST == 2) {
-      wait_loads_and_barrier<0>();
-    } else if (hg < NL_REM) {
-      if (younger >= 2) wait_loads_and_barrier<(NST - 2) * LPW_MAX>();
-      else if (younger == 1) wait_loads_and_barrier<LPW_MAX>();
-      else wait_loads_and_barrier<0>();
-    } else {
-      if (younger >= 2) wait_loads_and_barrier<(NST - 2) * LPW_MIN>();
-      else if (younger == 1) wait_loads_and_barrier<LPW_MIN>();
-      else wait_loads_and_barrier<0>();
-    }
-  };
+  auto wait = [&](int younger) { wait_chunk<NST, LPW_MAX, LPW_MIN>(younger, hg < NL_REM); };
 
 #pragma unroll
   for (int st = 0; st < NST - 1; ++st)
@@ -291,7 +313,7 @@ void attn_partial_kernel(AttnArgs a) {
   for (;;) {
     for (; it < n_it; ++it) {
       // chunks it+1 .. it+NST-2 were issued earlier and may still be in flight
-      wait_chunk(min(NST - 2, n_it - 1 - it));
+      wait(min(NST - 2, n_it - 1 - it));
       // every wave is past its reads of buffer (it-1) % NST: refill it with chunk it+NST-1
       if (it + NST - 1 < n_it) issue(it + NST - 1, (it + NST - 1) % NST);
 
@@ -372,6 +394,304 @@ void attn_partial_kernel(AttnArgs a) {
     a.part_ml[((int64_t)unit * a.n_parts + part) * a.H + head] = make_float2(m_run, l_run);
 }
 
+// Logical row r of a 32-token MFMA tile -> LDS tile row (token) for the latent-attention kernel.
+// With r = 16a + 8b + 4h + s the row is 16a + 4s + 2b + h: the P operand of a lane (k-step a,
+// half h) then comes straight from its S^T accumulator, and each group of 16 lanes of a V
+// transpose read touches rows 4 apart, i.e. four row bases 16 banks apart under the padded
+// stride, so those reads are free of bank conflicts; the 16 K rows one operand load reads are
+// a permutation of 16 consecutive rows, which are conflict-free as well.
+__device__ inline int mla_row(int r) {
+  return 16 * (r >> 4) + 4 * (r & 3) + 2 * ((r >> 3) & 1) + ((r >> 2) & 1);
+}
+
+// Scores of the latent-attention kernel may exceed the split's reference by this many powers
+// of two: P <= 2^64 and sums over at most 8192 tokens stay far inside the fp32/bf16 range.
+constexpr float kMlaSlack = 64.0f;
+
+// Exact fallback for a latent-attention split whose scores outgrow the reference: plain online
+// softmax with fp32 rescaling, one head at a time per wave, K and V read straight from the
+// pool. Writes the split's partial results in the fast path's format. Only inputs whose scores
+// span more than kMlaSlack powers of two within one split ever come here.
+__device__ __forceinline__ void mla_split_exact(const AttnArgs& a, const int32_t* s_idx,
+                                                const uint32_t* s_valid, int unit, int split,
+                                                int tok_begin, int tok_end, int rec_begin,
+                                                int head0) {
+  constexpr int DQK = 576, DV = 512;
+  const int lane = threadIdx.x & 63;
+  const uint8_t* pool_u = a.pool + (int64_t)unit * a.rec_per_unit * a.R;
+  const int tpr_mask = (1 << a.tpr_shift) - 1;
+  for (int hh = 0; hh < 32; ++hh) {
+    const int head = head0 + hh;
+    if (head >= a.H) break;
+    const uint16_t* qh = a.q + ((int64_t)unit * a.H + head) * DQK;
+    float qv[DQK / 64];
+#pragma unroll
+    for (int i = 0; i < DQK / 64; ++i) qv[i] = bf16_to_f32(qh[lane + 64 * i]);
+    float m = -INFINITY, l = 0.f, acc[DV / 64];
+#pragma unroll
+    for (int e = 0; e < DV / 64; ++e) acc[e] = 0.f;
+    for (int t = tok_begin; t < tok_end; ++t) {
+      const int bit = t - tok_begin;
+      if (!((s_valid[bit >> 5] >> (bit & 31)) & 1u)) continue;
+      const int rec = s_idx[(t >> a.tpr_shift) - rec_begin];
+      const uint16_t* kt = reinterpret_cast<const uint16_t*>(
+          pool_u + (int64_t)rec * a.R + (int64_t)(t & tpr_mask) * a.token_bytes);
+      float d = 0.f;
+#pragma unroll
+      for (int i = 0; i < DQK / 64; ++i) d += qv[i] * bf16_to_f32(kt[lane + 64 * i]);
+#pragma unroll
+      for (int x = 32; x >= 1; x >>= 1) d += __shfl_xor(d, x, 64);
+      const float sc = d * a.scale_log2;
+      const float m_new = fmaxf(m, sc);
+      const float alpha = exp2f(m - m_new);
+      const float pr = exp2f(sc - m_new);
+      l = l * alpha + pr;
+#pragma unroll
+      for (int e = 0; e < DV / 64; ++e)
+        acc[e] = acc[e] * alpha + pr * bf16_to_f32(kt[lane * (DV / 64) + e]);
+      m = m_new;
+    }
+    float* po = a.part_o + ((int64_t)unit * a.n_parts + split) * a.Hp * DV;
+#pragma unroll
+    for (int e = 0; e < DV / 64; ++e) po[mla_part_offset(head, lane * (DV / 64) + e)] = acc[e];
+    if (lane == 0)
+      a.part_ml[((int64_t)unit * a.n_parts + split) * a.H + head] = make_float2(m, l);
+  }
+}
+
+// Latent attention (d_qk 576, d_v 512 = the first 512 key dims). One workgroup per
+// (unit, token split, head block of 32 * NW heads); wave w owns 32 heads and the workgroup's
+// 32-token chunks are staged once in LDS for all of them.
+//   S^T[token][head] = K[token][:] . Q^T[:][head]   v_mfma_f32_32x32x16_bf16, 36 k-steps, K rows
+//                                                   from LDS, Q resident in VGPRs
+//   O[head][dim]    += P[head][token] . V[token][dim]  v_mfma_f32_32x32x16_bf16, 2 k-steps x 16
+//                                                   output tiles, V by LDS transpose reads
+// A lane holds 16 of a head's 32 scores (the other 16 are in lane ^ 32), which are exactly its
+// P operands of the two PV k-steps; O (16 tiles x 16 fp32 per lane) lives in accumulators.
+template <int NW, int NST>
+__global__ __launch_bounds__(64 * NW, 1)
+void attn_mla_kernel(AttnArgs a) {
+  constexpr int DQK = 576, DV = 512;
+  constexpr int P = DQK / 8;                              // 16-byte pieces per token
+  constexpr int PP = TileRow<P>::PP;                      // pieces per LDS row
+  constexpr int NL = ((kChunk - 1) * PP + P + 63) / 64;   // 64-lane loads per chunk
+  constexpr int TILE = NL * 64 * 8;                       // bf16 per chunk tile
+  constexpr int LPW_MAX = (NL + NW - 1) / NW;
+  constexpr int LPW_MIN = NL / NW;
+  constexpr int NL_REM = NL % NW;
+  constexpr int NKK = DQK / 16;  // QK k-steps
+  constexpr int NDV = DV / 32;   // PV output tiles
+  static_assert(NST >= 2 && NST <= 4 && (NST - 2) * LPW_MAX < 64, "pipeline depth");
+  __shared__ __align__(16) uint16_t s_kv[NST * TILE];
+  __shared__ int32_t s_idx[kMaxSplitRecords];         // the split's record indices, -1 = skip
+  __shared__ uint32_t s_valid[kMaxSplitTokens / 32];  // bit t of word c: token 32c+t attends
+  __shared__ int s_fallback;                           // some score outgrew its reference
+
+  // XCD-aware mapping, as in attn_partial_kernel
+  const int nwg_pad = (a.n_wg + 7) & ~7;
+  const int w = (int)(blockIdx.x & 7) * (nwg_pad >> 3) + (int)(blockIdx.x >> 3);
+  if (w >= a.n_wg) return;
+  const int hb = w % a.hb;
+  const int split = (w / a.hb) % a.n_wg_splits;
+  const int unit = w / (a.hb * a.n_wg_splits);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, col = lane & 31;
+
+  const int tok_begin = split * a.split_tokens;
+  const int tok_end = min(a.n_tok, tok_begin + a.split_tokens);
+  const int rec_begin = tok_begin >> a.tpr_shift;
+  const int n_rec = ((tok_end - 1) >> a.tpr_shift) - rec_begin + 1;
+  {
+    const int32_t* idx_u = a.idx + (int64_t)unit * a.k + rec_begin;
+    for (int i = tid; i < n_rec; i += 64 * NW) {
+      const int32_t s = idx_u[i];
+      s_idx[i] = (s >= 0 && s < a.rec_per_unit) ? s : -1;
+    }
+  }
+  const uint8_t* pool_u = a.pool + (int64_t)unit * a.rec_per_unit * a.R;
+
+  if (tid == 0) s_fallback = 0;
+  __syncthreads();  // s_idx is ready
+  const int n_it = (tok_end - tok_begin + kChunk - 1) / kChunk;
+  for (int base = wave * 64; base < n_it * kChunk; base += 64 * NW) {
+    const int tk = tok_begin + base + lane;
+    const bool ok = tk < tok_end && s_idx[(tk >> a.tpr_shift) - rec_begin] >= 0;
+    const uint64_t m = __ballot(ok);
+    if (lane == 0) {
+      s_valid[base >> 5] = (uint32_t)m;
+      if (base + 32 < n_it * kChunk) s_valid[(base >> 5) + 1] = (uint32_t)(m >> 32);
+    }
+  }
+
+  const int w_s = __builtin_amdgcn_readfirstlane(wave);
+  const int n_loads = w_s < NL_REM ? LPW_MAX : LPW_MIN;
+  const int j0 = w_s * LPW_MIN + min(w_s, NL_REM);
+  auto issue = [&](int it, int buf) {
+    stage_chunk<P, PP, LPW_MAX>(s_kv + buf * TILE, s_idx, pool_u, tok_begin + it * kChunk,
+                                tok_end, rec_begin, a.tpr_shift, a.R, a.token_bytes, j0,
+                                n_loads);
+  };
+  const int head0 = hb * 32 * NW + wave * 32;  // first head of this wave
+  const int head = head0 + col;
+  const bool head_ok = head < a.H;
+  f32x16 o[NDV];
+#pragma unroll
+  for (int n = 0; n < NDV; ++n) o[n] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.f;
+  float sc[16];
+
+  auto finish_chunk = [&](const uint16_t* tile) {
+    uint32_t pw[8];
+    float psum = 0.f;
+    if (m_run == -INFINITY) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) pw[j] = 0u;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 16; j += 2) {
+        const uint16_t b0 = f32_to_bf16_rne(exp2f(sc[j] - m_run));
+        const uint16_t b1 = f32_to_bf16_rne(exp2f(sc[j + 1] - m_run));
+        psum += bf16_to_f32(b0);
+        psum += bf16_to_f32(b1);
+        pw[j >> 1] = (uint32_t)b0 | ((uint32_t)b1 << 16);
+      }
+    }
+    psum += __shfl_xor(psum, 32, 64);
+    l_run += psum;
+    const bf16x8_t pa0 = __builtin_bit_cast(bf16x8_t, u32x4{pw[0], pw[1], pw[2], pw[3]});
+    const bf16x8_t pa1 = __builtin_bit_cast(bf16x8_t, u32x4{pw[4], pw[5], pw[6], pw[7]});
+    // V operand by transpose reads: in each 16-lane group lane 4s+q addresses row
+    // 16kb + 4s + half (+2 for the second read), columns 32n + 16 (col >> 4) + 4q .. +3; lane
+    // t of the group then holds V[those rows][32n + 16 (col >> 4) + t], the k order of P.
+    const uint16_t* v0 = tile + (4 * ((lane & 15) >> 2) + half) * PP * 8 + 16 * (col >> 4) +
+                         4 * (lane & 3);
+    // MFMA i = (k-step kb, tile n) = (i / NDV, i % NDV), so consecutive MFMAs update
+    // different tiles; its two reads run VD MFMAs ahead
+    constexpr int VD = 3;
+    constexpr int NM = 2 * NDV;
+    v4i16 vlo[VD], vhi[VD];
+    auto vread = [&](int i, int slot) {
+      const uint16_t* vp = v0 + (i / NDV) * 16 * PP * 8 + 32 * (i % NDV);
+      vlo[slot] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)vp);
+      vhi[slot] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vp + 2 * PP * 8));
+    };
+#pragma unroll
+    for (int i = 0; i < VD; ++i) vread(i, i);
+#pragma unroll
+    for (int i = 0; i < NM; ++i) {
+      const bf16x8_t vb = __builtin_bit_cast(
+          bf16x8_t, __builtin_shufflevector(vlo[i % VD], vhi[i % VD], 0, 1, 2, 3, 4, 5, 6, 7));
+      o[i % NDV] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(i < NDV ? pa0 : pa1, vb, o[i % NDV],
+                                                           0, 0, 0);
+      if (i + VD < NM) vread(i + VD, i % VD);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // Exponentials are taken against a per-head reference max fixed by the first valid chunk of
+  // the split (exact softmax arithmetic with a different reference point; the combine uses the
+  // same reference). Scores more than kMlaSlack powers of two above it send the whole split to
+  // an exact fallback after the loop, whose results are then discarded; the loop itself never
+  // leaves early, so O has a single update path (the MFMAs) and stays in accumulators.
+#pragma unroll
+  for (int st = 0; st < NST - 1; ++st)
+    if (st < n_it) issue(st, st);
+
+  // Q^T operand: Q[head][16kk + 8 half .. +7], loaded while the first chunks are in flight
+  bf16x8_t qreg[NKK];
+  {
+    const uint16_t* qrow = a.q + ((int64_t)unit * a.H + (head_ok ? head : 0)) * DQK + 8 * half;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (head_ok) v = *reinterpret_cast<const u32x4*>(qrow + kk * 16);
+      qreg[kk] = __builtin_bit_cast(bf16x8_t, v);
+    }
+  }
+
+
+  for (int it = 0; it < n_it; ++it) {
+    // chunks it+1 .. it+NST-2 were issued earlier and may still be in flight
+    wait_chunk<NST, LPW_MAX, LPW_MIN>(min(NST - 2, n_it - 1 - it), w_s < NL_REM);
+    // every wave is past its reads of buffer (it-1) % NST: refill it with chunk it+NST-1
+    if (it + NST - 1 < n_it) issue(it + NST - 1, (it + NST - 1) % NST);
+
+    const uint16_t* tile = s_kv + (it % NST) * TILE;
+    const int cbase = tok_begin + it * kChunk;
+
+    // ---- scores: S^T for the chunk's 32 tokens x this wave's 32 heads ----
+    // K operand reads run KD k-steps ahead of the MFMAs (a small register ring; the
+    // scheduling fences keep the compiler from hoisting all 36 reads). The score MFMAs are
+    // written as assembly so that their accumulator stays in VGPRs: the output tiles fill
+    // the accumulation registers. Hazards hidden from the compiler by the assembly are
+    // covered in it: wait states before each MFMA for a just-written operand, and after the
+    // last one before the scores are read.
+    constexpr int KD = 4;
+    f32x16 sacc, sacc1;  // even / odd k-steps: two independent MFMA chains
+    const uint16_t* krow = tile + (mla_row(col) * PP + half) * 8;
+    u32x4 kbuf[KD];
+#pragma unroll
+    for (int kk = 0; kk < KD; ++kk) kbuf[kk] = lds_load16(krow + kk * 16);
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      if (kk == 0)
+        asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0"
+                     : "=&v"(sacc) : "v"(kbuf[0]), "v"(qreg[0]));
+      else if (kk == 1)
+        asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0"
+                     : "=&v"(sacc1) : "v"(kbuf[1]), "v"(qreg[1]));
+      else if (kk & 1)
+        asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0"
+                     : "+v"(sacc1) : "v"(kbuf[kk % KD]), "v"(qreg[kk]));
+      else
+        asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0"
+                     : "+v"(sacc) : "v"(kbuf[kk % KD]), "v"(qreg[kk]));
+      if (kk + KD < NKK) kbuf[kk % KD] = lds_load16(krow + (kk + KD) * 16);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(sacc), "+v"(sacc1));
+    sacc += sacc1;
+    const uint32_t vmask = s_valid[(cbase - tok_begin) >> 5];
+    int hq = half;
+    asm volatile("" : "+v"(hq));
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int bit = mla_row(8 * (j >> 2) + 4 * hq + (j & 3));
+      sc[j] = ((vmask >> bit) & 1u) ? sacc[j] * a.scale_log2 : -INFINITY;
+    }
+    float cmax = sc[0];
+#pragma unroll
+    for (int j = 1; j < 16; ++j) cmax = fmaxf(cmax, sc[j]);
+    cmax = fmaxf(cmax, __shfl_xor(cmax, 32, 64));
+    // Validity is per token, so every head of the wave agrees on whether m_run is -inf; while
+    // it is, O and l are exactly zero and the reference can simply be set.
+    if (m_run == -INFINITY) m_run = cmax;
+    else if (__ballot(cmax > m_run + kMlaSlack) && lane == 0) s_fallback = 1;
+    finish_chunk(tile);
+  }
+  wait_loads_and_barrier<0>();  // no staging in flight; s_fallback is final
+  if (s_fallback) {
+    mla_split_exact(a, s_idx, s_valid, unit, split, tok_begin, tok_end, rec_begin, head0);
+    return;
+  }
+
+  // ---- partial results of this split, in the accumulator layout (see mla_part_offset) ----
+  if (head0 < a.H) {
+    float* po = a.part_o + ((int64_t)unit * a.n_parts + split) * a.Hp * DV +
+                (int64_t)(head0 >> 5) * 32 * DV + lane * 4;
+#pragma unroll
+    for (int n = 0; n < NDV; ++n) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<f32x4*>(po + (n * 4 + q) * 256) =
+            f32x4{o[n][4 * q], o[n][4 * q + 1], o[n][4 * q + 2], o[n][4 * q + 3]};
+    }
+  }
+  if (lane < 32 && head_ok)
+    a.part_ml[((int64_t)unit * a.n_parts + split) * a.H + head] = make_float2(m_run, l_run);
+}
+
 struct CombineArgs {
   const float* part_o;
   const float2* part_ml;
@@ -446,11 +766,88 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(CombineArgs a) {
     *reinterpret_cast<float2*>(dst + e) = make_float2(acc[e] * inv, acc[e + 1] * inv);
 }
 
+constexpr int kMlaMaxParts = 128;
+
+struct CombineMlaArgs {
+  const float* part_o;    // [units][n_parts][Hp * 512], block layout
+  const float2* part_ml;  // [units][n_parts][H]
+  float* out;             // [units][H][512]
+  int32_t H, Hp, n_parts, chunks;  // chunks: workgroups per (unit, 32-head block)
+};
+
+// Merge of latent-attention partials: one workgroup per (unit, 32-head block, slice of the
+// block). Weights w_ph = 2^(m_ph - M_h) and L_h = sum_p w_ph l_ph first (in LDS), then each
+// thread reduces whole 16-byte groups of the block layout over the parts in split order.
+__global__ __launch_bounds__(256) void attn_combine_mla_kernel(CombineMlaArgs a) {
+  constexpr int DV = 512, BLK4 = 32 * DV / 4;  // float4 groups per 32-head block
+  __shared__ __align__(16) float s_w[kMlaMaxParts][32];
+  __shared__ float s_inv[32];
+  const int nb = a.Hp >> 5;
+  const int chunk = blockIdx.x % a.chunks;
+  const int b = (blockIdx.x / a.chunks) % nb;
+  const int unit = blockIdx.x / (a.chunks * nb);
+  const int t = threadIdx.x, hl = t >> 3, sub = t & 7;
+  const int head = b * 32 + hl;
+  const int np = a.n_parts;
+  const float2* ml = a.part_ml + (int64_t)unit * np * a.H;
+  float M = -INFINITY;
+  if (head < a.H)
+    for (int p = sub; p < np; p += 8) M = fmaxf(M, ml[(int64_t)p * a.H + head].x);
+#pragma unroll
+  for (int x = 1; x < 8; x <<= 1) M = fmaxf(M, __shfl_xor(M, x, 64));
+  float lsum = 0.f;
+  for (int p = sub; p < np; p += 8) {
+    float w = 0.f;
+    if (head < a.H) {
+      const float2 v = ml[(int64_t)p * a.H + head];
+      w = v.x == -INFINITY ? 0.f : exp2f(v.x - M);
+      lsum += w * v.y;
+    }
+    s_w[p][hl] = w;
+  }
+#pragma unroll
+  for (int x = 1; x < 8; x <<= 1) lsum += __shfl_xor(lsum, x, 64);
+  if (sub == 0) s_inv[hl] = lsum > 0.f ? 1.f / lsum : 0.f;
+  __syncthreads();
+
+  const int per = BLK4 / a.chunks;  // groups of this workgroup
+  const int64_t pstride = (int64_t)a.Hp * DV;
+  const float* pb = a.part_o + (int64_t)unit * np * pstride + (int64_t)b * 32 * DV;
+  for (int f = chunk * per + t; f < (chunk + 1) * per; f += 256) {
+    const int ln = f & 63, q = (f >> 6) & 3, n = f >> 8;
+    const int h0 = 8 * q + 4 * (ln >> 5);  // first of the group's four heads (block-local)
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    int p = 0;
+    for (; p + 4 <= np; p += 4) {
+      f32x4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const f32x4*>(pb + (p + u) * pstride + 4 * f);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc += *reinterpret_cast<const f32x4*>(&s_w[p + u][h0]) * v[u];
+    }
+    for (; p < np; ++p)
+      acc += *reinterpret_cast<const f32x4*>(&s_w[p][h0]) *
+             *reinterpret_cast<const f32x4*>(pb + p * pstride + 4 * f);
+    const int dim = 32 * n + (ln & 31);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int h = b * 32 + h0 + e;
+      if (h < a.H) a.out[((int64_t)unit * a.H + h) * DV + dim] = acc[e] * s_inv[h0 + e];
+    }
+  }
+}
+
 template <int DQK, int DV, int VOFF, int HW, int TW, int NST>
 void launch_partial(const AttnArgs& args, hipStream_t stream) {
   const int nwg_pad = (args.n_wg + 7) & ~7;
   hipLaunchKernelGGL((attn_partial_kernel<DQK, DV, VOFF, HW, TW, NST>), dim3(nwg_pad),
                      dim3(64 * HW * TW), 0, stream, args);
+}
+
+template <int NW, int NST>
+void launch_mla(const AttnArgs& args, hipStream_t stream) {
+  const int nwg_pad = (args.n_wg + 7) & ~7;
+  hipLaunchKernelGGL((attn_mla_kernel<NW, NST>), dim3(nwg_pad), dim3(64 * NW), 0, stream, args);
 }
 
 bool is_mla(const hisparse_attn_desc_t& d) {
@@ -467,15 +864,26 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
   if (units <= 0 || (int64_t)units * 256 > (1LL << 30)) return HISPARSE_ERR_INVALID_ARG;
   const int H = attn->q_heads;
   AttnPlan p{};
-  if (is_mla(*attn)) {  // up to 64 heads per workgroup (Q and O of 16 heads fill a wave)
-    p.hw = H <= 16 ? 1 : (H <= 32 ? 2 : 4);
+  p.n_tok = top_k * attn->tokens_per_record;
+  if (is_mla(*attn)) {
+    // 32 heads per wave, up to 4 waves (128 heads) per workgroup: the most heads per staged
+    // chunk that still gives about a workgroup per CU with at least two chunks per split
+    const int64_t split_cap = std::max(1, p.n_tok / (2 * kChunk));
+    p.hw = 1;
+    for (int nw : {4, 2}) {
+      const int64_t hb = (H + 32 * nw - 1) / (32 * nw);
+      if (32 * (nw / 2) < H && (int64_t)units * hb * split_cap >= kTargetWorkgroups) {
+        p.hw = nw;
+        break;
+      }
+    }
     p.tw = 1;
-  } else {
+    p.hb = (H + 32 * p.hw - 1) / (32 * p.hw);
+  } else {              // up to 64 heads per workgroup, 16 per wave
     p.hw = H > 32 ? 4 : (H > 16 ? 2 : 1);
     p.tw = 4 / p.hw;
+    p.hb = (H + 16 * p.hw - 1) / (16 * p.hw);
   }
-  p.hb = (H + 16 * p.hw - 1) / (16 * p.hw);
-  p.n_tok = top_k * attn->tokens_per_record;
   const int chunk = kChunk * p.tw;
   const int max_splits = (p.n_tok + chunk - 1) / chunk;
   int splits;
@@ -486,11 +894,12 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
     // the load pipeline reaches steady state
     const int per_split = units * p.hb;
     splits = (kTargetWorkgroups + per_split - 1) / per_split;
-    const int min_work_splits = std::max(1, p.n_tok / (4 * chunk));
+    const int min_work_splits = std::max(1, p.n_tok / ((is_mla(*attn) ? 2 : 4) * chunk));
     splits = std::max(1, std::min({splits, max_splits, min_work_splits}));
   }
   const int max_split_tokens = std::min(kMaxSplitRecords * attn->tokens_per_record, kMaxSplitTokens);
   splits = std::max(splits, (p.n_tok + max_split_tokens - 1) / max_split_tokens);
+  if (is_mla(*attn)) splits = std::min(splits, kMlaMaxParts);  // the merge keeps weights in LDS
   const int per = (p.n_tok + splits - 1) / splits;
   p.split_tokens = (per + chunk - 1) / chunk * chunk;
   if (p.split_tokens > max_split_tokens) p.split_tokens = max_split_tokens / chunk * chunk;
@@ -498,7 +907,8 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
   p.n_parts = p.n_wg_splits * p.tw;
   const int64_t n_wg = (int64_t)units * p.n_wg_splits * p.hb;
   if (n_wg > (1LL << 30)) return HISPARSE_ERR_INVALID_ARG;
-  const size_t o_bytes = (size_t)units * p.n_parts * H * attn->d_v * sizeof(float);
+  const int h_store = is_mla(*attn) ? (H + 31) / 32 * 32 : H;
+  const size_t o_bytes = (size_t)units * p.n_parts * h_store * attn->d_v * sizeof(float);
   const size_t ml_bytes = (size_t)units * p.n_parts * H * sizeof(float2);
   p.workspace_bytes = ((o_bytes + 255) & ~(size_t)255) + ml_bytes;
   *plan = p;
@@ -513,7 +923,8 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
   a.pool = pool;
   a.q = q;
   a.idx = idx;
-  const size_t o_bytes = (size_t)units * p.n_parts * attn.q_heads * attn.d_v * sizeof(float);
+  a.Hp = is_mla(attn) ? (attn.q_heads + 31) / 32 * 32 : attn.q_heads;
+  const size_t o_bytes = (size_t)units * p.n_parts * a.Hp * attn.d_v * sizeof(float);
   a.part_o = reinterpret_cast<float*>(workspace);
   a.part_ml = reinterpret_cast<float2*>(reinterpret_cast<uint8_t*>(workspace) +
                                         ((o_bytes + 255) & ~(size_t)255));
@@ -535,9 +946,9 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
 
   if (is_mla(attn)) {
     switch (p.hw) {
-      case 1: launch_partial<576, 512, 0, 1, 1, 2>(a, stream); break;
-      case 2: launch_partial<576, 512, 0, 2, 1, 4>(a, stream); break;
-      default: launch_partial<576, 512, 0, 4, 1, 4>(a, stream); break;
+      case 1: launch_mla<1, 3>(a, stream); break;
+      case 2: launch_mla<2, 4>(a, stream); break;
+      default: launch_mla<4, 4>(a, stream); break;
     }
   } else {
     switch (p.hw) {
@@ -548,12 +959,17 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (is_mla(attn)) {
+    const int nb = a.Hp / 32;
+    int chunks = 1;
+    while (chunks < 16 && (int64_t)units * nb * chunks < kTargetWorkgroups) chunks *= 2;
+    CombineMlaArgs c{a.part_o, a.part_ml, out, attn.q_heads, a.Hp, p.n_parts, chunks};
+    hipLaunchKernelGGL(attn_combine_mla_kernel, dim3(units * nb * chunks), dim3(256), 0, stream, c);
+    return hipGetLastError();
+  }
   CombineArgs c{a.part_o, a.part_ml, out, attn.q_heads, p.n_parts, units * attn.q_heads};
   const int n_cwg = (units * attn.q_heads + 3) / 4;
-  if (attn.d_v == 512)
-    hipLaunchKernelGGL(attn_combine_kernel<512>, dim3(n_cwg), dim3(256), 0, stream, c);
-  else
-    hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(n_cwg), dim3(256), 0, stream, c);
+  hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(n_cwg), dim3(256), 0, stream, c);
   return hipGetLastError();
 }
 

@@ -138,3 +138,54 @@ def test_attention_ragged_and_padding(kind, H, k, tpr, splits):
     out_p = decode_pool(torch.from_numpy(pool_p.view(np.int16)).to(dev), n_rec, w, q_d,
                         torch.from_numpy(idx_p).to(dev), ws, splits, units=units).cpu().numpy()
     assert out.tobytes() == out_p.tobytes()
+
+
+@pytest.mark.parametrize("kind,H,splits", [("mla", 128, 1), ("mla", 20, 2), ("gqa", 16, 1),
+                                           ("gqa", 64, 0)])
+def test_attention_wide_score_range(kind, H, splits):
+    """Scores that keep growing along the selection (by far more than the kernels' reference
+    slack within one split) exercise the rescale / exact-fallback paths: still within the
+    oracle's tolerance, still independent of placement."""
+    rng = np.random.default_rng(zlib.crc32(f"wide-{kind}-{H}-{splits}".encode()))
+    units = 2
+    if kind == "mla":
+        d_qk, d_v, voff, te, scale, tpr, k = 576, 512, 0, 576, 1 / np.sqrt(192), 1, 256
+        growth = slice(512, 576)      # the rope dims carry the growth; values stay N(0,1)
+    else:
+        d_qk, d_v, voff, te, scale, tpr, k = 128, 128, 128, 256, 1 / np.sqrt(128), 16, 16
+        growth = slice(0, 128)        # keys grow, values (dims 128..255) stay N(0,1)
+    n_rec = k + 21
+    R = te * tpr * 2
+    w = W.workload(1 if kind == "mla" else 3, q_heads=H, k=k, d_qk=d_qk, d_v=d_v, v_offset=voff,
+                   tokens_per_record=tpr, record_bytes=R, scale=float(scale))
+    pool_f = rng.standard_normal((units, n_rec, tpr, te)).astype(np.float32)
+    q_f = (0.1 * rng.standard_normal((units, H, d_qk))).astype(np.float32)
+    q_f[:, :, growth] = 1.0
+    idx = np.stack([rng.choice(n_rec, size=k, replace=False) for _ in range(units)]).astype(np.int32)
+    n_tok = k * tpr
+    for u in range(units):
+        for i in range(k):
+            t = i * tpr + np.arange(tpr)                    # selection-order token numbers
+            pool_f[u, idx[u, i], :, growth] = (t * (25.0 / n_tok))[:, None]
+    to_bf16 = lambda a: torch.from_numpy(a).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    pool = to_bf16(pool_f.reshape(units, n_rec, tpr * te))
+    q = to_bf16(q_f)
+    dev = torch.device("cuda:0")
+    ad = attn_desc(w, splits)
+    ws = torch.empty(hs.hisparse_decode_workspace_bytes(units, k, R, ad), dtype=torch.uint8,
+                     device=dev)
+    q_d = torch.from_numpy(q.view(np.int16)).to(dev)
+    out = decode_pool(torch.from_numpy(pool.view(np.int16)).to(dev), n_rec, w, q_d,
+                      torch.from_numpy(idx).to(dev), ws, splits, units=units).cpu().numpy()
+    for u in range(units):
+        ref = oracle_unit(w, q[u], pool[u], idx[u])
+        err, rl2 = np.abs(out[u] - ref).max(), rel_l2(out[u], ref)
+        log(f"  {kind} H={H} unit {u}: max-abs {err:.2e} rel-L2 {rl2:.2e}")
+        assert err <= MAX_ABS and rl2 <= REL_L2
+    perm = rng.permutation(n_rec)
+    inv = np.argsort(perm)
+    idx_p = inv[idx].astype(np.int32)
+    out_p = decode_pool(torch.from_numpy(np.ascontiguousarray(pool[:, perm]).view(np.int16)).to(dev),
+                        n_rec, w, q_d, torch.from_numpy(idx_p).to(dev), ws, splits,
+                        units=units).cpu().numpy()
+    assert out.tobytes() == out_p.tobytes()
