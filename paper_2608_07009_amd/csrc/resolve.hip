@@ -6,8 +6,11 @@
 //            position->slot table answers membership directly), mark hit slots in an LDS
 //            bitmap (a second mark on the same slot is a repeated entry), and append the
 //            misses as (position, input index) keys to LDS.
-//   Phase 2  sort the miss keys (LDS bitonic sort): ascending position order is what the
-//            canonical victim pairing needs, and equal neighbours expose repeated misses.
+//   Phase 2  put the miss keys in ascending position order (what the canonical victim
+//            pairing needs): a counting pass over 2048 buckets of high position bits gives
+//            each bucket's start, and a miss's rank is its bucket start plus the number of
+//            bucket mates at lower positions; a mate at the same position exposes a repeated
+//            miss. A few barriers in all, where a sorting network needs dozens.
 //   Phase 3  victims and recency: the unit keeps a recency index `order` = its slots sorted
 //            by (timestamp, slot). Victims are the first m entries of `order` that were not
 //            hit (one workgroup prefix scan); the new index is
@@ -26,6 +29,9 @@ namespace {
 
 constexpr int kWave = 64;
 constexpr int kMaxChunk = 16;  // order entries per thread: B <= 16 * threads
+constexpr int kMaxPer = 4;     // selections per thread: k <= 4 * threads
+constexpr int kBucketBits = 11;
+constexpr int kBuckets = 1 << kBucketBits;  // miss rank buckets (high position bits)
 
 __device__ inline int wave_incl_scan(int x, int lane) {
 #pragma unroll
@@ -58,31 +64,6 @@ __device__ inline int block_excl_scan(int v, int* s_tmp, int* total) {
   return r;
 }
 
-// Ascending bitonic sort of n (a power of two) 64-bit keys in LDS.
-template <int NT>
-__device__ inline void bitonic_sort(uint64_t* keys, int n) {
-  for (int size = 2; size <= n; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int idx = threadIdx.x; idx < (n >> 1); idx += NT) {
-        const int lo = ((idx & ~(stride - 1)) << 1) | (idx & (stride - 1));
-        const int hi = lo + stride;
-        const bool asc = (lo & size) == 0;
-        const uint64_t x = keys[lo], y = keys[hi];
-        if ((x > y) == asc) {
-          keys[lo] = y;
-          keys[hi] = x;
-        }
-      }
-      __syncthreads();
-    }
-  }
-}
-
-__host__ __device__ inline int pow2_at_least(int n) {
-  int p = 2;
-  while (p < n) p <<= 1;
-  return p;
-}
 
 __device__ inline bool bit_test(const uint32_t* bm, int s) { return (bm[s >> 5] >> (s & 31)) & 1u; }
 
@@ -96,15 +77,15 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   const int tid = threadIdx.x;
   const int k = a.k, B = a.B;
   const int64_t L = a.L;
-  const int p2k = pow2_at_least(k);
   const int k4 = (k + 3) & ~3;
   const int bw = (B + 31) >> 5;
 
-  uint64_t* s_keys = reinterpret_cast<uint64_t*>(s_dyn);   // [p2k] miss keys (pos << 32 | i)
-  int32_t* s_out = reinterpret_cast<int32_t*>(s_keys + p2k);  // [k4] slot per input index
+  uint64_t* s_keys = reinterpret_cast<uint64_t*>(s_dyn);   // [k4] miss keys (pos << 32 | i)
+  int32_t* s_out = reinterpret_cast<int32_t*>(s_keys + k4);  // [k4] slot per input index
   int32_t* s_victim = s_out + k4;                           // [k4] victim slot per miss rank
   uint32_t* s_hit = reinterpret_cast<uint32_t*>(s_victim + k4);  // [bw] slots hit this step
   uint32_t* s_vic = s_hit + bw;                             // [bw] slots taken as victims
+  int32_t* s_cnt = reinterpret_cast<int32_t*>(s_vic + bw);  // [kBuckets] miss rank buckets
 
   const int32_t* sel = a.sel + (int64_t)unit * k;
   int32_t* pt = a.pt + (int64_t)unit * L;
@@ -124,16 +105,27 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   }
   __syncthreads();
 
-  // Phase 1: stage, validate, probe.
-  for (int i = tid; i < k; i += NT) {
-    const int32_t p = sel[i];
-    int32_t out = -1;
-    if (p >= 0) {
-      if ((int64_t)p >= L) {
-        s_bad = 1;
-      } else {
-        const int32_t s = pt[p];
-        if (s >= 0) {
+  // Phase 1: stage, validate, probe. A thread handles at most kMaxPer selections (k <= 4 NT);
+  // all its selection reads, then all its page-table probes, are issued before any is used.
+  int32_t pv[kMaxPer], sv[kMaxPer];
+#pragma unroll
+  for (int u = 0; u < kMaxPer; ++u) {
+    const int i = tid + u * NT;
+    pv[u] = i < k ? sel[i] : -1;
+  }
+#pragma unroll
+  for (int u = 0; u < kMaxPer; ++u) sv[u] = (pv[u] >= 0 && (int64_t)pv[u] < L) ? pt[pv[u]] : -1;
+  for (int b = tid; b < kBuckets; b += NT) s_cnt[b] = 0;
+#pragma unroll
+  for (int u = 0; u < kMaxPer; ++u) {
+    const int i = tid + u * NT;
+    if (i < k) {
+      const int32_t p = pv[u], s = sv[u];
+      int32_t out = -1;
+      if (p >= 0) {
+        if ((int64_t)p >= L) {
+          s_bad = 1;
+        } else if (s >= 0) {
           const uint32_t bit = 1u << (s & 31);
           if (atomicOr(&s_hit[s >> 5], bit) & bit) s_bad = 1;  // repeated resident entry
           out = s;
@@ -142,19 +134,77 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
           s_keys[r] = ((uint64_t)(uint32_t)p << 32) | (uint32_t)i;
         }
       }
+      s_out[i] = out;
     }
-    s_out[i] = out;
   }
   __syncthreads();
   const int m = s_nmiss;
 
-  // Phase 2: misses in ascending position order; repeated misses become neighbours.
-  const int p2 = pow2_at_least(m);
-  for (int i = m + tid; i < p2; i += NT) s_keys[i] = ~0ull;
+  // Phase 2: the misses in ascending position order. Bucket them by their high position bits
+  // (a counting pass), then each miss's rank is its bucket's start plus the number of bucket
+  // mates at lower positions; a mate at the same position is a repeated selection.
+  const int lg = L > 1 ? 64 - __clzll((unsigned long long)(L - 1)) : 1;
+  const int shift = lg > kBucketBits ? lg - kBucketBits : 0;
+  const uint32_t low_mask = (1u << shift) - 1u;
+  uint64_t key[kMaxPer];
+  int bkt[kMaxPer], loc[kMaxPer];
+#pragma unroll
+  for (int u = 0; u < kMaxPer; ++u) {
+    const int j = tid + u * NT;
+    key[u] = j < m ? s_keys[j] : 0ull;
+    bkt[u] = (int)((key[u] >> 32) >> shift);
+    loc[u] = j < m ? atomicAdd(&s_cnt[bkt[u]], 1) : 0;
+  }
   __syncthreads();
-  bitonic_sort<NT>(s_keys, p2);
-  for (int r = 1 + tid; r < m; r += NT)
-    if ((s_keys[r] >> 32) == (s_keys[r - 1] >> 32)) s_bad = 1;
+  {
+    // exclusive scan of the bucket counts, kBuckets / NT consecutive buckets per thread
+    constexpr int per = (kBuckets + NT - 1) / NT;
+    int c[per], sum = 0;
+#pragma unroll
+    for (int q = 0; q < per; ++q) {
+      const int b = tid * per + q;
+      c[q] = b < kBuckets ? s_cnt[b] : 0;
+      sum += c[q];
+    }
+    int total;
+    int run = block_excl_scan<NT>(sum, s_tmp, &total);  // all reads of s_cnt precede it
+#pragma unroll
+    for (int q = 0; q < per; ++q) {
+      const int b = tid * per + q;
+      if (b < kBuckets) s_cnt[b] = run;
+      run += c[q];
+    }
+  }
+  __syncthreads();
+  // bucketed order in the victim array (free until phase 3): low position bits and input index
+  uint32_t* s_bkt = reinterpret_cast<uint32_t*>(s_victim);
+#pragma unroll
+  for (int u = 0; u < kMaxPer; ++u)
+    if (tid + u * NT < m)
+      s_bkt[s_cnt[bkt[u]] + loc[u]] = (((uint32_t)(key[u] >> 32) & low_mask) << 12) | (uint32_t)key[u];
+  __syncthreads();
+  int rank[kMaxPer];
+#pragma unroll
+  for (int u = 0; u < kMaxPer; ++u) {
+    rank[u] = 0;
+    if (tid + u * NT < m) {
+      const int b0 = s_cnt[bkt[u]];
+      const int b1 = bkt[u] + 1 < kBuckets ? s_cnt[bkt[u] + 1] : m;
+      const uint32_t mine = ((uint32_t)(key[u] >> 32) & low_mask);
+      int lower = 0;
+      for (int q = b0; q < b1; ++q) {
+        const uint32_t e = s_bkt[q];
+        const uint32_t lowp = e >> 12;
+        lower += lowp < mine ? 1 : 0;
+        if (lowp == mine && (e & 0xFFFu) != ((uint32_t)key[u] & 0xFFFu)) s_bad = 1;
+      }
+      rank[u] = b0 + lower;
+    }
+  }
+  __syncthreads();  // all reads of the unsorted keys are done
+#pragma unroll
+  for (int u = 0; u < kMaxPer; ++u)
+    if (tid + u * NT < m) s_keys[rank[u]] = key[u];
   __syncthreads();
 
   if (s_bad) {  // invalid selection: publish -1 and leave the unit's state untouched
@@ -338,14 +388,20 @@ hipError_t launch_resolve_nt(const ResolveArgs& a, size_t lds, hipStream_t strea
 
 size_t resolve_lds_bytes(int32_t k, int32_t B) {
   const size_t k4 = (size_t)((k + 3) & ~3);
-  return 8 * (size_t)pow2_at_least(k) + 8 * k4 + 8 * (size_t)((B + 31) >> 5);
+  return 16 * k4 + 8 * (size_t)((B + 31) >> 5) + 4 * (size_t)kBuckets;
+}
+
+int resolve_threads(int32_t B) {
+  int nt = 64;
+  while (nt < 1024 && nt * kMaxChunk < B) nt <<= 1;
+  while (nt < 1024 && nt * 4 < B) nt <<= 1;  // about four order entries per thread
+  return nt;
 }
 
 hipError_t launch_resolve(const ResolveArgs& a, hipStream_t stream) {
   const size_t lds = resolve_lds_bytes(a.k, a.B);
-  int nt = 64;
-  while (nt < 1024 && nt * kMaxChunk < a.B) nt <<= 1;
-  while (nt < 1024 && nt * 4 < a.B) nt <<= 1;  // about four order entries per thread
+  const int nt = resolve_threads(a.B);
+  if (a.k > kMaxPer * nt) return hipErrorInvalidValue;  // excluded by descriptor validation
   switch (nt) {
     case 64: return launch_resolve_nt<64>(a, lds, stream);
     case 128: return launch_resolve_nt<128>(a, lds, stream);

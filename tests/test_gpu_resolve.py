@@ -10,7 +10,7 @@ import torch
 import oracle
 import workload as W
 from hs_harness import Run, expected_order, layer_cache_host, log
-from paper_2608_07009_amd import hisparse as hs
+from paper_2608_07009_amd import HiSparseCache, hisparse as hs
 
 pytestmark = pytest.mark.gpu
 
@@ -105,3 +105,54 @@ def test_sdma_fetch_matches_zero_copy(cfg, steps):
     finally:
         a.close()
         b.close()
+
+
+def test_resolve_padding_and_bad_selections():
+    """Padding entries, repeated entries (resident and not) and out-of-range positions, on the
+    device: bad units keep their state, publish -1 slots and (0, 0) counts, and the first error
+    is latched; every other unit stays bit-exact with the oracle throughout."""
+    U, L, B, k, steps = 4, 4096, 256, 96, 12
+    rng = np.random.default_rng(20261202)
+    dev = torch.device("cuda:0")
+    cache = HiSparseCache(num_requests=U, num_layers=1, units_per_request=1, capacity=B,
+                          num_records=L, top_k=k, record_bytes=64, fetch=hs.HISPARSE_FETCH_NONE)
+    orc = oracle.OracleCache(U, L, B, k)
+    slots = torch.empty((U, k), dtype=torch.int32, device=dev)
+    counts = torch.empty((U, 2), dtype=torch.int32, device=dev)
+    prev = None
+    injected = []
+    try:
+        for t in range(steps):
+            # a drifting window keeps some entries resident from step to step
+            sel = np.stack([rng.choice(np.arange(64 * t, 64 * t + 400), size=k, replace=False)
+                            for _ in range(U)]).astype(np.int32)
+            sel[1, 5:15] = -1                           # padding in every step
+            if t == 3:
+                sel[0, 7] = sel[0, 8]                   # repeated entry
+                injected.append((t, 0))
+            if t == 5 and prev is not None:
+                sel[2, :2] = prev[2, 0]                 # repeated entry resident from last step
+                injected.append((t, 2))
+            if t == 7:
+                sel[3, 40] = L + 5                      # beyond the records
+                injected.append((t, 3))
+            sel_d = torch.from_numpy(sel).to(dev)
+            hs.hisparse_resolve_tables(cache.handle, 0, sel_d, slots, counts,
+                                       torch.cuda.current_stream())
+            e_slots, e_counts, _, _, n_bad = orc.resolve(sel)
+            got_s, got_c = slots.cpu().numpy(), counts.cpu().numpy()
+            assert (got_s == e_slots).all(), f"slots step {t}"
+            assert (got_c == e_counts).all(), f"counts step {t}"
+            for (ti, u) in injected:
+                if ti == t:
+                    assert n_bad >= 1 and (got_s[u] == -1).all() and (got_c[u] == 0).all()
+            prev = sel
+        st = cache.read_state(0)
+        assert (st["slot_pos"] == orc.slot_pos).all() and (st["slot_ts"] == orc.slot_ts).all()
+        assert (st["page_table"] == orc.pt).all() and (st["clock"] == orc.clock).all()
+        code, info = cache.check_errors()
+        assert code == hs.HISPARSE_ERR_BAD_SELECTION
+        assert info[0] == 0 and info[1] == 0     # first latched error: layer 0, unit 0 (step 3)
+        assert info[2] == len(injected)
+    finally:
+        cache.close()
