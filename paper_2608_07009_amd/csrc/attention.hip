@@ -772,20 +772,24 @@ struct CombineMlaArgs {
   const float* part_o;    // [units][n_parts][Hp * 512], block layout
   const float2* part_ml;  // [units][n_parts][H]
   float* out;             // [units][H][512]
-  int32_t H, Hp, n_parts, chunks;  // chunks: workgroups per (unit, 32-head block)
+  int32_t H, Hp, n_parts;
 };
 
-// Merge of latent-attention partials: one workgroup per (unit, 32-head block, slice of the
-// block). Weights w_ph = 2^(m_ph - M_h) and L_h = sum_p w_ph l_ph first (in LDS), then each
-// thread reduces whole 16-byte groups of the block layout over the parts in split order.
+// Merge of latent-attention partials: one workgroup per (unit, 32-head block, 256 / NS of the
+// block's 4096 16-byte groups). Weights w_ph = 2^(m_ph - M_h) and L_h = sum_p w_ph l_ph first
+// (in LDS); then thread (slice s, group g) sums parts p = s, s + NS, ... of group g, and the NS
+// slice sums are added in slice order (NS > 1 puts more loads in flight when units are few).
+template <int NS>
 __global__ __launch_bounds__(256) void attn_combine_mla_kernel(CombineMlaArgs a) {
-  constexpr int DV = 512, BLK4 = 32 * DV / 4;  // float4 groups per 32-head block
+  constexpr int DV = 512, BLK4 = 32 * DV / 4, GPW = 256 / NS;
   __shared__ __align__(16) float s_w[kMlaMaxParts][32];
   __shared__ float s_inv[32];
+  __shared__ __align__(16) f32x4 s_acc[NS][GPW];
+  constexpr int chunks = BLK4 / GPW;
   const int nb = a.Hp >> 5;
-  const int chunk = blockIdx.x % a.chunks;
-  const int b = (blockIdx.x / a.chunks) % nb;
-  const int unit = blockIdx.x / (a.chunks * nb);
+  const int chunk = blockIdx.x % chunks;
+  const int b = (blockIdx.x / chunks) % nb;
+  const int unit = blockIdx.x / (chunks * nb);
   const int t = threadIdx.x, hl = t >> 3, sub = t & 7;
   const int head = b * 32 + hl;
   const int np = a.n_parts;
@@ -810,29 +814,35 @@ __global__ __launch_bounds__(256) void attn_combine_mla_kernel(CombineMlaArgs a)
   if (sub == 0) s_inv[hl] = lsum > 0.f ? 1.f / lsum : 0.f;
   __syncthreads();
 
-  const int per = BLK4 / a.chunks;  // groups of this workgroup
+  const int g = t % GPW, sl = t / GPW;
+  const int f = chunk * GPW + g;  // 16-byte group within the block
+  const int ln = f & 63, q = (f >> 6) & 3, n = f >> 8;
+  const int h0 = 8 * q + 4 * (ln >> 5);  // first of the group's four heads (block-local)
   const int64_t pstride = (int64_t)a.Hp * DV;
-  const float* pb = a.part_o + (int64_t)unit * np * pstride + (int64_t)b * 32 * DV;
-  for (int f = chunk * per + t; f < (chunk + 1) * per; f += 256) {
-    const int ln = f & 63, q = (f >> 6) & 3, n = f >> 8;
-    const int h0 = 8 * q + 4 * (ln >> 5);  // first of the group's four heads (block-local)
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    int p = 0;
-    for (; p + 4 <= np; p += 4) {
-      f32x4 v[4];
+  const float* pb = a.part_o + (int64_t)unit * np * pstride + (int64_t)b * 32 * DV + 4 * f;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  int p = sl;
+  for (; p + 3 * NS < np; p += 4 * NS) {
+    f32x4 v[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const f32x4*>(pb + (p + u) * pstride + 4 * f);
+    for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const f32x4*>(pb + (p + u * NS) * pstride);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) acc += *reinterpret_cast<const f32x4*>(&s_w[p + u][h0]) * v[u];
-    }
-    for (; p < np; ++p)
-      acc += *reinterpret_cast<const f32x4*>(&s_w[p][h0]) *
-             *reinterpret_cast<const f32x4*>(pb + p * pstride + 4 * f);
+    for (int u = 0; u < 4; ++u)
+      acc += *reinterpret_cast<const f32x4*>(&s_w[p + u * NS][h0]) * v[u];
+  }
+  for (; p < np; p += NS)
+    acc += *reinterpret_cast<const f32x4*>(&s_w[p][h0]) * *reinterpret_cast<const f32x4*>(pb + p * pstride);
+  s_acc[sl][g] = acc;
+  __syncthreads();
+  if (sl == 0) {
+    f32x4 r = s_acc[0][g];
+#pragma unroll
+    for (int s2 = 1; s2 < NS; ++s2) r += s_acc[s2][g];
     const int dim = 32 * n + (ln & 31);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int h = b * 32 + h0 + e;
-      if (h < a.H) a.out[((int64_t)unit * a.H + h) * DV + dim] = acc[e] * s_inv[h0 + e];
+      if (h < a.H) a.out[((int64_t)unit * a.H + h) * DV + dim] = r[e] * s_inv[h0 + e];
     }
   }
 }
@@ -866,17 +876,14 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
   AttnPlan p{};
   p.n_tok = top_k * attn->tokens_per_record;
   if (is_mla(*attn)) {
-    // 32 heads per wave, up to 4 waves (128 heads) per workgroup: the most heads per staged
-    // chunk that still gives about a workgroup per CU with at least two chunks per split
+    // 32 heads per wave, up to 4 waves (128 heads) per workgroup when that still gives about
+    // a workgroup per CU with at least two chunks per split; otherwise 2 waves, which measured
+    // faster than 1 or 4 for a single 128-head unit (more loads in flight per CU than 1 wave,
+    // twice the workgroups of 4)
     const int64_t split_cap = std::max(1, p.n_tok / (2 * kChunk));
-    p.hw = 1;
-    for (int nw : {4, 2}) {
-      const int64_t hb = (H + 32 * nw - 1) / (32 * nw);
-      if (32 * (nw / 2) < H && (int64_t)units * hb * split_cap >= kTargetWorkgroups) {
-        p.hw = nw;
-        break;
-      }
-    }
+    if (H <= 32) p.hw = 1;
+    else if (H > 64 && (int64_t)units * ((H + 127) / 128) * split_cap >= kTargetWorkgroups) p.hw = 4;
+    else p.hw = 2;
     p.tw = 1;
     p.hb = (H + 32 * p.hw - 1) / (32 * p.hw);
   } else {              // up to 64 heads per workgroup, 16 per wave
@@ -961,10 +968,11 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
   if (e != hipSuccess) return e;
   if (is_mla(attn)) {
     const int nb = a.Hp / 32;
-    int chunks = 1;
-    while (chunks < 16 && (int64_t)units * nb * chunks < kTargetWorkgroups) chunks *= 2;
-    CombineMlaArgs c{a.part_o, a.part_ml, out, attn.q_heads, a.Hp, p.n_parts, chunks};
-    hipLaunchKernelGGL(attn_combine_mla_kernel, dim3(units * nb * chunks), dim3(256), 0, stream, c);
+    CombineMlaArgs c{a.part_o, a.part_ml, out, attn.q_heads, a.Hp, p.n_parts};
+    if ((int64_t)units * nb * 16 >= 2 * kTargetWorkgroups)
+      hipLaunchKernelGGL(attn_combine_mla_kernel<1>, dim3(units * nb * 16), dim3(256), 0, stream, c);
+    else
+      hipLaunchKernelGGL(attn_combine_mla_kernel<4>, dim3(units * nb * 64), dim3(256), 0, stream, c);
     return hipGetLastError();
   }
   CombineArgs c{a.part_o, a.part_ml, out, attn.q_heads, p.n_parts, units * attn.q_heads};
