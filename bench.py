@@ -54,6 +54,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run one device-to-device copy of BYTES (calibrates the HBM "
+                         "byte counters of a profiler run) and exit")
     return ap.parse_args()
 
 
@@ -113,6 +116,29 @@ def pinned_sweep(torch, hip: Hip, host_ptr: int, host_bytes: int, dev, stream: i
     return res
 
 
+def traffic_record(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` on `workload`, from the rocprofv3 FETCH_SIZE and
+    WRITE_SIZE runs summarised under profiles/ (counter values already scaled by a plain copy
+    of known size), or None when no summary matches the current source of that kernel."""
+    import glob
+    import hashlib
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        for line in open(path):
+            if not line.startswith("traffic-record "):
+                continue
+            kv = dict(f.split("=", 1) for f in line.split()[1:])
+            if kv.get("workload") != workload or kv.get("kernel") != kernel:
+                continue
+            src = os.path.join(ROOT, kv["source"])
+            if not os.path.exists(src):
+                continue
+            if hashlib.sha256(open(src, "rb").read()).hexdigest() != kv.get("sha256"):
+                continue  # the kernel changed since the counters were taken
+            return {"fetch_bytes": int(kv["fetch_bytes"]), "write_bytes": int(kv["write_bytes"]),
+                    "profile": os.path.relpath(path, ROOT)}
+    return None
+
+
 def union_length(intervals) -> float:
     total, end = 0.0, None
     for a, b in sorted(intervals):
@@ -169,6 +195,18 @@ def main() -> int:
 
     import numpy as np
     import torch
+
+    if args.copy_probe:
+        if not torch.cuda.is_available():
+            print(json.dumps({"error": "no GPU visible"}))
+            return 1
+        src = torch.ones(args.copy_probe, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": args.copy_probe}))
+        return 0
 
     import workload as W
     from paper_2608_07009_amd import HiSparseCache, hisparse as hs
@@ -421,9 +459,14 @@ def main() -> int:
     dom = max(totals, key=totals.get)
     if dom in ("fetch", "prefetch_replay"):
         kd = kernels[dom]
+        tr = traffic_record(w.name, "fetch")
+        if tr:
+            tr["read_vs_algorithmic"] = tr["fetch_bytes"] / kd["bytes_per_launch"]
+            tr["write_vs_algorithmic"] = tr["write_bytes"] / kd["bytes_per_launch"]
         roof = {"kernel": dom, "bound": "host_link", "achieved": kd["GBps"],
                 "peak": PCIE_PEAK_GBPS, "unit": "GB/s", "frac": kd["GBps"] / PCIE_PEAK_GBPS,
-                "traffic": None, "measured_pinned_h2d_peak": pinned_peak,
+                "traffic": (tr["fetch_bytes"] + tr["write_bytes"]) if tr else None,
+                "traffic_detail": tr, "measured_pinned_h2d_peak": pinned_peak,
                 "frac_of_measured_peak": (kd["GBps"] / pinned_peak) if pinned_peak else None,
                 "algorithmic_bytes_per_launch": kd["bytes_per_launch"]}
     elif dom == "sparse_decode":

@@ -180,6 +180,13 @@ hisparse_status_t hisparse_resolve_tables(hisparse_cache_t cache, int32_t layer,
                                           int32_t* d_counts, void* stream);
 hisparse_status_t hisparse_fetch(hisparse_cache_t cache, int32_t layer, void* stream);
 
+/* [async] Phase 4 for units [unit_begin, unit_begin + unit_count) of an anchor layer only
+ * (Section 3.4; units are independent caches). Calls over disjoint ranges together equal
+ * hisparse_fetch, so a caller can pipeline a layer's fetch with the attention of the units
+ * already fetched. HISPARSE_ERR_INVALID_ARG for a range outside [0, units). */
+hisparse_status_t hisparse_fetch_units(hisparse_cache_t cache, int32_t layer,
+                                       int32_t unit_begin, int32_t unit_count, void* stream);
+
 /* [async] Exact prefetch (Section 3.5): replay the miss plan recorded by the latest resolve of
  * `anchor_layer` into the cache of `shared_layer` (anchor < shared < anchor + share_group),
  * copying each planned record from shared_layer's own host pool into the same slot. After the

@@ -305,8 +305,9 @@ namespace {
 // Copy the records of `anchor`'s latest miss plan from `target`'s host pool into `target`'s
 // GPU cache (target == anchor: the demand fetch; target a shared layer: the prefetch replay).
 hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t target,
-                                hipStream_t stream) {
-  if (c->desc.fetch == HISPARSE_FETCH_NONE) return HISPARSE_OK;
+                                hipStream_t stream, int32_t u0 = 0, int32_t nu = -1) {
+  if (nu < 0) nu = c->units - u0;
+  if (c->desc.fetch == HISPARSE_FETCH_NONE || nu == 0) return HISPARSE_OK;
   auto& an = c->anchors[anchor / c->desc.share_group];
   if (c->desc.fetch == HISPARSE_FETCH_SDMA) {
     hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
@@ -319,12 +320,13 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
                        stream) != hipSuccess ||
         hipStreamSynchronize(stream) != hipSuccess)
       return HISPARSE_ERR_HIP;
+    const size_t u_end = (size_t)u0 + (size_t)nu;
     const size_t R = (size_t)c->desc.record_bytes, L = (size_t)c->desc.num_records;
     const size_t B = (size_t)c->desc.capacity;
     uint8_t* host = reinterpret_cast<uint8_t*>(c->host[target]);
     uint8_t* cache = c->cache[target];
     size_t n = 0;
-    for (size_t u = 0; u < U; ++u) {
+    for (size_t u = (size_t)u0; u < u_end; ++u) {
       const int2* pl = c->h_plan + u * K;
       for (int32_t i = 0; i < c->h_plan_count[u]; ++i) {
         uint8_t* src = host + (u * L + (size_t)pl[i].x) * R;
@@ -357,15 +359,16 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
     return HISPARSE_OK;
   }
   hisparse::FetchArgs f{};
-  f.plan = an.plan;
-  f.plan_count = an.plan_count;
-  f.host = reinterpret_cast<const uint8_t*>(c->host_dev[target]);
-  f.cache = c->cache[target];
-  f.L = c->desc.num_records;
-  f.B = c->desc.capacity;
+  const int64_t L = c->desc.num_records, B = c->desc.capacity, R = c->desc.record_bytes;
+  f.plan = an.plan + (int64_t)u0 * c->desc.top_k;
+  f.plan_count = an.plan_count + u0;
+  f.host = reinterpret_cast<const uint8_t*>(c->host_dev[target]) + (int64_t)u0 * L * R;
+  f.cache = c->cache[target] + (int64_t)u0 * B * R;
+  f.L = L;
+  f.B = (int32_t)B;
   f.k = c->desc.top_k;
-  f.R = c->desc.record_bytes;
-  f.units = c->units;
+  f.R = (int32_t)R;
+  f.units = nu;
   if (hisparse::launch_fetch(f, transfer_block(c->desc), stream) != hipSuccess)
     return HISPARSE_ERR_HIP;
   return HISPARSE_OK;
@@ -375,6 +378,14 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
 hisparse_status_t hisparse_fetch(hisparse_cache_t c, int32_t layer, void* stream) {
   if (!c || !is_anchor(c, layer)) return HISPARSE_ERR_INVALID_ARG;
   return enqueue_fetch(c, layer, layer, as_stream(stream));
+}
+
+hisparse_status_t hisparse_fetch_units(hisparse_cache_t c, int32_t layer, int32_t unit_begin,
+                                       int32_t unit_count, void* stream) {
+  if (!c || !is_anchor(c, layer) || unit_begin < 0 || unit_count < 0 ||
+      unit_count > c->units - unit_begin)
+    return HISPARSE_ERR_INVALID_ARG;
+  return enqueue_fetch(c, layer, layer, as_stream(stream), unit_begin, unit_count);
 }
 
 hisparse_status_t hisparse_resolve(hisparse_cache_t c, int32_t layer, const int32_t* d_sel,

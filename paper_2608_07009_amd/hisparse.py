@@ -36,7 +36,7 @@ EXPORTED = (
     "hisparse_status_string", "hisparse_validate_desc", "hisparse_validate_attn",
     "hisparse_cache_create", "hisparse_cache_destroy", "hisparse_host_pool",
     "hisparse_layer_cache", "hisparse_reset", "hisparse_resolve", "hisparse_resolve_tables",
-    "hisparse_fetch", "hisparse_prefetch_layer",
+    "hisparse_fetch", "hisparse_fetch_units", "hisparse_prefetch_layer",
     "hisparse_decode_workspace_bytes", "hisparse_sparse_decode", "hisparse_sparse_decode_pool",
     "hisparse_read_state", "hisparse_read_plan", "hisparse_check_errors",
 )
@@ -91,6 +91,7 @@ def lib() -> ctypes.CDLL:
             "hisparse_resolve": (_I32, [_V, _I32, _V, _V, _V, _V]),
             "hisparse_resolve_tables": (_I32, [_V, _I32, _V, _V, _V, _V]),
             "hisparse_fetch": (_I32, [_V, _I32, _V]),
+            "hisparse_fetch_units": (_I32, [_V, _I32, _I32, _I32, _V]),
             "hisparse_prefetch_layer": (_I32, [_V, _I32, _I32, _V]),
             "hisparse_decode_workspace_bytes": (ctypes.c_size_t, [_I32, _I32, _I32,
                                                                   ctypes.POINTER(AttnDesc)]),
@@ -190,6 +191,12 @@ def hisparse_resolve_tables(cache: int, layer: int, d_sel, d_slots, d_counts=Non
 
 def hisparse_fetch(cache: int, layer: int, stream=None) -> None:
     _check("hisparse_fetch", lib().hisparse_fetch(cache, layer, _s(stream)))
+
+
+def hisparse_fetch_units(cache: int, layer: int, unit_begin: int, unit_count: int,
+                         stream=None) -> None:
+    _check("hisparse_fetch_units",
+           lib().hisparse_fetch_units(cache, layer, unit_begin, unit_count, _s(stream)))
 
 
 def hisparse_prefetch_layer(cache: int, anchor_layer: int, shared_layer: int,

@@ -156,3 +156,35 @@ def test_resolve_padding_and_bad_selections():
         assert info[2] == len(injected)
     finally:
         cache.close()
+
+
+def test_fetch_units_ranges_equal_whole_fetch():
+    """Phase 4 over disjoint unit ranges (ragged, one empty) leaves every slot of every unit
+    byte-identical to one whole-layer fetch; ranges outside [0, units) are argument errors."""
+    w = W.workload(3, num_layers=1)
+    steps = 6
+    log(f"test_fetch_units_ranges_equal_whole_fetch {w.name} units={w.units}")
+    whole = Run(w, steps)
+    parts = Run(w, steps)
+    try:
+        ranges = [(0, 5), (5, 0), (5, 25), (30, w.units - 30)]
+        for t in range(steps):
+            hs.hisparse_resolve_tables(whole.cache.handle, 0, whole.sel_ptr(t, 0), whole.slots[0],
+                                       whole.counts[0], whole.stream)
+            hs.hisparse_fetch(whole.cache.handle, 0, whole.stream)
+            hs.hisparse_resolve_tables(parts.cache.handle, 0, parts.sel_ptr(t, 0), parts.slots[0],
+                                       parts.counts[0], parts.stream)
+            for u0, n in ranges:
+                hs.hisparse_fetch_units(parts.cache.handle, 0, u0, n, parts.stream)
+        assert torch.equal(whole.slots, parts.slots)
+        a, b = layer_cache_host(whole, 0), layer_cache_host(parts, 0)
+        orc_state = whole.cache.read_state(0, page_table=False)
+        for u in range(w.units):
+            res = np.nonzero(orc_state["slot_pos"][u] >= 0)[0]
+            assert (a[u, res] == b[u, res]).all(), f"unit {u}"
+        for u0, n in [(-1, 2), (0, w.units + 1), (w.units, 1)]:
+            with pytest.raises(hs.HisparseError):
+                hs.hisparse_fetch_units(parts.cache.handle, 0, u0, n, parts.stream)
+    finally:
+        whole.close()
+        parts.close()
