@@ -54,6 +54,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--side-stream-replay", action="store_true",
+                    help="shared layers: replay on a side stream overlapped with the anchor's "
+                         "attention (default: the group's fetch and replays in one launch, then "
+                         "one attention launch for the group)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run one device-to-device copy of BYTES (calibrates the HBM "
                          "byte counters of a profiler run) and exit")
@@ -252,7 +256,10 @@ def main() -> int:
     ad = hs.AttnDesc(w.q_heads, w.d_qk, w.d_v, w.v_offset, w.tokens_per_record, args.splits,
                      w.scale, 0)
     ad_ref = ctypes.byref(ad)
-    ws_bytes = hs.hisparse_decode_workspace_bytes(U, k, w.record_bytes, ad)
+    # the shared layers of a group are decoded in one launch once their replays have landed
+    ws_bytes = max(hs.hisparse_decode_workspace_bytes(n * U, k, w.record_bytes, ad)
+                   for n in range(1, G + 1)) if G > 1 else 0
+    ws_bytes = max(ws_bytes, hs.hisparse_decode_workspace_bytes(U, k, w.record_bytes, ad))
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     out = torch.empty((w.num_layers, U, w.q_heads, w.d_v), dtype=torch.float32, device=dev)
     h = cache.handle
@@ -268,6 +275,7 @@ def main() -> int:
     groups = [(a, list(range(a + 1, min(a + G, w.num_layers)))) for a in w.anchors]
     f_tables, f_fetch = L.hisparse_resolve_tables, L.hisparse_fetch
     f_prefetch, f_decode = L.hisparse_prefetch_layer, L.hisparse_sparse_decode
+    f_decode_layers, f_fetch_group = L.hisparse_sparse_decode_layers, L.hisparse_fetch_group
     rec = hip.L.hipEventRecord
     wait = hip.L.hipStreamWaitEvent
     sync_events = [hip.event(timing=False) for _ in range(2 * G)]
@@ -291,6 +299,24 @@ def main() -> int:
                 spans.append(("resolve_tables", e0, e1))
             else:
                 check(f_tables(h, a, sp, slot_p[a], cp or None, main_s), "resolve_tables")
+            if shared and not args.side_stream_replay:
+                # nothing else to overlap the replays with: the anchor's fetch and its shared
+                # layers' replays in one launch, then one attention launch for the group
+                if ev is not None:
+                    e0, e1 = ev.pop(), ev.pop()
+                    rec(e0, main_s)
+                check(f_fetch_group(h, a, 1 + len(shared), main_s), "fetch_group")
+                if ev is not None:
+                    rec(e1, main_s)
+                    spans.append(("fetch_group", e0, e1))
+                    e0, e1 = ev.pop(), ev.pop()
+                    rec(e0, main_s)
+                check(f_decode_layers(h, a, 1 + len(shared), qv[a], slot_p[a], out_p[a],
+                                      ad_ref, ws_p, ws_bytes, main_s), "sparse_decode_layers")
+                if ev is not None:
+                    rec(e1, main_s)
+                    spans.append(("sparse_decode_layers", e0, e1))
+                continue
             # the anchor's own fetch goes first and alone on the host link (its attention is
             # next); the shared layers' replays follow back to back on the side stream, each
             # releasing its layer's attention as soon as it lands
@@ -326,18 +352,17 @@ def main() -> int:
                     else:
                         check(f_prefetch(h, a, s, side_s), "prefetch_layer")
                     rec(sync_events[1 + i], side_s)
-            for i, s in enumerate(shared):
-                wait(main_s, sync_events[1 + i], 0)
+            if shared:
+                wait(main_s, sync_events[len(shared)], 0)  # the last replay has landed
                 if ev is not None:
                     e0, e1 = ev.pop(), ev.pop()
                     rec(e0, main_s)
-                    check(f_decode(h, s, qv[s], slot_p[a], out_p[s], ad_ref, ws_p, ws_bytes,
-                                   main_s), "sparse_decode")
+                check(f_decode_layers(h, shared[0], len(shared), qv[shared[0]], slot_p[a],
+                                      out_p[shared[0]], ad_ref, ws_p, ws_bytes, main_s),
+                      "sparse_decode_layers")
+                if ev is not None:
                     rec(e1, main_s)
-                    spans.append(("sparse_decode", e0, e1))
-                else:
-                    check(f_decode(h, s, qv[s], slot_p[a], out_p[s], ad_ref, ws_p, ws_bytes,
-                                   main_s), "sparse_decode")
+                    spans.append(("sparse_decode_layers", e0, e1))
 
     # pinned H2D sweep over the same pool (hipMemcpyAsync), before the timed region
     sweep = {}
@@ -363,7 +388,8 @@ def main() -> int:
     # spin), so the host is ahead of the GPU for the whole pass and each event pair brackets
     # its kernel, not a host launch gap. Its GPU time per step is reported beside the timed
     # region's.
-    per_step_events = sum(6 + 4 * len(sh) for _, sh in groups)
+    per_step_events = sum((6 if (sh and not args.side_stream_replay) else
+                           6 + 2 * len(sh) + (2 if sh else 0)) for _, sh in groups)
     events = [hip.event() for _ in range(per_step_events * args.steps)]
     ref, end = hip.event(), hip.event()
     spans = []
@@ -392,7 +418,7 @@ def main() -> int:
         d = hip.ms(e0, e1) * 1e-3
         t_sum, n = tot.get(name, (0.0, 0))
         tot[name] = (t_sum + d, n + 1)
-        if name in ("fetch", "prefetch_replay"):
+        if name in ("fetch", "prefetch_replay", "fetch_group"):
             io_intervals.append((hip.ms(ref, e0) * 1e-3, hip.ms(ref, e1) * 1e-3))
     for e in events:
         hip.L.hipEventDestroy(e)
@@ -418,8 +444,20 @@ def main() -> int:
     t_fet, n_fet = kernel("fetch")
     t_rep, n_rep = kernel("prefetch_replay")
     t_att, n_att = kernel("sparse_decode")
-    fetch_bytes = misses_anchor * R
-    replay_bytes = misses_replay * R
+    # shared layers are decoded in batched launches; attention is accounted per layer call
+    t_lay, n_lay = kernel("sparse_decode_layers")
+    per_batch = (lambda sh: len(sh)) if args.side_stream_replay else (lambda sh: 1 + len(sh))
+    lay_calls = K * sum(per_batch(sh) for _, sh in groups if sh) if n_lay else 0
+    t_grp, n_grp = kernel("fetch_group")
+    t_att_one, n_att_one = t_att, n_att
+    t_att, n_att = t_att + t_lay, n_att + lay_calls
+    grouped = [a for a, sh in groups if sh and not args.side_stream_replay]
+    misses_grouped = int(c[:, grouped, :, 1].sum()) if grouped else 0
+    fetch_bytes = (misses_anchor - misses_grouped) * R      # plain demand fetches
+    replay_bytes = misses_replay * R                        # replays into shared layers
+    group_bytes = (misses_grouped * R + replay_bytes) if grouped else 0
+    if grouped:
+        replay_bytes = 0  # carried by the group launches
     moves_data = fetch != hs.HISPARSE_FETCH_NONE
     kernels = {}
     # resolve tables: integer metadata work per unit (algorithmic bytes):
@@ -435,6 +473,11 @@ def main() -> int:
         kernels["fetch"] = {"launches": n_fet, "avg_us": t_fet / n_fet * 1e6,
                             "bytes_per_launch": fetch_bytes / n_fet,
                             "GBps": fetch_bytes / t_fet / 1e9}
+    if n_grp and moves_data:
+        kernels["fetch_group"] = {"launches": n_grp, "avg_us": t_grp / n_grp * 1e6,
+                                  "layers_per_launch": 1 + len(groups[0][1]),
+                                  "bytes_per_launch": group_bytes / n_grp,
+                                  "GBps": group_bytes / t_grp / 1e9}
     if n_rep and moves_data:
         kernels["prefetch_replay"] = {"launches": n_rep, "avg_us": t_rep / n_rep * 1e6,
                                       "bytes_per_launch": replay_bytes / n_rep,
@@ -452,14 +495,22 @@ def main() -> int:
             "mfma_TFLOPs": att_flops_call / a_time / 1e12,
             "hbm_frac": att_bytes_call / a_time / 1e9 / HBM_PEAK_GBPS,
             "mfma_frac": att_flops_call / a_time / 1e12 / MFMA_BF16_PEAK_TFLOPS}
+        if n_lay:
+            kernels["sparse_decode"].update({
+                "per": "layer call (shared layers share one launch per group)",
+                "single_layer_launches": n_att_one,
+                "single_layer_avg_us": t_att_one / max(1, n_att_one) * 1e6,
+                "batched_launches": n_lay, "batched_layers": lay_calls,
+                "batched_avg_us": t_lay / n_lay * 1e6})
 
     # dominant kernel by total event time
     totals = {"resolve_tables": t_tab, "fetch": t_fet if moves_data else 0.0,
-              "prefetch_replay": t_rep if moves_data else 0.0, "sparse_decode": t_att}
+              "prefetch_replay": t_rep if moves_data else 0.0,
+              "fetch_group": t_grp if moves_data else 0.0, "sparse_decode": t_att}
     dom = max(totals, key=totals.get)
-    if dom in ("fetch", "prefetch_replay"):
+    if dom in ("fetch", "prefetch_replay", "fetch_group"):
         kd = kernels[dom]
-        tr = traffic_record(w.name, "fetch")
+        tr = traffic_record(w.name, dom)
         if tr:
             tr["read_vs_algorithmic"] = tr["fetch_bytes"] / kd["bytes_per_launch"]
             tr["write_vs_algorithmic"] = tr["write_bytes"] / kd["bytes_per_launch"]
@@ -487,7 +538,8 @@ def main() -> int:
                 "unit": "GB/s", "frac": kd["hbm_GBps"] / HBM_PEAK_GBPS, "traffic": None}
 
     io_busy = union_length(io_intervals)
-    miss_gbps = (fetch_bytes + replay_bytes) / io_busy / 1e9 if (io_busy and moves_data) else None
+    miss_gbps = ((fetch_bytes + replay_bytes + group_bytes) / io_busy / 1e9
+                 if (io_busy and moves_data) else None)
 
     # the same steps replayed from one captured HIP graph (cold reset, same warmup)
     graph = None

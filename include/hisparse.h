@@ -187,6 +187,14 @@ hisparse_status_t hisparse_fetch(hisparse_cache_t cache, int32_t layer, void* st
 hisparse_status_t hisparse_fetch_units(hisparse_cache_t cache, int32_t layer,
                                        int32_t unit_begin, int32_t unit_count, void* stream);
 
+/* [async] Phase 4 of an anchor layer and the exact-prefetch replay of the same miss plan into
+ * its next num_layers - 1 shared layers (Section 3.5), in one launch: equal to hisparse_fetch
+ * followed by hisparse_prefetch_layer for each of those layers, for a caller with nothing to
+ * overlap the replays with. HISPARSE_ERR_INVALID_ARG unless 1 <= num_layers <= share_group and
+ * the layers exist. */
+hisparse_status_t hisparse_fetch_group(hisparse_cache_t cache, int32_t anchor_layer,
+                                       int32_t num_layers, void* stream);
+
 /* [async] Exact prefetch (Section 3.5): replay the miss plan recorded by the latest resolve of
  * `anchor_layer` into the cache of `shared_layer` (anchor < shared < anchor + share_group),
  * copying each planned record from shared_layer's own host pool into the same slot. After the
@@ -218,6 +226,23 @@ hisparse_status_t hisparse_sparse_decode(hisparse_cache_t cache, int32_t layer, 
                                          const int32_t* d_slots, float* d_out,
                                          const hisparse_attn_desc_t* attn, void* d_workspace,
                                          size_t workspace_bytes, void* stream);
+
+/* [async] Sparse decode attention of layers [first_layer, first_layer + num_layers) of one
+ * share group in a single launch (Section 3.5: the shared layers read their records through
+ * the anchor's slots; batching them is this library's scheduling choice, the result per layer
+ * is the same attention as hisparse_sparse_decode up to the split boundaries).
+ *   d_q     bf16 [num_layers][units][q_heads][d_qk].
+ *   d_slots int32 [units][k]: the anchor's slot vector, read by every layer.
+ *   d_out   float32 [num_layers][units][q_heads][d_v].
+ *   d_workspace / workspace_bytes: at least
+ *           hisparse_decode_workspace_bytes(num_layers * units, k, R, attn) bytes.
+ * HISPARSE_ERR_INVALID_ARG if the layers span two share groups. */
+hisparse_status_t hisparse_sparse_decode_layers(hisparse_cache_t cache, int32_t first_layer,
+                                                int32_t num_layers, const void* d_q,
+                                                const int32_t* d_slots, float* d_out,
+                                                const hisparse_attn_desc_t* attn,
+                                                void* d_workspace, size_t workspace_bytes,
+                                                void* stream);
 
 /* [async] The same attention over an explicit device pool [units][records_per_unit][R], with
  * d_idx int32 [units][k] record indices into each unit's part of the pool (-1 = skip). Used for

@@ -42,8 +42,7 @@ void free_all(hisparse_cache* c) {
   (void)hipDeviceSynchronize();
   for (void* h : c->host)
     if (h) (void)hipHostFree(h);
-  for (uint8_t* p : c->cache)
-    if (p) (void)hipFree(p);
+  if (c->cache_all) (void)hipFree(c->cache_all);
   for (auto& a : c->anchors) {
     (void)hipFree(a.pt);
     (void)hipFree(a.slot_pos);
@@ -199,7 +198,11 @@ hisparse_status_t hisparse_cache_create(const hisparse_cache_desc_t* desc, int32
       st = HISPARSE_ERR_HIP;
       break;
     }
-    st = dmalloc(&c->cache[l], c->cache_layer_bytes);
+  }
+  if (st == HISPARSE_OK) {
+    st = dmalloc(&c->cache_all, c->cache_layer_bytes * (size_t)desc->num_layers);
+    for (int l = 0; l < desc->num_layers && st == HISPARSE_OK; ++l)
+      c->cache[l] = c->cache_all + (size_t)l * c->cache_layer_bytes;
   }
   for (int a = 0; a < c->n_anchors && st == HISPARSE_OK; ++a) {
     auto& an = c->anchors[a];
@@ -227,8 +230,8 @@ hisparse_status_t hisparse_cache_create(const hisparse_cache_desc_t* desc, int32
   }
   if (st == HISPARSE_OK) {
     if (hipMemset(c->err, 0, hisparse::kErrWords * 4) != hipSuccess) st = HISPARSE_ERR_HIP;
-    for (int l = 0; l < desc->num_layers && st == HISPARSE_OK; ++l)
-      if (hipMemset(c->cache[l], 0, c->cache_layer_bytes) != hipSuccess) st = HISPARSE_ERR_HIP;
+    if (hipMemset(c->cache_all, 0, c->cache_layer_bytes * (size_t)desc->num_layers) != hipSuccess)
+      st = HISPARSE_ERR_HIP;
     for (int a = 0; a < c->n_anchors && st == HISPARSE_OK; ++a) {
       if (hipMemset(c->anchors[a].plan, 0xFF, U * K * sizeof(int2)) != hipSuccess ||
           hisparse::launch_reset_state(state_args(c, c->anchors[a]), nullptr) != hipSuccess)
@@ -302,12 +305,21 @@ hisparse_status_t hisparse_resolve_tables(hisparse_cache_t c, int32_t layer,
 }
 
 namespace {
-// Copy the records of `anchor`'s latest miss plan from `target`'s host pool into `target`'s
-// GPU cache (target == anchor: the demand fetch; target a shared layer: the prefetch replay).
+// Copy the records of `anchor`'s latest miss plan from each target layer's host pool into
+// its GPU cache, for targets [target, target + n_layers) and units [u0, u0 + nu) (target ==
+// anchor: the demand fetch; a shared layer: the prefetch replay).
 hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t target,
-                                hipStream_t stream, int32_t u0 = 0, int32_t nu = -1) {
+                                hipStream_t stream, int32_t u0 = 0, int32_t nu = -1,
+                                int32_t n_layers = 1) {
   if (nu < 0) nu = c->units - u0;
   if (c->desc.fetch == HISPARSE_FETCH_NONE || nu == 0) return HISPARSE_OK;
+  if (c->desc.fetch == HISPARSE_FETCH_SDMA && n_layers > 1) {
+    for (int32_t j = 0; j < n_layers; ++j) {
+      const hisparse_status_t st = enqueue_fetch(c, anchor, target + j, stream, u0, nu, 1);
+      if (st != HISPARSE_OK) return st;
+    }
+    return HISPARSE_OK;
+  }
   auto& an = c->anchors[anchor / c->desc.share_group];
   if (c->desc.fetch == HISPARSE_FETCH_SDMA) {
     hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
@@ -358,19 +370,25 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
         return HISPARSE_ERR_HIP;
     return HISPARSE_OK;
   }
-  hisparse::FetchArgs f{};
   const int64_t L = c->desc.num_records, B = c->desc.capacity, R = c->desc.record_bytes;
-  f.plan = an.plan + (int64_t)u0 * c->desc.top_k;
-  f.plan_count = an.plan_count + u0;
-  f.host = reinterpret_cast<const uint8_t*>(c->host_dev[target]) + (int64_t)u0 * L * R;
-  f.cache = c->cache[target] + (int64_t)u0 * B * R;
-  f.L = L;
-  f.B = (int32_t)B;
-  f.k = c->desc.top_k;
-  f.R = (int32_t)R;
-  f.units = nu;
-  if (hisparse::launch_fetch(f, transfer_block(c->desc), stream) != hipSuccess)
-    return HISPARSE_ERR_HIP;
+  for (int32_t j0 = 0; j0 < n_layers; j0 += hisparse::kMaxFetchLayers) {
+    hisparse::FetchArgs f{};
+    f.n_layers = std::min(n_layers - j0, hisparse::kMaxFetchLayers);
+    f.plan = an.plan + (int64_t)u0 * c->desc.top_k;
+    f.plan_count = an.plan_count + u0;
+    for (int32_t j = 0; j < f.n_layers; ++j)
+      f.host[j] = reinterpret_cast<const uint8_t*>(c->host_dev[target + j0 + j]) +
+                  (int64_t)u0 * L * R;
+    f.cache = c->cache[target + j0] + (int64_t)u0 * B * R;
+    f.cache_stride = (int64_t)c->cache_layer_bytes;
+    f.L = L;
+    f.B = (int32_t)B;
+    f.k = c->desc.top_k;
+    f.R = (int32_t)R;
+    f.units = nu;
+    if (hisparse::launch_fetch(f, transfer_block(c->desc), stream) != hipSuccess)
+      return HISPARSE_ERR_HIP;
+  }
   return HISPARSE_OK;
 }
 }  // namespace
@@ -386,6 +404,14 @@ hisparse_status_t hisparse_fetch_units(hisparse_cache_t c, int32_t layer, int32_
       unit_count > c->units - unit_begin)
     return HISPARSE_ERR_INVALID_ARG;
   return enqueue_fetch(c, layer, layer, as_stream(stream), unit_begin, unit_count);
+}
+
+hisparse_status_t hisparse_fetch_group(hisparse_cache_t c, int32_t anchor_layer,
+                                       int32_t num_layers, void* stream) {
+  if (!c || !is_anchor(c, anchor_layer) || num_layers < 1 ||
+      num_layers > c->desc.share_group || num_layers > c->desc.num_layers - anchor_layer)
+    return HISPARSE_ERR_INVALID_ARG;
+  return enqueue_fetch(c, anchor_layer, anchor_layer, as_stream(stream), 0, -1, num_layers);
 }
 
 hisparse_status_t hisparse_resolve(hisparse_cache_t c, int32_t layer, const int32_t* d_sel,
@@ -441,6 +467,36 @@ hisparse_status_t hisparse_sparse_decode(hisparse_cache_t c, int32_t layer, cons
   return hisparse_sparse_decode_pool(c->cache[layer], c->desc.capacity, c->desc.record_bytes,
                                      c->units, c->desc.top_k, d_q, d_slots, d_out, attn,
                                      d_workspace, workspace_bytes, stream);
+}
+
+hisparse_status_t hisparse_sparse_decode_layers(hisparse_cache_t c, int32_t first_layer,
+                                                int32_t num_layers, const void* d_q,
+                                                const int32_t* d_slots, float* d_out,
+                                                const hisparse_attn_desc_t* attn,
+                                                void* d_workspace, size_t workspace_bytes,
+                                                void* stream) {
+  if (!c || first_layer < 0 || num_layers < 1 || num_layers > c->desc.num_layers - first_layer)
+    return HISPARSE_ERR_INVALID_ARG;
+  const int G = c->desc.share_group;
+  if (first_layer / G != (first_layer + num_layers - 1) / G) return HISPARSE_ERR_INVALID_ARG;
+  if (!d_q || !d_slots || !d_out || !d_workspace) return HISPARSE_ERR_INVALID_ARG;
+  if ((int64_t)c->units * num_layers > (int64_t)INT32_MAX / 256) return HISPARSE_ERR_INVALID_ARG;
+  const int32_t units = c->units * num_layers;
+  hisparse::AttnPlan p{};
+  hisparse_status_t st =
+      hisparse::plan_attention(units, c->desc.top_k, c->desc.record_bytes, attn, &p);
+  if (st != HISPARSE_OK) return st;
+  if (workspace_bytes < p.workspace_bytes) return HISPARSE_ERR_INVALID_ARG;
+  if ((int64_t)c->desc.capacity * c->desc.record_bytes > (int64_t)INT32_MAX)
+    return HISPARSE_ERR_UNSUPPORTED;
+  // the layers' caches are consecutive in one allocation, so unit u of layer first + j is
+  // unit j * units + u of one pool; every layer reads the same slot vector
+  if (hisparse::launch_attention(p, *attn, c->cache[first_layer], c->desc.capacity,
+                                 c->desc.record_bytes, units, c->desc.top_k,
+                                 reinterpret_cast<const uint16_t*>(d_q), d_slots, d_out,
+                                 d_workspace, as_stream(stream), c->units) != hipSuccess)
+    return HISPARSE_ERR_HIP;
+  return HISPARSE_OK;
 }
 
 hisparse_status_t hisparse_read_state(hisparse_cache_t c, int32_t layer, int32_t* slot_pos,

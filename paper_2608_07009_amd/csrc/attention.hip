@@ -54,7 +54,8 @@ struct AttnArgs {
   int64_t rec_per_unit;
   int32_t R, token_bytes, tpr_shift, k, H, n_tok;
   int32_t split_tokens, n_wg_splits, hb, n_parts, n_wg;
-  int32_t Hp;  // latent attention: heads rounded up to 32 (partial-output block layout)
+  int32_t Hp;         // latent attention: heads rounded up to 32 (partial-output block layout)
+  int32_t idx_units;  // unit u reads index row u % idx_units
   float scale_log2;
 };
 
@@ -200,7 +201,7 @@ void attn_partial_kernel(AttnArgs a) {
   const int rec_begin = tok_begin >> a.tpr_shift;
   const int n_rec = ((tok_end - 1) >> a.tpr_shift) - rec_begin + 1;
   {
-    const int32_t* idx_u = a.idx + (int64_t)unit * a.k + rec_begin;
+    const int32_t* idx_u = a.idx + (int64_t)(unit % a.idx_units) * a.k + rec_begin;
     for (int i = tid; i < n_rec; i += 64 * HW * TW) {
       const int32_t s = idx_u[i];
       s_idx[i] = (s >= 0 && s < a.rec_per_unit) ? s : -1;
@@ -503,7 +504,7 @@ void attn_mla_kernel(AttnArgs a) {
   const int rec_begin = tok_begin >> a.tpr_shift;
   const int n_rec = ((tok_end - 1) >> a.tpr_shift) - rec_begin + 1;
   {
-    const int32_t* idx_u = a.idx + (int64_t)unit * a.k + rec_begin;
+    const int32_t* idx_u = a.idx + (int64_t)(unit % a.idx_units) * a.k + rec_begin;
     for (int i = tid; i < n_rec; i += 64 * NW) {
       const int32_t s = idx_u[i];
       s_idx[i] = (s >= 0 && s < a.rec_per_unit) ? s : -1;
@@ -925,8 +926,10 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
 hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
                             const uint8_t* pool, int64_t records_per_unit, int32_t record_bytes,
                             int32_t units, int32_t top_k, const uint16_t* q, const int32_t* idx,
-                            float* out, void* workspace, hipStream_t stream) {
+                            float* out, void* workspace, hipStream_t stream,
+                            int32_t idx_units) {
   AttnArgs a{};
+  a.idx_units = idx_units > 0 ? idx_units : units;
   a.pool = pool;
   a.q = q;
   a.idx = idx;

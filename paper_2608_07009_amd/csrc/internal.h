@@ -33,13 +33,16 @@ struct ResolveArgs {
   int32_t B, k, layer, units;
 };
 
+constexpr int kMaxFetchLayers = 8;  // layers one fetch launch serves (grid z)
+
 struct FetchArgs {
   const int2* plan;         // [units][k]
   const int32_t* plan_count;  // [units]
-  const uint8_t* host;      // device-visible address of the layer's host pool [units][L][R]
-  uint8_t* cache;           // layer's GPU cache [units][B][R]
+  const uint8_t* host[kMaxFetchLayers];  // per target layer: device-visible host pool [units][L][R]
+  uint8_t* cache;           // first target layer's GPU cache [units][B][R]
+  int64_t cache_stride;     // bytes from one target layer's cache to the next
   int64_t L;
-  int32_t B, k, R, units;
+  int32_t B, k, R, units, n_layers;
 };
 
 struct StateArgs {
@@ -73,7 +76,8 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
 hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
                             const uint8_t* pool, int64_t records_per_unit, int32_t record_bytes,
                             int32_t units, int32_t top_k, const uint16_t* q, const int32_t* idx,
-                            float* out, void* workspace, hipStream_t stream);
+                            float* out, void* workspace, hipStream_t stream,
+                            int32_t idx_units = 0);
 
 }  // namespace hisparse
 
@@ -86,7 +90,8 @@ struct hisparse_cache {
   size_t cache_layer_bytes = 0;
   std::vector<void*> host;       // per layer, host address of the pinned pool
   std::vector<void*> host_dev;   // per layer, device-visible address of the same pool
-  std::vector<uint8_t*> cache;   // per layer, GPU cache
+  uint8_t* cache_all = nullptr;  // GPU caches of all layers, one allocation [layer][unit][B][R]
+  std::vector<uint8_t*> cache;   // per layer, GPU cache (into cache_all)
   struct Anchor {
     int32_t* pt = nullptr;
     int32_t* slot_pos = nullptr;

@@ -21,7 +21,9 @@
 //            slot of every input entry in input order.
 // fetch_kernel: copies each planned record from the pinned host pool (zero-copy 16-byte
 //   loads through the mapped address) into its slot; a wide grid over all units' misses, so a
-//   layer call with few units still keeps many loads in flight across the chip.
+//   layer call with few units still keeps many loads in flight across the chip. One launch can
+//   serve several layers of a share group (grid z): the anchor's demand fetch and the replays
+//   of the same plan into its shared layers.
 #include "internal.h"
 
 namespace hisparse {
@@ -336,8 +338,9 @@ __global__ __launch_bounds__(256) void fetch_kernel(FetchArgs a, FastDiv div_cpr
   const uint32_t cpr = (uint32_t)a.R >> 4;  // 16-byte chunks per record
   const uint32_t total = (uint32_t)m * cpr;
   const int2* plan = a.plan + (int64_t)unit * a.k;
-  const uint8_t* host = a.host + (int64_t)unit * a.L * a.R;
-  uint8_t* cache = a.cache + (int64_t)unit * a.B * a.R;
+  // grid z: the target layers (one plan, each layer's own host records and cache)
+  const uint8_t* host = a.host[blockIdx.z] + (int64_t)unit * a.L * a.R;
+  uint8_t* cache = a.cache + (int64_t)blockIdx.z * a.cache_stride + (int64_t)unit * a.B * a.R;
   const uint32_t stride = gridDim.x * 256u;
   for (uint32_t c0 = blockIdx.x * 256u + threadIdx.x; c0 < total; c0 += stride * U) {
     u32x4 v[U];
@@ -415,9 +418,9 @@ hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, hipStream_
   const int U = transfer_block_bytes / 16;
   const int64_t max_chunks = (int64_t)a.k * (a.R / 16);
   int64_t x = (max_chunks + 256LL * U - 1) / (256LL * U);
-  const int64_t cap = std::max<int64_t>(1, 4096 / a.units);
+  const int64_t cap = std::max<int64_t>(1, 4096 / ((int64_t)a.units * a.n_layers));
   if (x > cap) x = cap;
-  const dim3 grid((unsigned)x, (unsigned)a.units);
+  const dim3 grid((unsigned)x, (unsigned)a.units, (unsigned)a.n_layers);
   const FastDiv f = make_fastdiv((uint32_t)(a.R / 16));
   switch (U) {
     case 1: hipLaunchKernelGGL(fetch_kernel<1>, grid, dim3(256), 0, stream, a, f); break;

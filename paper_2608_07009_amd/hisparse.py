@@ -36,8 +36,9 @@ EXPORTED = (
     "hisparse_status_string", "hisparse_validate_desc", "hisparse_validate_attn",
     "hisparse_cache_create", "hisparse_cache_destroy", "hisparse_host_pool",
     "hisparse_layer_cache", "hisparse_reset", "hisparse_resolve", "hisparse_resolve_tables",
-    "hisparse_fetch", "hisparse_fetch_units", "hisparse_prefetch_layer",
-    "hisparse_decode_workspace_bytes", "hisparse_sparse_decode", "hisparse_sparse_decode_pool",
+    "hisparse_fetch", "hisparse_fetch_units", "hisparse_fetch_group", "hisparse_prefetch_layer",
+    "hisparse_decode_workspace_bytes", "hisparse_sparse_decode", "hisparse_sparse_decode_layers",
+    "hisparse_sparse_decode_pool",
     "hisparse_read_state", "hisparse_read_plan", "hisparse_check_errors",
 )
 
@@ -92,11 +93,15 @@ def lib() -> ctypes.CDLL:
             "hisparse_resolve_tables": (_I32, [_V, _I32, _V, _V, _V, _V]),
             "hisparse_fetch": (_I32, [_V, _I32, _V]),
             "hisparse_fetch_units": (_I32, [_V, _I32, _I32, _I32, _V]),
+            "hisparse_fetch_group": (_I32, [_V, _I32, _I32, _V]),
             "hisparse_prefetch_layer": (_I32, [_V, _I32, _I32, _V]),
             "hisparse_decode_workspace_bytes": (ctypes.c_size_t, [_I32, _I32, _I32,
                                                                   ctypes.POINTER(AttnDesc)]),
             "hisparse_sparse_decode": (_I32, [_V, _I32, _V, _V, _V, ctypes.POINTER(AttnDesc), _V,
                                               ctypes.c_size_t, _V]),
+            "hisparse_sparse_decode_layers": (_I32, [_V, _I32, _I32, _V, _V, _V,
+                                                     ctypes.POINTER(AttnDesc), _V,
+                                                     ctypes.c_size_t, _V]),
             "hisparse_sparse_decode_pool": (_I32, [_V, ctypes.c_int64, _I32, _I32, _I32, _V, _V,
                                                    _V, ctypes.POINTER(AttnDesc), _V,
                                                    ctypes.c_size_t, _V]),
@@ -199,6 +204,11 @@ def hisparse_fetch_units(cache: int, layer: int, unit_begin: int, unit_count: in
            lib().hisparse_fetch_units(cache, layer, unit_begin, unit_count, _s(stream)))
 
 
+def hisparse_fetch_group(cache: int, anchor_layer: int, num_layers: int, stream=None) -> None:
+    _check("hisparse_fetch_group",
+           lib().hisparse_fetch_group(cache, anchor_layer, num_layers, _s(stream)))
+
+
 def hisparse_prefetch_layer(cache: int, anchor_layer: int, shared_layer: int,
                             stream=None) -> None:
     _check("hisparse_prefetch_layer",
@@ -216,6 +226,15 @@ def hisparse_sparse_decode(cache: int, layer: int, d_q, d_slots, d_out, attn: At
            lib().hisparse_sparse_decode(cache, layer, _p(d_q), _p(d_slots), _p(d_out),
                                         ctypes.byref(attn), _p(d_workspace), workspace_bytes,
                                         _s(stream)))
+
+
+def hisparse_sparse_decode_layers(cache: int, first_layer: int, num_layers: int, q, slots, out,
+                                  attn: AttnDesc, workspace, workspace_bytes: int,
+                                  stream=None) -> None:
+    _check("hisparse_sparse_decode_layers",
+           lib().hisparse_sparse_decode_layers(cache, first_layer, num_layers, _p(q), _p(slots),
+                                               _p(out), ctypes.byref(attn), _p(workspace),
+                                               workspace_bytes, _s(stream)))
 
 
 def hisparse_sparse_decode_pool(d_pool, records_per_unit: int, record_bytes: int, units: int,

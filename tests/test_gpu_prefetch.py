@@ -128,3 +128,78 @@ def test_prefetch_side_stream(cfg, steps):
                     log(f"  step {t} shared layer {s}: ok")
     finally:
         run.close()
+
+
+def test_decode_layers_batch_matches_resident():
+    """One launch for an anchor and its shared layers (all reading the anchor's slots): for
+    every layer, bit-identical to the same plan over the stacked, fully resident KV of those
+    layers (positions instead of slots), and within the oracle's tolerance."""
+    G = 4
+    w = W.workload(2, num_layers=G, share_group=G, num_requests=3)
+    steps = 3
+    log(f"test_decode_layers_batch_matches_resident {w.name} units={w.units}")
+    run = Run(w, steps)
+    try:
+        U, k, H = w.units, w.k, w.q_heads
+        for t in range(steps):
+            run.resolve_step(t, prefetch=True)
+        t = steps - 1
+        ad = attn_desc(w)
+        q_host = np.stack([W.queries(w, t, l) for l in range(G)])       # [G][U][H][d_qk]
+        q = torch.from_numpy(q_host.view(np.int16)).to(run.dev)
+        ws = torch.empty(hs.hisparse_decode_workspace_bytes(G * U, k, w.record_bytes, ad),
+                         dtype=torch.uint8, device=run.dev)
+        out = torch.empty((G, U, H, w.d_v), dtype=torch.float32, device=run.dev)
+        hs.hisparse_sparse_decode_layers(run.cache.handle, 0, G, q, run.slots[0], out, ad, ws,
+                                         ws.numel(), run.stream)
+        hosts = [run.cache.host_view(l) for l in range(G)]               # [U][L][R] each
+        pool = torch.from_numpy(np.ascontiguousarray(np.stack(hosts)).reshape(-1)).to(run.dev)
+        sel = run.sel_host[t, 0:U]                                       # anchor 0's streams
+        idx = torch.from_numpy(np.ascontiguousarray(np.tile(sel, (G, 1)))).to(run.dev)
+        ref = torch.empty_like(out)
+        hs.hisparse_sparse_decode_pool(pool, w.L, w.record_bytes, G * U, k, q, idx, ref, ad, ws,
+                                       ws.numel(), run.stream)
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), "placement changed the batched output"
+        o = out.cpu().numpy()
+        for l, u in [(0, 0), (G - 1, U - 1), (1, 1)]:
+            e = oracle.sparse_decode(q_host[l, u], hosts[l][u].view(np.uint16).reshape(w.L, -1),
+                                     sel[u], d_qk=w.d_qk, d_v=w.d_v, v_off=w.v_offset,
+                                     token_elems=w.token_elems,
+                                     tokens_per_record=w.tokens_per_record, scale=w.scale)
+            assert np.abs(o[l, u] - e).max() <= 1e-2
+            assert np.linalg.norm(o[l, u] - e) / np.linalg.norm(e) <= 5e-3
+        with pytest.raises(hs.HisparseError):   # spans two share groups
+            hs.hisparse_sparse_decode_layers(run.cache.handle, 2, 3, q, run.slots[0], out, ad,
+                                             ws, ws.numel(), run.stream)
+    finally:
+        run.close()
+
+
+def test_fetch_group_equals_fetch_and_replays():
+    """One launch for the anchor's fetch and its shared layers' replays leaves every layer's
+    cache byte-identical to hisparse_fetch followed by one hisparse_prefetch_layer per shared
+    layer; bad group sizes are argument errors."""
+    G = 4
+    w = W.workload(2, num_layers=G, share_group=G, num_requests=2)
+    steps = 4
+    log(f"test_fetch_group_equals_fetch_and_replays {w.name}")
+    grouped = Run(w, steps)
+    single = Run(w, steps)
+    try:
+        for t in range(steps):
+            hs.hisparse_resolve_tables(grouped.cache.handle, 0, grouped.sel_ptr(t, 0),
+                                       grouped.slots[0], grouped.counts[0], grouped.stream)
+            hs.hisparse_fetch_group(grouped.cache.handle, 0, G, grouped.stream)
+            single.resolve_step(t, prefetch=True)
+        assert torch.equal(grouped.slots[0], single.slots[0])
+        for l in range(G):
+            assert (layer_cache_host(grouped, l) == layer_cache_host(single, l)).all(), f"layer {l}"
+        for n in (0, G + 1):
+            with pytest.raises(hs.HisparseError):
+                hs.hisparse_fetch_group(grouped.cache.handle, 0, n, grouped.stream)
+        with pytest.raises(hs.HisparseError):   # not an anchor layer
+            hs.hisparse_fetch_group(grouped.cache.handle, 1, 2, grouped.stream)
+    finally:
+        grouped.close()
+        single.close()
