@@ -21,6 +21,7 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import dataclasses
 import json
 import os
 import sys
@@ -54,10 +55,19 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-sweep", action="store_true")
-    ap.add_argument("--side-stream-replay", action="store_true",
-                    help="shared layers: replay on a side stream overlapped with the anchor's "
-                         "attention (default: the group's fetch and replays in one launch, then "
-                         "one attention launch for the group)")
+    ap.add_argument("--micro-batches", type=int, default=0,
+                    help="independent request groups, each with its own cache handle and "
+                         "streams, whose steps run concurrently (0 = 2 when there are at least "
+                         "2 requests, else 1)")
+    ap.add_argument("--fetch-workgroups", type=int, default=0,
+                    help="workgroups of one fetch launch (0 = the library default)")
+    ap.add_argument("--schedule", choices=["overlap", "serial", "batched"], default="overlap",
+                    help="shared layers: 'overlap' replays them on a side stream while the "
+                         "anchor's attention runs, each replay releasing its layer's attention; "
+                         "'serial' fetches the anchor and its shared layers in one launch, then "
+                         "runs the layers' attention in order; 'batched' (not realisable in a "
+                         "model: later layers' queries depend on earlier layers) decodes the "
+                         "group's layers in one attention launch")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run one device-to-device copy of BYTES (calibrates the HBM "
                          "byte counters of a profiler run) and exit")
@@ -228,146 +238,181 @@ def main() -> int:
                           f"{w.steps} steps"}))
         return 2
     dev = torch.device("cuda:0")
-    main_t = torch.cuda.Stream()  # a capturable stream (not the legacy null stream)
-    torch.cuda.set_stream(main_t)
-    side_t = torch.cuda.Stream()
-    main_s, side_s = main_t.cuda_stream, side_t.cuda_stream
+    root_t = torch.cuda.Stream()  # a capturable stream (not the legacy null stream)
+    torch.cuda.set_stream(root_t)
+    root_s = root_t.cuda_stream
     fetch = {"none": hs.HISPARSE_FETCH_NONE, "sdma": hs.HISPARSE_FETCH_SDMA,
              "zero_copy": hs.HISPARSE_FETCH_ZERO_COPY}[args.fetch]
     hmem = {"coherent": hs.HISPARSE_HOST_COHERENT, "noncoherent": hs.HISPARSE_HOST_NONCOHERENT,
             "uncached": hs.HISPARSE_HOST_UNCACHED}[args.host_memory]
+    n_mb = args.micro_batches or (2 if w.num_requests >= 2 else 1)
+    if w.num_requests % n_mb:
+        print(json.dumps({"error": f"{w.num_requests} requests do not split into {n_mb} "
+                          f"micro-batches"}))
+        return 2
+    if n_mb > 1 and fetch == hs.HISPARSE_FETCH_SDMA:
+        n_mb = 1  # the SDMA path synchronises the host on every fetch: nothing to overlap
 
+    U_all, k, G = w.units, w.k, w.share_group
     t0 = time.time()
-    cache = HiSparseCache.for_workload(w, fetch=fetch, host_memory=hmem,
-                                       transfer_block_bytes=args.transfer_block)
-    for l in range(w.num_layers):
-        W.fill_kv(cache.host_pool(l)[0], w, l)
     sel_host = W.selection_streams(w, steps=steps_needed)
     sel = torch.from_numpy(sel_host).to(dev)
     n_qv = 2  # queries vary by (layer, step parity)
     q_all = torch.stack([torch.stack([torch.from_numpy(W.queries(w, v, l).view(np.int16))
                                       for l in range(w.num_layers)]) for v in range(n_qv)]).to(dev)
-    log(f"{w.name}: layers {w.num_layers} (of {w0.num_layers}), host pool "
-        f"{w.host_pool_bytes() / 2**30:.1f} GiB, set up in {time.time() - t0:.1f}s")
-
-    U, k, G = w.units, w.k, w.share_group
-    slots = torch.empty((w.num_layers, U, k), dtype=torch.int32, device=dev)
-    counts = torch.zeros((steps_needed, w.num_layers, U, 2), dtype=torch.int32, device=dev)
+    out = torch.empty((w.num_layers, U_all, w.q_heads, w.d_v), dtype=torch.float32, device=dev)
     ad = hs.AttnDesc(w.q_heads, w.d_qk, w.d_v, w.v_offset, w.tokens_per_record, args.splits,
                      w.scale, 0)
     ad_ref = ctypes.byref(ad)
-    # the shared layers of a group are decoded in one launch once their replays have landed
-    ws_bytes = max(hs.hisparse_decode_workspace_bytes(n * U, k, w.record_bytes, ad)
-                   for n in range(1, G + 1)) if G > 1 else 0
-    ws_bytes = max(ws_bytes, hs.hisparse_decode_workspace_bytes(U, k, w.record_bytes, ad))
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
-    out = torch.empty((w.num_layers, U, w.q_heads, w.d_v), dtype=torch.float32, device=dev)
-    h = cache.handle
-
-    # every pointer of every step, precomputed
-    sel_p = [[sel[t, (a // G) * U:(a // G + 1) * U].data_ptr() for a in range(w.num_layers)]
-             for t in range(steps_needed)]
-    cnt_p = [[counts[t, a].data_ptr() for a in range(w.num_layers)] for t in range(steps_needed)]
-    slot_p = [slots[a].data_ptr() for a in range(w.num_layers)]
-    q_p = [[q_all[v, l].data_ptr() for l in range(w.num_layers)] for v in range(n_qv)]
-    out_p = [out[l].data_ptr() for l in range(w.num_layers)]
-    ws_p = ws.data_ptr()
     groups = [(a, list(range(a + 1, min(a + G, w.num_layers)))) for a in w.anchors]
+
+    class MicroBatch:
+        """Requests [r0, r0 + n) with their own cache handle and streams. Micro-batches are
+        independent decode chains: one's host-link transfers overlap another's attention and
+        resolve work."""
+
+        def __init__(self, i):
+            n = w.num_requests // n_mb
+            self.r0 = i * n
+            self.U = n * w.units_per_request
+            self.u0 = self.r0 * w.units_per_request
+            wm = dataclasses.replace(w, num_requests=n)
+            self.cache = HiSparseCache.for_workload(
+                wm, fetch=fetch, host_memory=hmem, transfer_block_bytes=args.transfer_block,
+                fetch_workgroups=args.fetch_workgroups)
+            for l in range(w.num_layers):
+                W.fill_kv(self.cache.host_pool(l)[0], w, l, self.u0, self.U)
+            self.h = self.cache.handle
+            self.main_t = root_t if i == 0 else torch.cuda.Stream()
+            self.side_t = torch.cuda.Stream()
+            self.main, self.side = self.main_t.cuda_stream, self.side_t.cuda_stream
+            U = self.U
+            self.slots = torch.empty((w.num_layers, U, k), dtype=torch.int32, device=dev)
+            self.counts = torch.zeros((steps_needed, w.num_layers, U, 2), dtype=torch.int32,
+                                      device=dev)
+            self.ws_bytes = max(hs.hisparse_decode_workspace_bytes(m * U, k, w.record_bytes, ad)
+                                for m in range(1, G + 1))
+            self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
+            sl = slice(self.u0, self.u0 + U)
+            self.sel_p = [[sel[t, (a // G) * U_all + self.u0:(a // G) * U_all + self.u0 + U]
+                           .data_ptr() for a in range(w.num_layers)] for t in range(steps_needed)]
+            self.cnt_p = [[self.counts[t, a].data_ptr() for a in range(w.num_layers)]
+                          for t in range(steps_needed)]
+            self.slot_p = [self.slots[a].data_ptr() for a in range(w.num_layers)]
+            self.q_p = [[q_all[v, l, sl].data_ptr() for l in range(w.num_layers)]
+                        for v in range(n_qv)]
+            self.out_p = [out[l, sl].data_ptr() for l in range(w.num_layers)]
+            self.sync = [hip.event(timing=False) for _ in range(G + 1)]
+            self.link = [hip.event(timing=False) for _ in groups]
+
+    mbs = [MicroBatch(i) for i in range(n_mb)]
+    cache = mbs[0].cache
+    fork_ev = hip.event(timing=False)
+    join_evs = [hip.event(timing=False) for _ in mbs]
+    log(f"{w.name}: layers {w.num_layers} (of {w0.num_layers}), host pool "
+        f"{w.host_pool_bytes() / 2**30:.1f} GiB, {n_mb} micro-batch(es), schedule "
+        f"{args.schedule}, set up in {time.time() - t0:.1f}s")
+
     f_tables, f_fetch = L.hisparse_resolve_tables, L.hisparse_fetch
     f_prefetch, f_decode = L.hisparse_prefetch_layer, L.hisparse_sparse_decode
     f_decode_layers, f_fetch_group = L.hisparse_sparse_decode_layers, L.hisparse_fetch_group
     rec = hip.L.hipEventRecord
     wait = hip.L.hipStreamWaitEvent
-    sync_events = [hip.event(timing=False) for _ in range(2 * G)]
 
     def check(rc, what):
         if rc != 0:
             raise RuntimeError(f"{what} -> {hs.hisparse_status_string(rc)}")
 
+    def call(name, stream, ev, spans, fn, *fargs):
+        """One library call; with ev (timing events, consumed in order) bracketed by events."""
+        if ev is not None:
+            e0, e1 = ev.pop(), ev.pop()
+            rec(e0, stream)
+        check(fn(*fargs), name)
+        if ev is not None:
+            rec(e1, stream)
+            spans.append((name, e0, e1))
+
+    def group_step(mb, gi, t, ev, spans, sel_override, q_override, link):
+        """Share group gi of decode step t for one micro-batch, layers in model order: every
+        layer's attention follows the previous layer's (its query depends on it). `link`:
+        (event to wait for before this group's host-link transfer, event to record after it),
+        or None."""
+        a, shared = groups[gi]
+        qv = q_override[mb.u0] if q_override else mb.q_p[t % n_qv]
+        h, ms, ss = mb.h, mb.main, mb.side
+        sp = sel_override[mb.u0][a] if sel_override else mb.sel_p[t][a]
+        cp = None if sel_override else mb.cnt_p[t][a]
+        call("resolve_tables", ms, ev, spans, f_tables, h, a, sp, mb.slot_p[a], cp, ms)
+
+        def decode(l):
+            call("sparse_decode", ms, ev, spans, f_decode, h, l, qv[l], mb.slot_p[a],
+                 mb.out_p[l], ad_ref, mb.ws.data_ptr(), mb.ws_bytes, ms)
+
+        def transfer(name, fn, *fargs):
+            if link and link[0] is not None:
+                wait(ms, link[0], 0)
+            call(name, ms, ev, spans, fn, *fargs)
+            if link:
+                rec(link[1], ms)
+
+        if not shared:
+            transfer("fetch", f_fetch, h, a, ms)
+            decode(a)
+        elif args.schedule == "serial":
+            # the anchor's fetch and its shared layers' replays in one launch, then the
+            # layers' attention in order
+            transfer("fetch_group", f_fetch_group, h, a, 1 + len(shared), ms)
+            for l in [a] + shared:
+                decode(l)
+        elif args.schedule == "batched":
+            # NOT realisable inside a model (the queries of a group's later layers depend on
+            # the earlier layers' outputs): one attention launch for the whole group
+            transfer("fetch_group", f_fetch_group, h, a, 1 + len(shared), ms)
+            call("sparse_decode_layers", ms, ev, spans, f_decode_layers, h, a, 1 + len(shared),
+                 qv[a], mb.slot_p[a], mb.out_p[a], ad_ref, mb.ws.data_ptr(), mb.ws_bytes, ms)
+        else:
+            # overlap (Section 3.5): the anchor's fetch first, then its attention on the main
+            # stream while the side stream replays the plan into the shared layers one by one,
+            # each replay releasing its layer's attention
+            transfer("fetch", f_fetch, h, a, ms)
+            rec(mb.sync[0], ms)
+            wait(ss, mb.sync[0], 0)
+            for i, l in enumerate(shared):
+                call("prefetch_replay", ss, ev, spans, f_prefetch, h, a, l, ss)
+                rec(mb.sync[1 + i], ss)
+            decode(a)
+            for i, l in enumerate(shared):
+                wait(ms, mb.sync[1 + i], 0)
+                decode(l)
+
     def step(t, ev=None, spans=None, sel_override=None, q_override=None):
-        """Enqueue decode step t. With ev (a list of timing events, consumed in order) every
-        kernel call is bracketed by events and (name, e0, e1) appended to spans."""
-        qv = q_override or q_p[t % n_qv]
-        for a, shared in groups:
-            sp = sel_override[a] if sel_override else sel_p[t][a]
-            cp = 0 if sel_override else cnt_p[t][a]
-            if ev is not None:
-                e0, e1 = ev.pop(), ev.pop()
-                rec(e0, main_s)
-                check(f_tables(h, a, sp, slot_p[a], cp or None, main_s), "resolve_tables")
-                rec(e1, main_s)
-                spans.append(("resolve_tables", e0, e1))
-            else:
-                check(f_tables(h, a, sp, slot_p[a], cp or None, main_s), "resolve_tables")
-            if shared and not args.side_stream_replay:
-                # nothing else to overlap the replays with: the anchor's fetch and its shared
-                # layers' replays in one launch, then one attention launch for the group
-                if ev is not None:
-                    e0, e1 = ev.pop(), ev.pop()
-                    rec(e0, main_s)
-                check(f_fetch_group(h, a, 1 + len(shared), main_s), "fetch_group")
-                if ev is not None:
-                    rec(e1, main_s)
-                    spans.append(("fetch_group", e0, e1))
-                    e0, e1 = ev.pop(), ev.pop()
-                    rec(e0, main_s)
-                check(f_decode_layers(h, a, 1 + len(shared), qv[a], slot_p[a], out_p[a],
-                                      ad_ref, ws_p, ws_bytes, main_s), "sparse_decode_layers")
-                if ev is not None:
-                    rec(e1, main_s)
-                    spans.append(("sparse_decode_layers", e0, e1))
-                continue
-            # the anchor's own fetch goes first and alone on the host link (its attention is
-            # next); the shared layers' replays follow back to back on the side stream, each
-            # releasing its layer's attention as soon as it lands
-            if ev is not None:
-                e0, e1 = ev.pop(), ev.pop()
-                rec(e0, main_s)
-                check(f_fetch(h, a, main_s), "fetch")
-                rec(e1, main_s)
-                spans.append(("fetch", e0, e1))
-            else:
-                check(f_fetch(h, a, main_s), "fetch")
-            if shared:
-                rec(sync_events[0], main_s)  # the anchor's fetch has landed
-            if ev is not None:
-                e0, e1 = ev.pop(), ev.pop()
-                rec(e0, main_s)
-                check(f_decode(h, a, qv[a], slot_p[a], out_p[a], ad_ref, ws_p, ws_bytes, main_s),
-                      "sparse_decode")
-                rec(e1, main_s)
-                spans.append(("sparse_decode", e0, e1))
-            else:
-                check(f_decode(h, a, qv[a], slot_p[a], out_p[a], ad_ref, ws_p, ws_bytes, main_s),
-                      "sparse_decode")
-            if shared:
-                wait(side_s, sync_events[0], 0)
-                for i, s in enumerate(shared):
-                    if ev is not None:
-                        e0, e1 = ev.pop(), ev.pop()
-                        rec(e0, side_s)
-                        check(f_prefetch(h, a, s, side_s), "prefetch_layer")
-                        rec(e1, side_s)
-                        spans.append(("prefetch_replay", e0, e1))
-                    else:
-                        check(f_prefetch(h, a, s, side_s), "prefetch_layer")
-                    rec(sync_events[1 + i], side_s)
-            if shared:
-                wait(main_s, sync_events[len(shared)], 0)  # the last replay has landed
-                if ev is not None:
-                    e0, e1 = ev.pop(), ev.pop()
-                    rec(e0, main_s)
-                check(f_decode_layers(h, shared[0], len(shared), qv[shared[0]], slot_p[a],
-                                      out_p[shared[0]], ad_ref, ws_p, ws_bytes, main_s),
-                      "sparse_decode_layers")
-                if ev is not None:
-                    rec(e1, main_s)
-                    spans.append(("sparse_decode_layers", e0, e1))
+        """Enqueue decode step t of every micro-batch: forked from the root stream, joined back
+        into it. Micro-batches take turns on the host link: the transfer of group g of
+        micro-batch i waits for that of micro-batch i-1 (and micro-batch 0's for the last
+        micro-batch's transfer of group g-1), so while one micro-batch moves its misses the
+        others resolve and attend instead of splitting the link and falling into lockstep."""
+        if n_mb > 1:
+            rec(fork_ev, root_s)
+            for mb in mbs[1:]:
+                wait(mb.main, fork_ev, 0)
+        for gi in range(len(groups)):
+            for i, mb in enumerate(mbs):
+                link = None
+                if n_mb > 1:
+                    prev = (mbs[i - 1].link[gi] if i > 0 else
+                            (mbs[-1].link[gi - 1] if gi > 0 else None))
+                    link = (prev, mb.link[gi])
+                group_step(mb, gi, t, ev, spans, sel_override, q_override, link)
+        if n_mb > 1:
+            for mb, je in zip(mbs[1:], join_evs[1:]):
+                rec(je, mb.main)
+                wait(root_s, je, 0)
 
     # pinned H2D sweep over the same pool (hipMemcpyAsync), before the timed region
     sweep = {}
     if not args.no_sweep:
-        sweep = pinned_sweep(torch, hip, *cache.host_pool(0), dev, main_s)
+        sweep = pinned_sweep(torch, hip, *cache.host_pool(0), dev, root_s)
         log("pinned H2D sweep GB/s: " + ", ".join(f"{s >> 10}K:{v:.1f}" for s, v in sweep.items()))
     pinned_peak = max(sweep.values()) if sweep else None
 
@@ -387,30 +432,31 @@ def main() -> int:
     # Kernel-span pass: the K steps are enqueued behind a bounded GPU delay (torch's clock
     # spin), so the host is ahead of the GPU for the whole pass and each event pair brackets
     # its kernel, not a host launch gap. Its GPU time per step is reported beside the timed
-    # region's.
-    per_step_events = sum((6 if (sh and not args.side_stream_replay) else
-                           6 + 2 * len(sh) + (2 if sh else 0)) for _, sh in groups)
+    # region's. With several micro-batches the spans of concurrent kernels overlap: each span
+    # is that kernel's duration while sharing the GPU.
+    per_step_events = n_mb * sum(2 * (3 + 2 * len(sh)) for _, sh in groups)
     events = [hip.event() for _ in range(per_step_events * args.steps)]
     ref, end = hip.event(), hip.event()
     spans = []
     cal0, cal1 = hip.event(), hip.event()
-    rec(cal0, main_s)
+    rec(cal0, root_s)
     torch.cuda._sleep(1_000_000)
-    rec(cal1, main_s)
+    rec(cal1, root_s)
     torch.cuda.synchronize()
     cycles_per_ms = 1_000_000 / max(1e-3, hip.ms(cal0, cal1))
     delay_ms = min(4000.0, 3.0 * host_ms * args.steps + 20.0)
     torch.cuda._sleep(int(delay_ms * cycles_per_ms))
-    rec(ref, main_s)
+    rec(ref, root_s)
     for t in range(args.warmup, steps_needed):
         step(t, events, spans)
-    rec(end, main_s)
+    rec(end, root_s)
     torch.cuda.synchronize()
     eager_gpu_ms = hip.ms(ref, end) / args.steps
-    st, info = cache.check_errors()
-    if st != hs.HISPARSE_OK:
-        print(json.dumps({"error": f"device-side selection error {info}"}))
-        return 1
+    for mb in mbs:
+        st, info = mb.cache.check_errors()
+        if st != hs.HISPARSE_OK:
+            print(json.dumps({"error": f"device-side selection error {info}"}))
+            return 1
 
     tot = {}
     io_intervals = []
@@ -428,14 +474,16 @@ def main() -> int:
     for e in (ref, end, cal0, cal1):
         hip.L.hipEventDestroy(e)
 
-    c = counts[args.warmup:steps_needed].cpu().numpy().astype(np.int64)  # [K][layers][U][2]
+    # [K][layers][units][2] over all micro-batches (units in global order)
+    c = np.concatenate([mb.counts[args.warmup:steps_needed].cpu().numpy() for mb in mbs],
+                       axis=2).astype(np.int64)
     K = args.steps
+    U = U_all // n_mb  # units of one launch
     anchor_calls = K * len(w.anchors)
     misses_anchor = int(c[:, w.anchors, :, 1].sum())
     hits_anchor = int(c[:, w.anchors, :, 0].sum())
-    misses_replay = int(sum(c[:, a, :, 1].sum() * len(sh) for a, sh in groups))
     R = w.record_bytes
-    served = K * w.num_layers * U * k
+    served = K * w.num_layers * U_all * k
 
     def kernel(name):
         return tot.get(name, (0.0, 0))
@@ -444,31 +492,29 @@ def main() -> int:
     t_fet, n_fet = kernel("fetch")
     t_rep, n_rep = kernel("prefetch_replay")
     t_att, n_att = kernel("sparse_decode")
-    # shared layers are decoded in batched launches; attention is accounted per layer call
-    t_lay, n_lay = kernel("sparse_decode_layers")
-    per_batch = (lambda sh: len(sh)) if args.side_stream_replay else (lambda sh: 1 + len(sh))
-    lay_calls = K * sum(per_batch(sh) for _, sh in groups if sh) if n_lay else 0
     t_grp, n_grp = kernel("fetch_group")
+    # batched schedule: one attention launch per group; attention is accounted per layer call
+    t_lay, n_lay = kernel("sparse_decode_layers")
+    grouped = [(a, sh) for a, sh in groups if sh and args.schedule in ("serial", "batched")]
+    lay_calls = K * n_mb * sum(1 + len(sh) for _, sh in grouped) if n_lay else 0
     t_att_one, n_att_one = t_att, n_att
     t_att, n_att = t_att + t_lay, n_att + lay_calls
-    grouped = [a for a, sh in groups if sh and not args.side_stream_replay]
-    misses_grouped = int(c[:, grouped, :, 1].sum()) if grouped else 0
+    misses_grouped = sum(int(c[:, a, :, 1].sum()) for a, _ in grouped)
     fetch_bytes = (misses_anchor - misses_grouped) * R      # plain demand fetches
-    replay_bytes = misses_replay * R                        # replays into shared layers
-    group_bytes = (misses_grouped * R + replay_bytes) if grouped else 0
-    if grouped:
-        replay_bytes = 0  # carried by the group launches
+    group_bytes = sum(int(c[:, a, :, 1].sum()) * (1 + len(sh)) for a, sh in grouped) * R
+    replay_bytes = sum(int(c[:, a, :, 1].sum()) * len(sh) for a, sh in groups
+                       if sh and (a, sh) not in grouped) * R
     moves_data = fetch != hs.HISPARSE_FETCH_NONE
     kernels = {}
     # resolve tables: integer metadata work per unit (algorithmic bytes):
     # sel 4k + page-table probes 4k + slot outputs 4k + recency index read+write 8B
     # + hit stamps 4h + per miss (slot map r/w 8, page table 8, stamp 4, plan 8) = 28m
-    tab_bytes = anchor_calls * U * (12 * k + 8 * w.B) + 4 * hits_anchor + 28 * misses_anchor
+    tab_bytes = anchor_calls * U_all * (12 * k + 8 * w.B) + 4 * hits_anchor + 28 * misses_anchor
     if n_tab:
         kernels["resolve_tables"] = {
             "launches": n_tab, "avg_us": t_tab / n_tab * 1e6, "bound": "latency",
             "hbm_GBps": tab_bytes / t_tab / 1e9,
-            "selections_per_s_no_io": anchor_calls * U * k / t_tab}
+            "selections_per_s_no_io": anchor_calls * U_all * k / t_tab}
     if n_fet and moves_data:
         kernels["fetch"] = {"launches": n_fet, "avg_us": t_fet / n_fet * 1e6,
                             "bytes_per_launch": fetch_bytes / n_fet,
@@ -547,18 +593,20 @@ def main() -> int:
         stage_sel = torch.empty_like(sel[0])
         stage_q = torch.empty_like(q_all[0])
         tidx = torch.zeros(1, dtype=torch.int64, device=dev)
-        sel_stage_p = [stage_sel[(a // G) * U:(a // G + 1) * U].data_ptr()
-                       for a in range(w.num_layers)]
-        q_stage_p = [stage_q[l].data_ptr() for l in range(w.num_layers)]
+        sel_stage_p = {mb.u0: [stage_sel[(a // G) * U_all + mb.u0:(a // G) * U_all + mb.u0 + mb.U]
+                               .data_ptr() for a in range(w.num_layers)] for mb in mbs}
+        q_stage_p = {mb.u0: [stage_q[l, mb.u0:mb.u0 + mb.U].data_ptr()
+                             for l in range(w.num_layers)] for mb in mbs}
         g = torch.cuda.CUDAGraph()
         torch.cuda.synchronize()
-        with torch.cuda.graph(g, stream=main_t):
+        with torch.cuda.graph(g, stream=root_t):
             stage_sel.copy_(sel.index_select(0, tidx).squeeze(0))
             stage_q.copy_(q_all.index_select(0, torch.remainder(tidx, n_qv)).squeeze(0))
             tidx.add_(1)
             step(0, sel_override=sel_stage_p, q_override=q_stage_p)
         torch.cuda.synchronize()
-        hs.hisparse_reset(h, main_s)
+        for mb in mbs:
+            hs.hisparse_reset(mb.h, root_s)
         tidx.zero_()
         for _ in range(args.warmup):
             g.replay()
@@ -569,10 +617,11 @@ def main() -> int:
         torch.cuda.synchronize()
         gwall = time.perf_counter() - tg
         graph = {"ms_per_step": gwall / K * 1e3}
-        st, info = cache.check_errors()
-        if st != hs.HISPARSE_OK:
-            print(json.dumps({"error": f"device-side selection error in graph replay {info}"}))
-            return 1
+        for mb in mbs:
+            st, info = mb.cache.check_errors()
+            if st != hs.HISPARSE_OK:
+                print(json.dumps({"error": f"device-side selection error in graph replay {info}"}))
+                return 1
 
     if graph is not None:
         mode, wall = "hip_graph_replay", gwall
@@ -594,7 +643,8 @@ def main() -> int:
         "dtype": "int32+bf16",
         "data": "synthetic",
         "config": {"workload": w.name, "requests": w.num_requests, "layers": w.num_layers,
-                   "layers_in_workload": w0.num_layers, "units_per_layer": U,
+                   "layers_in_workload": w0.num_layers, "units_per_layer": U_all,
+                   "micro_batches": n_mb, "schedule": args.schedule,
                    "records_per_unit": w.L, "record_bytes": R, "top_k": k, "capacity": w.B,
                    "share_group": G, "q_heads": w.q_heads, "fetch": args.fetch,
                    "host_memory": args.host_memory, "mode": mode},
@@ -605,19 +655,22 @@ def main() -> int:
         "pinned_h2d_peak_GBps": pinned_peak,
         "pinned_h2d_sweep_GBps": {str(s): v for s, v in sweep.items()},
         "hit_rate": hits_anchor / max(1, hits_anchor + misses_anchor),
-        "misses_per_unit_step": misses_anchor / max(1, anchor_calls * U),
+        "misses_per_unit_step": misses_anchor / max(1, anchor_calls * U_all),
         "cold_step_ms": cold_ms,
         "kernels": kernels,
         "roofline": roof,
         "eager_gpu_ms_per_step": eager_gpu_ms,
-        "hbm_footprint_GiB": (w0.num_layers * U * w.B * R) / 2**30,
+        "hbm_footprint_GiB": (w0.num_layers * U_all * w.B * R) / 2**30,
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle baseline")
-        result["cpu_baseline"] = cpu_baseline(w, cache, sel_host[:, :U], args.cpu_budget)
-    for e in sync_events:
+        result["cpu_baseline"] = cpu_baseline(w, cache, sel_host[:, :mbs[0].U], args.cpu_budget)
+    for mb in mbs:
+        for e in mb.sync + mb.link:
+            hip.L.hipEventDestroy(e)
+        mb.cache.close()
+    for e in [fork_ev] + join_evs:
         hip.L.hipEventDestroy(e)
-    cache.close()
     print(json.dumps(result), flush=True)
     return 0
 

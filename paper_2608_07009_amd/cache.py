@@ -12,10 +12,10 @@ class HiSparseCache:
                  capacity: int, num_records: int, top_k: int, record_bytes: int,
                  share_group: int = 1, fetch: int = hs.HISPARSE_FETCH_ZERO_COPY,
                  host_memory: int = hs.HISPARSE_HOST_COHERENT, transfer_block_bytes: int = 0,
-                 device: int = 0):
+                 fetch_workgroups: int = 0, device: int = 0):
         self.desc = hs.CacheDesc(num_requests, num_layers, units_per_request, capacity,
                                  num_records, top_k, record_bytes, share_group, fetch,
-                                 host_memory, transfer_block_bytes, 0)
+                                 host_memory, transfer_block_bytes, fetch_workgroups)
         self.units = num_requests * units_per_request
         self.handle = hs.hisparse_cache_create(self.desc, device)
 

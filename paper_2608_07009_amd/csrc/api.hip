@@ -31,7 +31,11 @@ bool is_anchor(const hisparse_cache* c, int32_t layer) {
 }
 
 int transfer_block(const hisparse_cache_desc_t& d) {
-  return d.transfer_block_bytes == 0 ? 64 : d.transfer_block_bytes;
+  return d.transfer_block_bytes == 0 ? 32 : d.transfer_block_bytes;
+}
+
+int fetch_workgroups(const hisparse_cache_desc_t& d) {
+  return d.fetch_workgroups == 0 ? 64 : d.fetch_workgroups;
 }
 
 void free_all(hisparse_cache* c) {
@@ -121,7 +125,7 @@ hisparse_status_t hisparse_validate_desc(const hisparse_cache_desc_t* d) {
   const int tb = d->transfer_block_bytes;
   if (!(tb == 0 || tb == 16 || tb == 32 || tb == 64 || tb == 128 || tb == 256))
     return HISPARSE_ERR_INVALID_ARG;
-  if (d->reserved != 0) return HISPARSE_ERR_INVALID_ARG;
+  if (d->fetch_workgroups < 0 || d->fetch_workgroups > 4096) return HISPARSE_ERR_INVALID_ARG;
   // the resolve kernel keeps the sorted misses, the slot outputs and two slot bitmaps in LDS
   if (hisparse::resolve_lds_bytes(d->top_k, d->capacity) > 64 * 1024)
     return HISPARSE_ERR_INVALID_ARG;
@@ -386,7 +390,8 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
     f.k = c->desc.top_k;
     f.R = (int32_t)R;
     f.units = nu;
-    if (hisparse::launch_fetch(f, transfer_block(c->desc), stream) != hipSuccess)
+    if (hisparse::launch_fetch(f, transfer_block(c->desc), fetch_workgroups(c->desc), stream) !=
+        hipSuccess)
       return HISPARSE_ERR_HIP;
   }
   return HISPARSE_OK;

@@ -57,7 +57,8 @@ struct StateArgs {
 };
 
 hipError_t launch_resolve(const ResolveArgs& a, hipStream_t stream);
-hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, hipStream_t stream);
+hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgroups,
+                        hipStream_t stream);
 hipError_t launch_reset_state(const StateArgs& a, hipStream_t stream);
 size_t resolve_lds_bytes(int32_t k, int32_t B);
 int resolve_threads(int32_t B);

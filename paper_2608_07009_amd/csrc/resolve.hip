@@ -20,10 +20,12 @@
 //   Phase 5  update page table / slot map / stamps, record the miss plan, and publish the
 //            slot of every input entry in input order.
 // fetch_kernel: copies each planned record from the pinned host pool (zero-copy 16-byte
-//   loads through the mapped address) into its slot; a wide grid over all units' misses, so a
-//   layer call with few units still keeps many loads in flight across the chip. One launch can
-//   serve several layers of a share group (grid z): the anchor's demand fetch and the replays
-//   of the same plan into its shared layers.
+//   loads through the mapped address) into its slot. The grid is small (a fixed workgroup
+//   budget shared by the launch's units, each thread keeping one transfer block of loads in
+//   flight): about 1 MB of reads in flight saturates the host link, and the CUs it leaves
+//   idle run attention or resolve work of other streams meanwhile. One launch can serve
+//   several layers of a share group (grid z): the anchor's demand fetch and the replays of
+//   the same plan into its shared layers.
 #include "internal.h"
 
 namespace hisparse {
@@ -414,11 +416,14 @@ hipError_t launch_resolve(const ResolveArgs& a, hipStream_t stream) {
   }
 }
 
-hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, hipStream_t stream) {
+hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgroups,
+                        hipStream_t stream) {
   const int U = transfer_block_bytes / 16;
   const int64_t max_chunks = (int64_t)a.k * (a.R / 16);
   int64_t x = (max_chunks + 256LL * U - 1) / (256LL * U);
-  const int64_t cap = std::max<int64_t>(1, 4096 / ((int64_t)a.units * a.n_layers));
+  // the workgroup budget is shared by the launch's (unit, layer) pairs; each pair's workgroups
+  // stride over its plan, so any x >= 1 covers it
+  const int64_t cap = std::max<int64_t>(1, workgroups / ((int64_t)a.units * a.n_layers));
   if (x > cap) x = cap;
   const dim3 grid((unsigned)x, (unsigned)a.units, (unsigned)a.n_layers);
   const FastDiv f = make_fastdiv((uint32_t)(a.R / 16));

@@ -49,7 +49,7 @@ class CacheDesc(ctypes.Structure):
                 ("num_records", ctypes.c_int64), ("top_k", ctypes.c_int32),
                 ("record_bytes", ctypes.c_int32), ("share_group", ctypes.c_int32),
                 ("fetch", ctypes.c_int32), ("host_memory", ctypes.c_int32),
-                ("transfer_block_bytes", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("transfer_block_bytes", ctypes.c_int32), ("fetch_workgroups", ctypes.c_int32)]
 
 
 class AttnDesc(ctypes.Structure):

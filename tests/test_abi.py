@@ -33,7 +33,7 @@ def desc_for(w, **kw):
     d = dict(num_requests=w.num_requests, num_layers=w.num_layers,
              units_per_request=w.units_per_request, capacity=w.B, num_records=w.L, top_k=w.k,
              record_bytes=w.record_bytes, share_group=w.share_group, fetch=0, host_memory=0,
-             transfer_block_bytes=0, reserved=0)
+             transfer_block_bytes=0, fetch_workgroups=0)
     d.update(kw)
     return hs.CacheDesc(**d)
 
@@ -59,7 +59,8 @@ def test_workload_descriptors_are_valid(cfg):
     ("fetch", 3, hs.HISPARSE_ERR_UNSUPPORTED),
     ("host_memory", 7, hs.HISPARSE_ERR_INVALID_ARG),
     ("transfer_block_bytes", 48, hs.HISPARSE_ERR_INVALID_ARG),
-    ("reserved", 1, hs.HISPARSE_ERR_INVALID_ARG),
+    ("fetch_workgroups", -1, hs.HISPARSE_ERR_INVALID_ARG),
+    ("fetch_workgroups", 4097, hs.HISPARSE_ERR_INVALID_ARG),
     ("capacity", 20000, hs.HISPARSE_ERR_INVALID_ARG),        # beyond the LDS-resident maximum
 ])
 def test_invalid_descriptors(field, value, status):
