@@ -61,11 +61,11 @@ def parse():
                          "2 requests, else 1)")
     ap.add_argument("--fetch-workgroups", type=int, default=0,
                     help="workgroups of one fetch launch (0 = the library default)")
-    ap.add_argument("--schedule", choices=["overlap", "serial", "batched"], default="overlap",
-                    help="shared layers: 'overlap' replays them on a side stream while the "
-                         "anchor's attention runs, each replay releasing its layer's attention; "
-                         "'serial' fetches the anchor and its shared layers in one launch, then "
-                         "runs the layers' attention in order; 'batched' (not realisable in a "
+    ap.add_argument("--schedule", choices=["serial", "overlap", "batched"], default="serial",
+                    help="shared layers: 'serial' fetches the anchor and its shared layers in "
+                         "one launch, then runs the layers' attention in order; 'overlap' "
+                         "replays them on a side stream while the anchor's attention runs, each "
+                         "replay releasing its layer's attention; 'batched' (not realisable in a "
                          "model: later layers' queries depend on earlier layers) decodes the "
                          "group's layers in one attention launch")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",

@@ -95,16 +95,15 @@ typedef struct {
   int32_t fetch;                 /* hisparse_fetch_t */
   int32_t host_memory;           /* hisparse_host_memory_t */
   int32_t transfer_block_bytes;  /* bytes each fetch thread keeps in flight: 16, 32, 64, 128
-                                    or 256 (the paper's swap-in transfer block size); 0 = 32.
-                                    32 and 64 keep the fetch kernel within 40 VGPRs, which lets
-                                    its waves share a SIMD with a latent-attention wave (472),
-                                    so a concurrent attention launch loses no CU to it */
-  int32_t fetch_workgroups;      /* 256-thread workgroups of one fetch launch, 0 .. 4096, spread
-                                    over its units and target layers (at least one per unit and
-                                    layer); 0 = 64. The host link saturates with about 1 MB of
-                                    reads in flight, so a small grid moves misses as fast as a
-                                    wide one and leaves the other CUs to kernels running
-                                    concurrently on other streams (attention, resolve) */
+                                    or 256 (the paper's swap-in transfer block size); 0 = 16 */
+  int32_t fetch_workgroups;      /* one-wave (64-thread) workgroups of one fetch launch,
+                                    0 .. 4096, shared by its units and target layers (at least
+                                    one per unit and layer); 0 = 256. A few hundred KB of host
+                                    reads in flight saturate the link, so a thin grid moves
+                                    misses as fast as a wide one while keeping few slow host
+                                    reads outstanding per CU, which leaves kernels of other
+                                    streams on the same CUs (attention, resolve) nearly
+                                    undisturbed */
 } hisparse_cache_desc_t;
 
 /* Sparse decode attention descriptor. The token layout inside a record is

@@ -31,11 +31,11 @@ bool is_anchor(const hisparse_cache* c, int32_t layer) {
 }
 
 int transfer_block(const hisparse_cache_desc_t& d) {
-  return d.transfer_block_bytes == 0 ? 32 : d.transfer_block_bytes;
+  return d.transfer_block_bytes == 0 ? 16 : d.transfer_block_bytes;
 }
 
 int fetch_workgroups(const hisparse_cache_desc_t& d) {
-  return d.fetch_workgroups == 0 ? 64 : d.fetch_workgroups;
+  return d.fetch_workgroups == 0 ? 256 : d.fetch_workgroups;
 }
 
 void free_all(hisparse_cache* c) {

@@ -20,10 +20,11 @@
 //   Phase 5  update page table / slot map / stamps, record the miss plan, and publish the
 //            slot of every input entry in input order.
 // fetch_kernel: copies each planned record from the pinned host pool (zero-copy 16-byte
-//   loads through the mapped address) into its slot. The grid is small (a fixed workgroup
-//   budget shared by the launch's units, each thread keeping one transfer block of loads in
-//   flight): about 1 MB of reads in flight saturates the host link, and the CUs it leaves
-//   idle run attention or resolve work of other streams meanwhile. One launch can serve
+//   loads through the mapped address) into its slot. The grid is small: a fixed budget of
+//   one-wave workgroups shared by the launch's units, each thread keeping one transfer block
+//   of loads in flight. A few hundred KB of reads in flight saturate the host link; spread
+//   thinly over the chip, the fetch keeps only a few slow host reads outstanding per CU, so
+//   attention or resolve work of other streams running on the same CUs is barely delayed. One launch can serve
 //   several layers of a share group (grid z): the anchor's demand fetch and the replays of
 //   the same plan into its shared layers.
 #include "internal.h"
@@ -36,6 +37,9 @@ constexpr int kMaxChunk = 16;  // order entries per thread: B <= 16 * threads
 constexpr int kMaxPer = 4;     // selections per thread: k <= 4 * threads
 constexpr int kBucketBits = 11;
 constexpr int kBuckets = 1 << kBucketBits;  // miss rank buckets (high position bits)
+// One wave per fetch workgroup: each CU that hosts fetch work gives it one wave and a few
+// outstanding host reads, not a whole workgroup's worth.
+constexpr int kFetchThreads = 64;
 
 __device__ inline int wave_incl_scan(int x, int lane) {
 #pragma unroll
@@ -334,7 +338,7 @@ __device__ inline uint32_t fastdiv(uint32_t n, FastDiv f) {
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 template <int U>
-__global__ __launch_bounds__(256) void fetch_kernel(FetchArgs a, FastDiv div_cpr) {
+__global__ __launch_bounds__(kFetchThreads) void fetch_kernel(FetchArgs a, FastDiv div_cpr) {
   const int unit = blockIdx.y;
   const int m = a.plan_count[unit];
   const uint32_t cpr = (uint32_t)a.R >> 4;  // 16-byte chunks per record
@@ -343,8 +347,9 @@ __global__ __launch_bounds__(256) void fetch_kernel(FetchArgs a, FastDiv div_cpr
   // grid z: the target layers (one plan, each layer's own host records and cache)
   const uint8_t* host = a.host[blockIdx.z] + (int64_t)unit * a.L * a.R;
   uint8_t* cache = a.cache + (int64_t)blockIdx.z * a.cache_stride + (int64_t)unit * a.B * a.R;
-  const uint32_t stride = gridDim.x * 256u;
-  for (uint32_t c0 = blockIdx.x * 256u + threadIdx.x; c0 < total; c0 += stride * U) {
+  const uint32_t stride = gridDim.x * (uint32_t)kFetchThreads;
+  for (uint32_t c0 = blockIdx.x * (uint32_t)kFetchThreads + threadIdx.x; c0 < total;
+       c0 += stride * U) {
     u32x4 v[U];
     int64_t dst[U];
 #pragma unroll
@@ -420,7 +425,7 @@ hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgr
                         hipStream_t stream) {
   const int U = transfer_block_bytes / 16;
   const int64_t max_chunks = (int64_t)a.k * (a.R / 16);
-  int64_t x = (max_chunks + 256LL * U - 1) / (256LL * U);
+  int64_t x = (max_chunks + (int64_t)kFetchThreads * U - 1) / ((int64_t)kFetchThreads * U);
   // the workgroup budget is shared by the launch's (unit, layer) pairs; each pair's workgroups
   // stride over its plan, so any x >= 1 covers it
   const int64_t cap = std::max<int64_t>(1, workgroups / ((int64_t)a.units * a.n_layers));
@@ -428,11 +433,11 @@ hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgr
   const dim3 grid((unsigned)x, (unsigned)a.units, (unsigned)a.n_layers);
   const FastDiv f = make_fastdiv((uint32_t)(a.R / 16));
   switch (U) {
-    case 1: hipLaunchKernelGGL(fetch_kernel<1>, grid, dim3(256), 0, stream, a, f); break;
-    case 2: hipLaunchKernelGGL(fetch_kernel<2>, grid, dim3(256), 0, stream, a, f); break;
-    case 4: hipLaunchKernelGGL(fetch_kernel<4>, grid, dim3(256), 0, stream, a, f); break;
-    case 8: hipLaunchKernelGGL(fetch_kernel<8>, grid, dim3(256), 0, stream, a, f); break;
-    default: hipLaunchKernelGGL(fetch_kernel<16>, grid, dim3(256), 0, stream, a, f); break;
+    case 1: hipLaunchKernelGGL(fetch_kernel<1>, grid, dim3(kFetchThreads), 0, stream, a, f); break;
+    case 2: hipLaunchKernelGGL(fetch_kernel<2>, grid, dim3(kFetchThreads), 0, stream, a, f); break;
+    case 4: hipLaunchKernelGGL(fetch_kernel<4>, grid, dim3(kFetchThreads), 0, stream, a, f); break;
+    case 8: hipLaunchKernelGGL(fetch_kernel<8>, grid, dim3(kFetchThreads), 0, stream, a, f); break;
+    default: hipLaunchKernelGGL(fetch_kernel<16>, grid, dim3(kFetchThreads), 0, stream, a, f); break;
   }
   return hipGetLastError();
 }
