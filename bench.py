@@ -59,6 +59,9 @@ def parse():
                     help="independent request groups, each with its own cache handle and "
                          "streams, whose steps run concurrently (0 = 2 when there are at least "
                          "2 requests, else 1)")
+    ap.add_argument("--turns", choices=["first", "all"], default="first",
+                    help="micro-batches take turns on the host link at the first layer only "
+                         "(then run free from that offset), or at every layer")
     ap.add_argument("--fetch-workgroups", type=int, default=0,
                     help="workgroups of one fetch launch (0 = the library default)")
     ap.add_argument("--schedule", choices=["serial", "overlap", "batched"], default="serial",
@@ -391,7 +394,11 @@ def main() -> int:
         into it. Micro-batches take turns on the host link: the transfer of group g of
         micro-batch i waits for that of micro-batch i-1 (and micro-batch 0's for the last
         micro-batch's transfer of group g-1), so while one micro-batch moves its misses the
-        others resolve and attend instead of splitting the link and falling into lockstep."""
+        others resolve and attend instead of splitting the link and falling into lockstep.
+        With --turns first (the default) only the first group is ordered this way; from that
+        offset the chains run free, with no cross-stream wait per layer. Where a chain's
+        compute is short next to its transfer the two transfers end up sharing the link,
+        which leaves the link just as busy."""
         if n_mb > 1:
             rec(fork_ev, root_s)
             for mb in mbs[1:]:
@@ -399,7 +406,7 @@ def main() -> int:
         for gi in range(len(groups)):
             for i, mb in enumerate(mbs):
                 link = None
-                if n_mb > 1:
+                if n_mb > 1 and (args.turns == "all" or gi == 0):
                     prev = (mbs[i - 1].link[gi] if i > 0 else
                             (mbs[-1].link[gi - 1] if gi > 0 else None))
                     link = (prev, mb.link[gi])

@@ -898,11 +898,14 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
   if (attn->num_splits > 0) {
     splits = std::min(attn->num_splits, max_splits);
   } else {
-    // about one workgroup per CU, but at least four chunks per token group in every split so
-    // the load pipeline reaches steady state
+    // about one workgroup per CU, but at least four chunks per token group (two for latent
+    // attention) in every split so the load pipeline reaches steady state
     const int per_split = units * p.hb;
     splits = (kTargetWorkgroups + per_split - 1) / per_split;
-    const int min_work_splits = std::max(1, p.n_tok / ((is_mla(*attn) ? 2 : 4) * chunk));
+    int chunks_per_split = is_mla(*attn) ? 2 : 4;
+    // a call too small to give even 64 such workgroups is all latency: one chunk per split
+    if (is_mla(*attn) && (int64_t)per_split * (p.n_tok / (2 * chunk)) < 64) chunks_per_split = 1;
+    const int min_work_splits = std::max(1, p.n_tok / (chunks_per_split * chunk));
     splits = std::max(1, std::min({splits, max_splits, min_work_splits}));
   }
   const int max_split_tokens = std::min(kMaxSplitRecords * attn->tokens_per_record, kMaxSplitTokens);
