@@ -64,13 +64,15 @@ def parse():
                          "(then run free from that offset), or at every layer")
     ap.add_argument("--fetch-workgroups", type=int, default=0,
                     help="workgroups of one fetch launch (0 = the library default)")
-    ap.add_argument("--schedule", choices=["serial", "overlap", "batched"], default="serial",
-                    help="shared layers: 'serial' fetches the anchor and its shared layers in "
-                         "one launch, then runs the layers' attention in order; 'overlap' "
-                         "replays them on a side stream while the anchor's attention runs, each "
-                         "replay releasing its layer's attention; 'batched' (not realisable in a "
-                         "model: later layers' queries depend on earlier layers) decodes the "
-                         "group's layers in one attention launch")
+    ap.add_argument("--schedule", choices=["overlap", "serial", "side", "batched"],
+                    default="overlap",
+                    help="shared layers: 'overlap' lets each layer's attention launch carry the "
+                         "replay into the next shared layer; 'serial' fetches the anchor and "
+                         "its shared layers in one launch, then runs the layers' attention in "
+                         "order; 'side' replays into the shared layers on a side stream from "
+                         "the end of the resolve on; 'batched' (not realisable in a model: "
+                         "later layers' queries depend on earlier layers) decodes the group's "
+                         "layers in one attention launch")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run one device-to-device copy of BYTES (calibrates the HBM "
                          "byte counters of a profiler run) and exit")
@@ -317,7 +319,8 @@ def main() -> int:
         f"{args.schedule}, set up in {time.time() - t0:.1f}s")
 
     f_tables, f_fetch = L.hisparse_resolve_tables, L.hisparse_fetch
-    f_prefetch, f_decode = L.hisparse_prefetch_layer, L.hisparse_sparse_decode
+    f_prefetch_layers, f_decode = L.hisparse_prefetch_layers, L.hisparse_sparse_decode
+    f_decode_prefetch = L.hisparse_sparse_decode_prefetch
     f_decode_layers, f_fetch_group = L.hisparse_sparse_decode_layers, L.hisparse_fetch_group
     rec = hip.L.hipEventRecord
     wait = hip.L.hipStreamWaitEvent
@@ -374,20 +377,31 @@ def main() -> int:
             transfer("fetch_group", f_fetch_group, h, a, 1 + len(shared), ms)
             call("sparse_decode_layers", ms, ev, spans, f_decode_layers, h, a, 1 + len(shared),
                  qv[a], mb.slot_p[a], mb.out_p[a], ad_ref, mb.ws.data_ptr(), mb.ws_bytes, ms)
-        else:
-            # overlap (Section 3.5): the anchor's fetch first, then its attention on the main
-            # stream while the side stream replays the plan into the shared layers one by one,
-            # each replay releasing its layer's attention
-            transfer("fetch", f_fetch, h, a, ms)
+        elif args.schedule == "side":
+            # as soon as the resolve has recorded the plan, a side stream replays it into all
+            # shared layers in one launch, sharing the host link with the anchor's own fetch
+            # and running under the anchor's attention; the shared layers' attention waits
             rec(mb.sync[0], ms)
             wait(ss, mb.sync[0], 0)
-            for i, l in enumerate(shared):
-                call("prefetch_replay", ss, ev, spans, f_prefetch, h, a, l, ss)
-                rec(mb.sync[1 + i], ss)
+            call("prefetch_replay", ss, ev, spans, f_prefetch_layers, h, a, shared[0],
+                 len(shared), ss)
+            rec(mb.sync[1], ss)
+            transfer("fetch", f_fetch, h, a, ms)
             decode(a)
-            for i, l in enumerate(shared):
-                wait(ms, mb.sync[1 + i], 0)
+            wait(ms, mb.sync[1], 0)
+            for l in shared:
                 decode(l)
+        else:
+            # overlap (Section 3.5), on one stream: the anchor's fetch, then each layer's
+            # attention launch carries the replay of the plan into the next shared layer, so
+            # layer l+1's misses cross the host link while layer l attends
+            transfer("fetch", f_fetch, h, a, ms)
+            layers = [a] + shared
+            for i, l in enumerate(layers[:-1]):
+                call("sparse_decode_prefetch", ms, ev, spans, f_decode_prefetch, h, l, qv[l],
+                     mb.slot_p[a], mb.out_p[l], ad_ref, mb.ws.data_ptr(), mb.ws_bytes, a,
+                     layers[i + 1], 1, ms)
+            decode(layers[-1])
 
     def step(t, ev=None, spans=None, sel_override=None, q_override=None):
         """Enqueue decode step t of every micro-batch: forked from the root stream, joined back
@@ -471,7 +485,7 @@ def main() -> int:
         d = hip.ms(e0, e1) * 1e-3
         t_sum, n = tot.get(name, (0.0, 0))
         tot[name] = (t_sum + d, n + 1)
-        if name in ("fetch", "prefetch_replay", "fetch_group"):
+        if name in ("fetch", "prefetch_replay", "fetch_group", "sparse_decode_prefetch"):
             io_intervals.append((hip.ms(ref, e0) * 1e-3, hip.ms(ref, e1) * 1e-3))
     for e in events:
         hip.L.hipEventDestroy(e)
@@ -504,13 +518,17 @@ def main() -> int:
     t_lay, n_lay = kernel("sparse_decode_layers")
     grouped = [(a, sh) for a, sh in groups if sh and args.schedule in ("serial", "batched")]
     lay_calls = K * n_mb * sum(1 + len(sh) for _, sh in grouped) if n_lay else 0
+    t_pf, n_pf = kernel("sparse_decode_prefetch")  # attention carrying a replay
     t_att_one, n_att_one = t_att, n_att
-    t_att, n_att = t_att + t_lay, n_att + lay_calls
+    t_att, n_att = t_att + t_lay + t_pf, n_att + lay_calls + n_pf
     misses_grouped = sum(int(c[:, a, :, 1].sum()) for a, _ in grouped)
     fetch_bytes = (misses_anchor - misses_grouped) * R      # plain demand fetches
     group_bytes = sum(int(c[:, a, :, 1].sum()) * (1 + len(sh)) for a, sh in grouped) * R
     replay_bytes = sum(int(c[:, a, :, 1].sum()) * len(sh) for a, sh in groups
                        if sh and (a, sh) not in grouped) * R
+    carried_bytes = replay_bytes if n_pf else 0  # replays inside attention launches
+    if n_pf:
+        replay_bytes = 0
     moves_data = fetch != hs.HISPARSE_FETCH_NONE
     kernels = {}
     # resolve tables: integer metadata work per unit (algorithmic bytes):
@@ -533,8 +551,16 @@ def main() -> int:
                                   "GBps": group_bytes / t_grp / 1e9}
     if n_rep and moves_data:
         kernels["prefetch_replay"] = {"launches": n_rep, "avg_us": t_rep / n_rep * 1e6,
+                                      "layers_per_launch": len(groups[0][1]),
                                       "bytes_per_launch": replay_bytes / n_rep,
                                       "GBps": replay_bytes / t_rep / 1e9}
+    if n_pf and moves_data:
+        kernels["sparse_decode_prefetch"] = {
+            "launches": n_pf, "avg_us": t_pf / n_pf * 1e6,
+            "replay_bytes_per_launch": carried_bytes / n_pf,
+            "GBps": carried_bytes / t_pf / 1e9,
+            "note": "attention of one layer with the replay into the next shared layer in the "
+                    "same launch; also counted in sparse_decode"}
     n_tok = k * w.tokens_per_record
     att_flops_call = 2.0 * U * w.q_heads * n_tok * (w.d_qk + w.d_v)
     att_bytes_call = (U * n_tok * (R // w.tokens_per_record) + U * w.q_heads * w.d_qk * 2
@@ -559,10 +585,15 @@ def main() -> int:
     # dominant kernel by total event time
     totals = {"resolve_tables": t_tab, "fetch": t_fet if moves_data else 0.0,
               "prefetch_replay": t_rep if moves_data else 0.0,
-              "fetch_group": t_grp if moves_data else 0.0, "sparse_decode": t_att}
+              "fetch_group": t_grp if moves_data else 0.0,
+              "sparse_decode_prefetch": t_pf if moves_data else 0.0,
+              "sparse_decode": t_att - (t_pf if moves_data else 0.0)}
     dom = max(totals, key=totals.get)
-    if dom in ("fetch", "prefetch_replay", "fetch_group"):
-        kd = kernels[dom]
+    if dom == "sparse_decode_prefetch":  # host-link bound: the replay outlasts the attention
+        kd = dict(kernels[dom], bytes_per_launch=kernels[dom]["replay_bytes_per_launch"])
+    else:
+        kd = kernels.get(dom)
+    if dom in ("fetch", "prefetch_replay", "fetch_group", "sparse_decode_prefetch"):
         tr = traffic_record(w.name, dom)
         if tr:
             tr["read_vs_algorithmic"] = tr["fetch_bytes"] / kd["bytes_per_launch"]
@@ -574,7 +605,6 @@ def main() -> int:
                 "frac_of_measured_peak": (kd["GBps"] / pinned_peak) if pinned_peak else None,
                 "algorithmic_bytes_per_launch": kd["bytes_per_launch"]}
     elif dom == "sparse_decode":
-        kd = kernels[dom]
         t_hbm = att_bytes_call / (HBM_PEAK_GBPS * 1e9)
         t_mfma = att_flops_call / (MFMA_BF16_PEAK_TFLOPS * 1e12)
         if t_hbm >= t_mfma:
@@ -591,7 +621,7 @@ def main() -> int:
                 "unit": "GB/s", "frac": kd["hbm_GBps"] / HBM_PEAK_GBPS, "traffic": None}
 
     io_busy = union_length(io_intervals)
-    miss_gbps = ((fetch_bytes + replay_bytes + group_bytes) / io_busy / 1e9
+    miss_gbps = ((fetch_bytes + replay_bytes + group_bytes + carried_bytes) / io_busy / 1e9
                  if (io_busy and moves_data) else None)
 
     # the same steps replayed from one captured HIP graph (cold reset, same warmup)

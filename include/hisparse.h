@@ -212,6 +212,17 @@ hisparse_status_t hisparse_fetch_group(hisparse_cache_t cache, int32_t anchor_la
 hisparse_status_t hisparse_prefetch_layer(hisparse_cache_t cache, int32_t anchor_layer,
                                           int32_t shared_layer, void* stream);
 
+/* [async] hisparse_prefetch_layer for the num_layers consecutive shared layers first_shared ..
+ * first_shared + num_layers - 1 of `anchor_layer`'s group, in one launch (Section 3.5): the
+ * side-stream form of the replay, started as soon as the anchor's resolve has recorded its
+ * plan, so that it shares the host link with the anchor's own fetch and runs under the anchor
+ * layer's attention. Same ordering rules as hisparse_prefetch_layer. HISPARSE_ERR_INVALID_ARG
+ * unless anchor < first_shared and first_shared + num_layers <= min(anchor + share_group,
+ * num_layers), num_layers >= 1. */
+hisparse_status_t hisparse_prefetch_layers(hisparse_cache_t cache, int32_t anchor_layer,
+                                           int32_t first_shared, int32_t num_layers,
+                                           void* stream);
+
 /* Bytes of device workspace hisparse_sparse_decode(_pool) needs for `units` units of top_k
  * records each; 0 if the descriptor is invalid. */
 size_t hisparse_decode_workspace_bytes(int32_t units, int32_t top_k, int32_t record_bytes,
@@ -233,6 +244,22 @@ hisparse_status_t hisparse_sparse_decode(hisparse_cache_t cache, int32_t layer, 
                                          const int32_t* d_slots, float* d_out,
                                          const hisparse_attn_desc_t* attn, void* d_workspace,
                                          size_t workspace_bytes, void* stream);
+
+/* [async] hisparse_sparse_decode of `layer` and, in the same launch, the exact-prefetch replay
+ * of `anchor_layer`'s latest plan into shared layers [first_shared, first_shared + num_shared)
+ * (Section 3.5): equal to hisparse_prefetch_layers followed by hisparse_sparse_decode, but the
+ * replay runs in extra workgroups beside the attention, so the next layers' misses cross the
+ * host link while this layer attends, on one stream. Ordering rules of
+ * hisparse_prefetch_layer apply to the replay. With HISPARSE_FETCH_SDMA the replay is issued
+ * on its own first (host-synchronising); with HISPARSE_FETCH_NONE nothing is copied.
+ * HISPARSE_ERR_INVALID_ARG for a replay range hisparse_prefetch_layers would refuse, for
+ * num_shared > 8, or if `layer` is one of the replay's targets. */
+hisparse_status_t hisparse_sparse_decode_prefetch(hisparse_cache_t cache, int32_t layer,
+                                                  const void* d_q, const int32_t* d_slots,
+                                                  float* d_out, const hisparse_attn_desc_t* attn,
+                                                  void* d_workspace, size_t workspace_bytes,
+                                                  int32_t anchor_layer, int32_t first_shared,
+                                                  int32_t num_shared, void* stream);
 
 /* [async] Sparse decode attention of layers [first_layer, first_layer + num_layers) of one
  * share group in a single launch (Section 3.5: the shared layers read their records through

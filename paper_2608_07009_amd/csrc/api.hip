@@ -309,6 +309,28 @@ hisparse_status_t hisparse_resolve_tables(hisparse_cache_t c, int32_t layer,
 }
 
 namespace {
+// Kernel arguments for copying `anchor`'s latest miss plan into target layers [target, target +
+// n_layers) (n_layers <= kMaxFetchLayers), units [u0, u0 + nu).
+hisparse::FetchArgs fetch_args(hisparse_cache_t c, int32_t anchor, int32_t target, int32_t u0,
+                               int32_t nu, int32_t n_layers) {
+  auto& an = c->anchors[anchor / c->desc.share_group];
+  const int64_t L = c->desc.num_records, B = c->desc.capacity, R = c->desc.record_bytes;
+  hisparse::FetchArgs f{};
+  f.n_layers = n_layers;
+  f.plan = an.plan + (int64_t)u0 * c->desc.top_k;
+  f.plan_count = an.plan_count + u0;
+  for (int32_t j = 0; j < n_layers; ++j)
+    f.host[j] = reinterpret_cast<const uint8_t*>(c->host_dev[target + j]) + (int64_t)u0 * L * R;
+  f.cache = c->cache[target] + (int64_t)u0 * B * R;
+  f.cache_stride = (int64_t)c->cache_layer_bytes;
+  f.L = L;
+  f.B = (int32_t)B;
+  f.k = c->desc.top_k;
+  f.R = (int32_t)R;
+  f.units = nu;
+  return f;
+}
+
 // Copy the records of `anchor`'s latest miss plan from each target layer's host pool into
 // its GPU cache, for targets [target, target + n_layers) and units [u0, u0 + nu) (target ==
 // anchor: the demand fetch; a shared layer: the prefetch replay).
@@ -374,22 +396,9 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
         return HISPARSE_ERR_HIP;
     return HISPARSE_OK;
   }
-  const int64_t L = c->desc.num_records, B = c->desc.capacity, R = c->desc.record_bytes;
   for (int32_t j0 = 0; j0 < n_layers; j0 += hisparse::kMaxFetchLayers) {
-    hisparse::FetchArgs f{};
-    f.n_layers = std::min(n_layers - j0, hisparse::kMaxFetchLayers);
-    f.plan = an.plan + (int64_t)u0 * c->desc.top_k;
-    f.plan_count = an.plan_count + u0;
-    for (int32_t j = 0; j < f.n_layers; ++j)
-      f.host[j] = reinterpret_cast<const uint8_t*>(c->host_dev[target + j0 + j]) +
-                  (int64_t)u0 * L * R;
-    f.cache = c->cache[target + j0] + (int64_t)u0 * B * R;
-    f.cache_stride = (int64_t)c->cache_layer_bytes;
-    f.L = L;
-    f.B = (int32_t)B;
-    f.k = c->desc.top_k;
-    f.R = (int32_t)R;
-    f.units = nu;
+    const hisparse::FetchArgs f = fetch_args(c, anchor, target + j0, u0, nu,
+                                             std::min(n_layers - j0, hisparse::kMaxFetchLayers));
     if (hisparse::launch_fetch(f, transfer_block(c->desc), fetch_workgroups(c->desc), stream) !=
         hipSuccess)
       return HISPARSE_ERR_HIP;
@@ -435,6 +444,17 @@ hisparse_status_t hisparse_prefetch_layer(hisparse_cache_t c, int32_t anchor_lay
   return enqueue_fetch(c, anchor_layer, shared_layer, as_stream(stream));
 }
 
+hisparse_status_t hisparse_prefetch_layers(hisparse_cache_t c, int32_t anchor_layer,
+                                           int32_t first_shared, int32_t num_layers,
+                                           void* stream) {
+  if (!c || !is_anchor(c, anchor_layer) || num_layers < 1) return HISPARSE_ERR_INVALID_ARG;
+  const int64_t end = (int64_t)first_shared + num_layers;
+  if (first_shared <= anchor_layer ||
+      end > std::min<int64_t>((int64_t)anchor_layer + c->desc.share_group, c->desc.num_layers))
+    return HISPARSE_ERR_INVALID_ARG;
+  return enqueue_fetch(c, anchor_layer, first_shared, as_stream(stream), 0, -1, num_layers);
+}
+
 size_t hisparse_decode_workspace_bytes(int32_t units, int32_t top_k, int32_t record_bytes,
                                        const hisparse_attn_desc_t* attn) {
   hisparse::AttnPlan p{};
@@ -472,6 +492,47 @@ hisparse_status_t hisparse_sparse_decode(hisparse_cache_t c, int32_t layer, cons
   return hisparse_sparse_decode_pool(c->cache[layer], c->desc.capacity, c->desc.record_bytes,
                                      c->units, c->desc.top_k, d_q, d_slots, d_out, attn,
                                      d_workspace, workspace_bytes, stream);
+}
+
+hisparse_status_t hisparse_sparse_decode_prefetch(hisparse_cache_t c, int32_t layer,
+                                                  const void* d_q, const int32_t* d_slots,
+                                                  float* d_out, const hisparse_attn_desc_t* attn,
+                                                  void* d_workspace, size_t workspace_bytes,
+                                                  int32_t anchor_layer, int32_t first_shared,
+                                                  int32_t num_shared, void* stream) {
+  if (!c || layer < 0 || layer >= c->desc.num_layers) return HISPARSE_ERR_INVALID_ARG;
+  if (!is_anchor(c, anchor_layer) || num_shared < 1 || num_shared > hisparse::kMaxFetchLayers)
+    return HISPARSE_ERR_INVALID_ARG;
+  const int64_t end = (int64_t)first_shared + num_shared;
+  if (first_shared <= anchor_layer ||
+      end > std::min<int64_t>((int64_t)anchor_layer + c->desc.share_group, c->desc.num_layers))
+    return HISPARSE_ERR_INVALID_ARG;
+  if (layer >= first_shared && layer < end) return HISPARSE_ERR_INVALID_ARG;  // reads what it writes
+  if (!d_q || !d_slots || !d_out || !d_workspace) return HISPARSE_ERR_INVALID_ARG;
+  if (c->desc.fetch != HISPARSE_FETCH_ZERO_COPY) {
+    // no kernel-issued copy to carry: the replay on its own (or nothing), then the attention
+    const hisparse_status_t st =
+        enqueue_fetch(c, anchor_layer, first_shared, as_stream(stream), 0, -1, num_shared);
+    if (st != HISPARSE_OK) return st;
+    return hisparse_sparse_decode(c, layer, d_q, d_slots, d_out, attn, d_workspace,
+                                  workspace_bytes, stream);
+  }
+  hisparse::AttnPlan p{};
+  hisparse_status_t st =
+      hisparse::plan_attention(c->units, c->desc.top_k, c->desc.record_bytes, attn, &p);
+  if (st != HISPARSE_OK) return st;
+  if (workspace_bytes < p.workspace_bytes) return HISPARSE_ERR_INVALID_ARG;
+  if ((int64_t)c->desc.capacity * c->desc.record_bytes > (int64_t)INT32_MAX)
+    return HISPARSE_ERR_UNSUPPORTED;
+  const hisparse::FetchArgs f = fetch_args(c, anchor_layer, first_shared, 0, c->units, num_shared);
+  if (hisparse::launch_attention(p, *attn, c->cache[layer], c->desc.capacity,
+                                 c->desc.record_bytes, c->units, c->desc.top_k,
+                                 reinterpret_cast<const uint16_t*>(d_q), d_slots, d_out,
+                                 d_workspace, as_stream(stream), 0, &f,
+                                 fetch_workgroups(c->desc) * 64 * 2,
+                                 transfer_block(c->desc) * 2) != hipSuccess)
+    return HISPARSE_ERR_HIP;
+  return HISPARSE_OK;
 }
 
 hisparse_status_t hisparse_sparse_decode_layers(hisparse_cache_t c, int32_t first_layer,

@@ -22,7 +22,9 @@
 // values, so any placement of the same records gives bit-identical outputs.
 #include <math.h>
 
-#include "internal.h"
+#include <algorithm>
+
+#include "fetch_device.h"
 
 namespace hisparse {
 namespace {
@@ -57,7 +59,23 @@ struct AttnArgs {
   int32_t Hp;         // latent attention: heads rounded up to 32 (partial-output block layout)
   int32_t idx_units;  // unit u reads index row u % idx_units
   float scale_log2;
+  // A prefetch replay carried by the launch: pf_per_pair extra workgroups per (unit, target
+  // layer) of pf, after the attention workgroups, copy that plan's records (0: none).
+  FetchArgs pf;
+  FastDiv pf_div;
+  int32_t pf_per_pair, pf_wg, pf_u;  // pf_u: 16-byte loads each replay thread keeps in flight
 };
+
+// An extra workgroup of an attention launch: its share of the carried replay. It shares no
+// memory with the attention workgroups (other layers' caches), so it needs no synchronisation.
+__device__ __forceinline__ void replay_worker(const AttnArgs& a, int e) {
+  const int pair = e / a.pf_per_pair, x = e - pair * a.pf_per_pair;
+  const int unit = pair % a.pf.units, z = pair / a.pf.units;
+  const uint32_t first = x * blockDim.x + threadIdx.x, stride = a.pf_per_pair * blockDim.x;
+  if (a.pf_u >= 4) fetch_slice<4>(a.pf, a.pf_div, unit, z, first, stride);
+  else if (a.pf_u == 2) fetch_slice<2>(a.pf, a.pf_div, unit, z, first, stride);
+  else fetch_slice<1>(a.pf, a.pf_div, unit, z, first, stride);
+}
 
 // Latent-attention partial outputs are stored in the PV accumulators' own layout, so every
 // lane writes 16 contiguous bytes: per part, 32-head block b, output tile n (dims 32n..32n+31),
@@ -185,6 +203,10 @@ void attn_partial_kernel(AttnArgs a) {
   // XCD a contiguous range of work items; the head blocks of one (unit, split) then share the
   // staged records through the same L2.
   const int nwg_pad = (a.n_wg + 7) & ~7;
+  if ((int)blockIdx.x >= nwg_pad) {  // wave-uniform: the whole workgroup replays
+    replay_worker(a, (int)blockIdx.x - nwg_pad);
+    return;
+  }
   const int w = (int)(blockIdx.x & 7) * (nwg_pad >> 3) + (int)(blockIdx.x >> 3);
   if (w >= a.n_wg) return;
   const int hb = w % a.hb;
@@ -490,6 +512,10 @@ void attn_mla_kernel(AttnArgs a) {
 
   // XCD-aware mapping, as in attn_partial_kernel
   const int nwg_pad = (a.n_wg + 7) & ~7;
+  if ((int)blockIdx.x >= nwg_pad) {  // wave-uniform: the whole workgroup replays
+    replay_worker(a, (int)blockIdx.x - nwg_pad);
+    return;
+  }
   const int w = (int)(blockIdx.x & 7) * (nwg_pad >> 3) + (int)(blockIdx.x >> 3);
   if (w >= a.n_wg) return;
   const int hb = w % a.hb;
@@ -851,14 +877,15 @@ __global__ __launch_bounds__(256) void attn_combine_mla_kernel(CombineMlaArgs a)
 template <int DQK, int DV, int VOFF, int HW, int TW, int NST>
 void launch_partial(const AttnArgs& args, hipStream_t stream) {
   const int nwg_pad = (args.n_wg + 7) & ~7;
-  hipLaunchKernelGGL((attn_partial_kernel<DQK, DV, VOFF, HW, TW, NST>), dim3(nwg_pad),
+  hipLaunchKernelGGL((attn_partial_kernel<DQK, DV, VOFF, HW, TW, NST>), dim3(nwg_pad + args.pf_wg),
                      dim3(64 * HW * TW), 0, stream, args);
 }
 
 template <int NW, int NST>
 void launch_mla(const AttnArgs& args, hipStream_t stream) {
   const int nwg_pad = (args.n_wg + 7) & ~7;
-  hipLaunchKernelGGL((attn_mla_kernel<NW, NST>), dim3(nwg_pad), dim3(64 * NW), 0, stream, args);
+  hipLaunchKernelGGL((attn_mla_kernel<NW, NST>), dim3(nwg_pad + args.pf_wg), dim3(64 * NW), 0,
+                     stream, args);
 }
 
 bool is_mla(const hisparse_attn_desc_t& d) {
@@ -930,8 +957,27 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
                             const uint8_t* pool, int64_t records_per_unit, int32_t record_bytes,
                             int32_t units, int32_t top_k, const uint16_t* q, const int32_t* idx,
                             float* out, void* workspace, hipStream_t stream,
-                            int32_t idx_units) {
+                            int32_t idx_units, const FetchArgs* prefetch,
+                            int32_t prefetch_threads, int32_t prefetch_block_bytes) {
   AttnArgs a{};
+  if (prefetch && prefetch->units > 0 && prefetch->n_layers > 0) {
+    // about prefetch_threads threads spread over the replay's (unit, layer) pairs, in
+    // workgroups of the attention kernel's size, on the CUs the attention leaves idle
+    // (a workgroup of these kernels holds a CU's LDS, so replay and attention never share a
+    // CU's memory pipeline)
+    const int bd = 64 * p.hw * (is_mla(attn) ? 1 : p.tw);
+    const int64_t pairs = (int64_t)prefetch->units * prefetch->n_layers;
+    const int64_t n_attn = (int64_t)units * p.n_wg_splits * p.hb;
+    const int64_t idle = std::max<int64_t>(0, kTargetWorkgroups - ((n_attn + 7) & ~7LL));
+    int64_t per_pair = std::max<int64_t>(1, prefetch_threads / (bd * pairs));
+    per_pair = std::max<int64_t>(1, std::min(per_pair, idle / pairs));
+    if (pairs * per_pair > (1 << 20)) return hipErrorInvalidValue;
+    a.pf = *prefetch;
+    a.pf_div = make_fastdiv((uint32_t)(prefetch->R / 16));
+    a.pf_per_pair = (int32_t)per_pair;
+    a.pf_wg = (int32_t)(pairs * per_pair);
+    a.pf_u = std::max(1, prefetch_block_bytes / 16);
+  }
   a.idx_units = idx_units > 0 ? idx_units : units;
   a.pool = pool;
   a.q = q;

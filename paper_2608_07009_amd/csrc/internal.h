@@ -78,7 +78,8 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
                             const uint8_t* pool, int64_t records_per_unit, int32_t record_bytes,
                             int32_t units, int32_t top_k, const uint16_t* q, const int32_t* idx,
                             float* out, void* workspace, hipStream_t stream,
-                            int32_t idx_units = 0);
+                            int32_t idx_units = 0, const FetchArgs* prefetch = nullptr,
+                            int32_t prefetch_threads = 0, int32_t prefetch_block_bytes = 16);
 
 }  // namespace hisparse
 

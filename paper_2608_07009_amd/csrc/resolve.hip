@@ -27,7 +27,7 @@
 //   attention or resolve work of other streams running on the same CUs is barely delayed. One launch can serve
 //   several layers of a share group (grid z): the anchor's demand fetch and the replays of
 //   the same plan into its shared layers.
-#include "internal.h"
+#include "fetch_device.h"
 
 namespace hisparse {
 namespace {
@@ -318,57 +318,12 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   }
 }
 
-// Unsigned division by a runtime constant d >= 1 for n < 2^31 (round-up multiplier method:
-// magic = floor(2^32 (2^l - d) / d) + 1, l = ceil(log2 d); n / d = (umulhi(n, magic) + n) >> l).
-struct FastDiv {
-  uint32_t magic, shift;
-};
-
-inline FastDiv make_fastdiv(uint32_t d) {
-  uint32_t l = 0;
-  while ((1ull << l) < d) ++l;
-  uint64_t magic = ((1ull << 32) * ((1ull << l) - d)) / d + 1;
-  return FastDiv{(uint32_t)magic, l};
-}
-
-__device__ inline uint32_t fastdiv(uint32_t n, FastDiv f) {
-  return (__umulhi(n, f.magic) + n) >> f.shift;
-}
-
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
 template <int U>
 __global__ __launch_bounds__(kFetchThreads) void fetch_kernel(FetchArgs a, FastDiv div_cpr) {
-  const int unit = blockIdx.y;
-  const int m = a.plan_count[unit];
-  const uint32_t cpr = (uint32_t)a.R >> 4;  // 16-byte chunks per record
-  const uint32_t total = (uint32_t)m * cpr;
-  const int2* plan = a.plan + (int64_t)unit * a.k;
   // grid z: the target layers (one plan, each layer's own host records and cache)
-  const uint8_t* host = a.host[blockIdx.z] + (int64_t)unit * a.L * a.R;
-  uint8_t* cache = a.cache + (int64_t)blockIdx.z * a.cache_stride + (int64_t)unit * a.B * a.R;
-  const uint32_t stride = gridDim.x * (uint32_t)kFetchThreads;
-  for (uint32_t c0 = blockIdx.x * (uint32_t)kFetchThreads + threadIdx.x; c0 < total;
-       c0 += stride * U) {
-    u32x4 v[U];
-    int64_t dst[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const uint32_t c = c0 + u * stride;
-      dst[u] = -1;
-      if (c < total) {
-        const uint32_t r = fastdiv(c, div_cpr);
-        const uint32_t w = c - r * cpr;
-        const int2 pe = plan[r];
-        v[u] = __builtin_nontemporal_load(
-            reinterpret_cast<const u32x4*>(host + (int64_t)pe.x * a.R + (w << 4)));
-        dst[u] = (int64_t)pe.y * a.R + (w << 4);
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-      if (dst[u] >= 0) *reinterpret_cast<u32x4*>(cache + dst[u]) = v[u];
-  }
+  fetch_slice<U>(a, div_cpr, blockIdx.y, blockIdx.z,
+                 blockIdx.x * (uint32_t)kFetchThreads + threadIdx.x,
+                 gridDim.x * (uint32_t)kFetchThreads);
 }
 
 __global__ void reset_state_kernel(StateArgs a) {

@@ -37,7 +37,9 @@ EXPORTED = (
     "hisparse_cache_create", "hisparse_cache_destroy", "hisparse_host_pool",
     "hisparse_layer_cache", "hisparse_reset", "hisparse_resolve", "hisparse_resolve_tables",
     "hisparse_fetch", "hisparse_fetch_units", "hisparse_fetch_group", "hisparse_prefetch_layer",
+    "hisparse_prefetch_layers",
     "hisparse_decode_workspace_bytes", "hisparse_sparse_decode", "hisparse_sparse_decode_layers",
+    "hisparse_sparse_decode_prefetch",
     "hisparse_sparse_decode_pool",
     "hisparse_read_state", "hisparse_read_plan", "hisparse_check_errors",
 )
@@ -95,6 +97,7 @@ def lib() -> ctypes.CDLL:
             "hisparse_fetch_units": (_I32, [_V, _I32, _I32, _I32, _V]),
             "hisparse_fetch_group": (_I32, [_V, _I32, _I32, _V]),
             "hisparse_prefetch_layer": (_I32, [_V, _I32, _I32, _V]),
+            "hisparse_prefetch_layers": (_I32, [_V, _I32, _I32, _I32, _V]),
             "hisparse_decode_workspace_bytes": (ctypes.c_size_t, [_I32, _I32, _I32,
                                                                   ctypes.POINTER(AttnDesc)]),
             "hisparse_sparse_decode": (_I32, [_V, _I32, _V, _V, _V, ctypes.POINTER(AttnDesc), _V,
@@ -102,6 +105,9 @@ def lib() -> ctypes.CDLL:
             "hisparse_sparse_decode_layers": (_I32, [_V, _I32, _I32, _V, _V, _V,
                                                      ctypes.POINTER(AttnDesc), _V,
                                                      ctypes.c_size_t, _V]),
+            "hisparse_sparse_decode_prefetch": (_I32, [_V, _I32, _V, _V, _V,
+                                                       ctypes.POINTER(AttnDesc), _V,
+                                                       ctypes.c_size_t, _I32, _I32, _I32, _V]),
             "hisparse_sparse_decode_pool": (_I32, [_V, ctypes.c_int64, _I32, _I32, _I32, _V, _V,
                                                    _V, ctypes.POINTER(AttnDesc), _V,
                                                    ctypes.c_size_t, _V]),
@@ -215,6 +221,13 @@ def hisparse_prefetch_layer(cache: int, anchor_layer: int, shared_layer: int,
            lib().hisparse_prefetch_layer(cache, anchor_layer, shared_layer, _s(stream)))
 
 
+def hisparse_prefetch_layers(cache: int, anchor_layer: int, first_shared: int, num_layers: int,
+                             stream=None) -> None:
+    _check("hisparse_prefetch_layers",
+           lib().hisparse_prefetch_layers(cache, anchor_layer, first_shared, num_layers,
+                                          _s(stream)))
+
+
 def hisparse_decode_workspace_bytes(units: int, top_k: int, record_bytes: int,
                                     attn: AttnDesc) -> int:
     return lib().hisparse_decode_workspace_bytes(units, top_k, record_bytes, ctypes.byref(attn))
@@ -235,6 +248,16 @@ def hisparse_sparse_decode_layers(cache: int, first_layer: int, num_layers: int,
            lib().hisparse_sparse_decode_layers(cache, first_layer, num_layers, _p(q), _p(slots),
                                                _p(out), ctypes.byref(attn), _p(workspace),
                                                workspace_bytes, _s(stream)))
+
+
+def hisparse_sparse_decode_prefetch(cache: int, layer: int, q, slots, out, attn: AttnDesc,
+                                    workspace, workspace_bytes: int, anchor_layer: int,
+                                    first_shared: int, num_shared: int, stream=None) -> None:
+    _check("hisparse_sparse_decode_prefetch",
+           lib().hisparse_sparse_decode_prefetch(cache, layer, _p(q), _p(slots), _p(out),
+                                                 ctypes.byref(attn), _p(workspace),
+                                                 workspace_bytes, anchor_layer, first_shared,
+                                                 num_shared, _s(stream)))
 
 
 def hisparse_sparse_decode_pool(d_pool, records_per_unit: int, record_bytes: int, units: int,

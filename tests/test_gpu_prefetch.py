@@ -177,29 +177,111 @@ def test_decode_layers_batch_matches_resident():
 
 
 def test_fetch_group_equals_fetch_and_replays():
-    """One launch for the anchor's fetch and its shared layers' replays leaves every layer's
-    cache byte-identical to hisparse_fetch followed by one hisparse_prefetch_layer per shared
-    layer; bad group sizes are argument errors."""
+    """One launch for the anchor's fetch and its shared layers' replays, and the multi-layer
+    replay launch on a side stream, leave every layer's cache byte-identical to hisparse_fetch
+    followed by one hisparse_prefetch_layer per shared layer; bad layer ranges are argument
+    errors."""
     G = 4
     w = W.workload(2, num_layers=G, share_group=G, num_requests=2)
     steps = 4
     log(f"test_fetch_group_equals_fetch_and_replays {w.name}")
     grouped = Run(w, steps)
     single = Run(w, steps)
+    multi = Run(w, steps)
+    side = torch.cuda.Stream()
     try:
         for t in range(steps):
             hs.hisparse_resolve_tables(grouped.cache.handle, 0, grouped.sel_ptr(t, 0),
                                        grouped.slots[0], grouped.counts[0], grouped.stream)
             hs.hisparse_fetch_group(grouped.cache.handle, 0, G, grouped.stream)
             single.resolve_step(t, prefetch=True)
+            # the replays on a side stream, started right after the resolve, as two launches
+            hs.hisparse_resolve_tables(multi.cache.handle, 0, multi.sel_ptr(t, 0),
+                                       multi.slots[0], multi.counts[0], multi.stream)
+            resolved = torch.cuda.Event()
+            resolved.record(multi.stream)
+            side.wait_event(resolved)
+            hs.hisparse_prefetch_layers(multi.cache.handle, 0, 1, 2, side)
+            hs.hisparse_prefetch_layers(multi.cache.handle, 0, 3, 1, side)
+            hs.hisparse_fetch(multi.cache.handle, 0, multi.stream)
+            replayed = torch.cuda.Event()
+            replayed.record(side)
+            multi.stream.wait_event(replayed)  # before the anchor's next resolve
+        torch.cuda.synchronize()
         assert torch.equal(grouped.slots[0], single.slots[0])
+        assert torch.equal(multi.slots[0], single.slots[0])
         for l in range(G):
-            assert (layer_cache_host(grouped, l) == layer_cache_host(single, l)).all(), f"layer {l}"
+            ref = layer_cache_host(single, l)
+            assert (layer_cache_host(grouped, l) == ref).all(), f"group fetch, layer {l}"
+            assert (layer_cache_host(multi, l) == ref).all(), f"multi-layer replay, layer {l}"
         for n in (0, G + 1):
             with pytest.raises(hs.HisparseError):
                 hs.hisparse_fetch_group(grouped.cache.handle, 0, n, grouped.stream)
         with pytest.raises(hs.HisparseError):   # not an anchor layer
             hs.hisparse_fetch_group(grouped.cache.handle, 1, 2, grouped.stream)
+        for first, n in ((0, 1), (1, 0), (1, G), (2, G - 1), (4, 1)):
+            with pytest.raises(hs.HisparseError):
+                hs.hisparse_prefetch_layers(multi.cache.handle, 0, first, n, multi.stream)
     finally:
+        torch.cuda.synchronize()
         grouped.close()
         single.close()
+        multi.close()
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_decode_prefetch_equals_separate(cfg):
+    """Attention of one layer carrying the replay into later shared layers in the same launch
+    gives bit-identical attention outputs and byte-identical caches to the replay and the
+    attention issued apart, for the latent (MLA) and the grouped-query kernels; replay ranges
+    that include the attended layer, or that hisparse_prefetch_layers would refuse, are
+    argument errors."""
+    G = 4
+    if cfg == 2:
+        w = W.workload(2, num_layers=G, share_group=G, num_requests=2)
+    else:
+        w = W.workload(3, num_layers=G, share_group=G, num_requests=2)
+    steps = 3
+    log(f"test_decode_prefetch_equals_separate {w.name}")
+    fused, apart = Run(w, steps), Run(w, steps)
+    dev = fused.dev
+    ad = attn_desc(w)
+    nb = hs.hisparse_decode_workspace_bytes(w.units, w.k, w.record_bytes, ad)
+    ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+    out_f = torch.empty((G, w.units, w.q_heads, w.d_v), dtype=torch.float32, device=dev)
+    out_a = torch.empty_like(out_f)
+    try:
+        for t in range(steps):
+            q = [torch.from_numpy(W.queries(w, t, l).view(np.int16)).to(dev) for l in range(G)]
+            for r in (fused, apart):
+                hs.hisparse_resolve(r.cache.handle, 0, r.sel_ptr(t, 0), r.slots[0], r.counts[0],
+                                    r.stream)
+            h = fused.cache.handle
+            hs.hisparse_sparse_decode_prefetch(h, 0, q[0], fused.slots[0], out_f[0], ad, ws, nb,
+                                               0, 1, 1, fused.stream)
+            hs.hisparse_sparse_decode_prefetch(h, 1, q[1], fused.slots[0], out_f[1], ad, ws, nb,
+                                               0, 2, 2, fused.stream)
+            for l in (2, 3):
+                hs.hisparse_sparse_decode(h, l, q[l], fused.slots[0], out_f[l], ad, ws, nb,
+                                          fused.stream)
+            hs.hisparse_prefetch_layers(apart.cache.handle, 0, 1, G - 1, apart.stream)
+            for l in range(G):
+                hs.hisparse_sparse_decode(apart.cache.handle, l, q[l], apart.slots[0], out_a[l],
+                                          ad, ws, nb, apart.stream)
+            torch.cuda.synchronize()
+            assert torch.equal(out_f, out_a), f"step {t}"
+            for l in range(G):
+                assert (layer_cache_host(fused, l) == layer_cache_host(apart, l)).all(), \
+                    f"step {t} layer {l}"
+        h = fused.cache.handle
+        for layer, first, n in ((1, 1, 1), (2, 1, 3), (0, 0, 1), (0, 1, 0), (0, 2, 3), (1, 2, 9)):
+            with pytest.raises(hs.HisparseError):
+                hs.hisparse_sparse_decode_prefetch(h, layer, q[0], fused.slots[0], out_f[0], ad,
+                                                   ws, nb, 0, first, n, fused.stream)
+        with pytest.raises(hs.HisparseError):  # the replay's anchor must be an anchor layer
+            hs.hisparse_sparse_decode_prefetch(h, 0, q[0], fused.slots[0], out_f[0], ad, ws, nb,
+                                               1, 2, 1, fused.stream)
+    finally:
+        torch.cuda.synchronize()
+        fused.close()
+        apart.close()
