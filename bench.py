@@ -59,9 +59,11 @@ def parse():
                     help="independent request groups, each with its own cache handle and "
                          "streams, whose steps run concurrently (0 = 2 when there are at least "
                          "2 requests, else 1)")
-    ap.add_argument("--turns", choices=["first", "all"], default="first",
-                    help="micro-batches take turns on the host link at the first layer only "
-                         "(then run free from that offset), or at every layer")
+    ap.add_argument("--turns", choices=["all", "first"], default="all",
+                    help="micro-batches take turns on the host link at every layer, or at the "
+                         "first only (then run free from that offset: 1-2%% faster when "
+                         "undisturbed, but a perturbation such as a profiler attached can push "
+                         "the chains into lockstep for good)")
     ap.add_argument("--fetch-workgroups", type=int, default=0,
                     help="workgroups of one fetch launch (0 = the library default)")
     ap.add_argument("--schedule", choices=["overlap", "serial", "side", "batched"],
@@ -409,10 +411,8 @@ def main() -> int:
         micro-batch i waits for that of micro-batch i-1 (and micro-batch 0's for the last
         micro-batch's transfer of group g-1), so while one micro-batch moves its misses the
         others resolve and attend instead of splitting the link and falling into lockstep.
-        With --turns first (the default) only the first group is ordered this way; from that
-        offset the chains run free, with no cross-stream wait per layer. Where a chain's
-        compute is short next to its transfer the two transfers end up sharing the link,
-        which leaves the link just as busy."""
+        With --turns first only the first group is ordered this way; from that offset the
+        chains run free, with no cross-stream wait per layer."""
         if n_mb > 1:
             rec(fork_ev, root_s)
             for mb in mbs[1:]:
