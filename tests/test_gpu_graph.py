@@ -11,7 +11,7 @@ import pytest
 import torch
 
 import workload as W
-from hs_harness import Run, attn_desc, log
+from hs_harness import Run, attn_desc, layer_cache_host, log
 from paper_2608_07009_amd import hisparse as hs
 
 pytestmark = pytest.mark.gpu
@@ -76,6 +76,82 @@ def test_graph_replay_matches_eager(cfg, layers, steps):
             del scratch
         st, _ = graph.cache.check_errors()
         assert st == hs.HISPARSE_OK
+    finally:
+        eager.close()
+        graph.close()
+
+
+def _shared_group_step(run, sel_ptr, q, out, ad, ws, ws_bytes, stream):
+    """One decode step of a share group of 4 layers through every shared-layer entry point:
+    resolve tables, fetch of the anchor by unit ranges, attention of layer 0 carrying the
+    replay into layer 1, a multi-layer replay into layer 2, the group fetch (idempotent here),
+    attention of layer 1, and layers 2-3 in one batched launch."""
+    h, U = run.cache.handle, run.w.units
+    hs.hisparse_resolve_tables(h, 0, sel_ptr, run.slots[0], run.counts[0], stream)
+    hs.hisparse_fetch_units(h, 0, 0, 1, stream)
+    hs.hisparse_fetch_units(h, 0, 1, U - 1, stream)
+    hs.hisparse_sparse_decode_prefetch(h, 0, q[0], run.slots[0], out[0], ad, ws, ws_bytes,
+                                       0, 1, 1, stream)
+    hs.hisparse_prefetch_layers(h, 0, 2, 1, stream)
+    hs.hisparse_fetch_group(h, 0, 4, stream)
+    hs.hisparse_sparse_decode(h, 1, q[1], run.slots[0], out[1], ad, ws, ws_bytes, stream)
+    hs.hisparse_sparse_decode_layers(h, 2, 2, q[2], run.slots[0], out[2], ad, ws, ws_bytes,
+                                     stream)
+
+
+def test_graph_replay_shared_layers():
+    """The shared-layer entry points (unit-range fetch, replay carried by attention,
+    multi-layer replay, group fetch, batched attention) replay from a captured graph with the
+    same slots, counts, attention outputs and cache contents as eager calls."""
+    w = W.workload(1, num_layers=4, share_group=4, num_requests=2)
+    steps = 8
+    log(f"test_graph_replay_shared_layers {w.name} steps={steps}")
+    eager, graph = Run(w, steps), Run(w, steps)
+    try:
+        dev = eager.dev
+        ad = attn_desc(w)
+        ws_bytes = hs.hisparse_decode_workspace_bytes(2 * w.units, w.k, w.record_bytes, ad)
+        q_all = torch.stack([torch.stack([torch.from_numpy(W.queries(w, t, l).view(np.int16))
+                                          for l in range(4)]) for t in range(steps)]).to(dev)
+        ws_e = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+        out_e = torch.empty((4, w.units, w.q_heads, w.d_v), dtype=torch.float32, device=dev)
+        ref = []
+        for t in range(steps):
+            _shared_group_step(eager, eager.sel_ptr(t, 0), q_all[t], out_e, ad, ws_e, ws_bytes,
+                               eager.stream)
+            torch.cuda.synchronize()
+            ref.append((eager.slots[0].clone(), eager.counts[0].clone(), out_e.clone(),
+                        [layer_cache_host(eager, l) for l in range(4)]))
+
+        ws_g = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+        out_g = torch.empty_like(out_e)
+        step = torch.zeros(1, dtype=torch.int64, device=dev)
+        sel_buf = torch.empty_like(graph.sel[0])
+        q_buf = torch.empty_like(q_all[0])
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(g, stream=s):
+                cs = torch.cuda.current_stream()
+                sel_buf.copy_(graph.sel.index_select(0, step).squeeze(0))
+                q_buf.copy_(q_all.index_select(0, step).squeeze(0))
+                step.add_(1)
+                _shared_group_step(graph, sel_buf[:w.units], q_buf, out_g, ad, ws_g, ws_bytes,
+                                   cs)
+        torch.cuda.synchronize()
+        for t in range(steps):
+            g.replay()
+            torch.cuda.synchronize()
+            scratch = torch.randn(1 << 16, device=dev).sum()  # eager work between replays
+            e_slots, e_counts, e_out, e_caches = ref[t]
+            assert torch.equal(graph.slots[0], e_slots), f"slots differ at replay {t}"
+            assert torch.equal(graph.counts[0], e_counts), f"counts differ at replay {t}"
+            assert torch.equal(out_g, e_out), f"attention differs at replay {t}"
+            for l in range(4):
+                assert (layer_cache_host(graph, l) == e_caches[l]).all(), f"replay {t} layer {l}"
+            del scratch
+        assert graph.cache.check_errors()[0] == hs.HISPARSE_OK
     finally:
         eager.close()
         graph.close()
