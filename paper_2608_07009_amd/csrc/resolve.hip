@@ -23,10 +23,10 @@
 //   loads through the mapped address) into its slot. The grid is small: a fixed budget of
 //   one-wave workgroups shared by the launch's units, each thread keeping one transfer block
 //   of loads in flight. A few hundred KB of reads in flight saturate the host link; spread
-//   thinly over the chip, the fetch keeps only a few slow host reads outstanding per CU, so
-//   attention or resolve work of other streams running on the same CUs is barely delayed. One launch can serve
-//   several layers of a share group (grid z): the anchor's demand fetch and the replays of
-//   the same plan into its shared layers.
+//   thinly over the chip, the fetch keeps only a few slow host reads outstanding per CU,
+//   which limits how much it delays other streams' work on the same CUs. One launch can
+//   serve several layers of a share group (grid z): the anchor's demand fetch and the
+//   replays of the same plan into its shared layers.
 #include "fetch_device.h"
 
 namespace hisparse {
