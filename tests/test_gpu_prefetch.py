@@ -229,21 +229,23 @@ def test_fetch_group_equals_fetch_and_replays():
         multi.close()
 
 
-@pytest.mark.parametrize("cfg", [2, 3])
-def test_decode_prefetch_equals_separate(cfg):
+@pytest.mark.parametrize("cfg,fetch", [(2, hs.HISPARSE_FETCH_ZERO_COPY),
+                                       (3, hs.HISPARSE_FETCH_ZERO_COPY),
+                                       (2, hs.HISPARSE_FETCH_SDMA)])
+def test_decode_prefetch_equals_separate(cfg, fetch):
     """Attention of one layer carrying the replay into later shared layers in the same launch
     gives bit-identical attention outputs and byte-identical caches to the replay and the
-    attention issued apart, for the latent (MLA) and the grouped-query kernels; replay ranges
-    that include the attended layer, or that hisparse_prefetch_layers would refuse, are
-    argument errors."""
+    attention issued apart, for the latent (MLA) and the grouped-query kernels, and with the
+    copy-engine path (where the replay is issued on its own first); replay ranges that include
+    the attended layer, or that hisparse_prefetch_layers would refuse, are argument errors."""
     G = 4
     if cfg == 2:
         w = W.workload(2, num_layers=G, share_group=G, num_requests=2)
     else:
         w = W.workload(3, num_layers=G, share_group=G, num_requests=2)
     steps = 3
-    log(f"test_decode_prefetch_equals_separate {w.name}")
-    fused, apart = Run(w, steps), Run(w, steps)
+    log(f"test_decode_prefetch_equals_separate {w.name} fetch={fetch}")
+    fused, apart = Run(w, steps, fetch=fetch), Run(w, steps, fetch=fetch)
     dev = fused.dev
     ad = attn_desc(w)
     nb = hs.hisparse_decode_workspace_bytes(w.units, w.k, w.record_bytes, ad)
