@@ -190,7 +190,9 @@ def cpu_baseline(w, cache, sel_host, budget_s: float) -> dict:
     while time.perf_counter() - t0 < budget_s and t < sel_host.shape[0]:
         q = W.queries(w, t, 0, 0, n_units)
         for u in range(n_units):
-            rc, slots, counts, pp, ps = orcs[u].resolve_unit(0, sel_host[t, u])
+            rc, slots, _, pp, ps = orcs[u].resolve_unit(0, sel_host[t, u])
+            if rc != 0:
+                raise RuntimeError(f"oracle resolve failed ({rc}) at step {t}, unit {u}")
             oracle.apply_plan(host[u], imgs[u], pp, ps)
             oracle.sparse_decode(q[u], imgs[u].view(np.uint16).reshape(w.B, -1), slots,
                                  d_qk=w.d_qk, d_v=w.d_v, v_off=w.v_offset,
@@ -309,7 +311,7 @@ def main() -> int:
             self.q_p = [[q_all[v, l, sl].data_ptr() for l in range(w.num_layers)]
                         for v in range(n_qv)]
             self.out_p = [out[l, sl].data_ptr() for l in range(w.num_layers)]
-            self.sync = [hip.event(timing=False) for _ in range(G + 1)]
+            self.sync = [hip.event(timing=False) for _ in range(2)]  # side-stream fork / join
             self.link = [hip.event(timing=False) for _ in groups]
 
     mbs = [MicroBatch(i) for i in range(n_mb)]

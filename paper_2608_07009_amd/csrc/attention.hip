@@ -4,20 +4,25 @@
 // For each unit and query head h:  out_h = sum_j softmax_j(scale * q_h . key_j) value_j,
 // over the tokens of the k selected records, in the order of the slot vector.
 //
-// Structure
-//   attn_partial_kernel  one workgroup per (unit, token split, head block). A wave owns 16
-//     query heads (the MFMA N dimension) and one 32-token chunk per iteration; the workgroup
-//     stages its chunk(s) into LDS once and shares them across its head waves.
+// Structure (every attention kernel: one workgroup per (unit, token split, head block); each
+// 32-token chunk is staged into LDS once with direct global->LDS loads and shared by the
+// workgroup's head waves)
+//   attn_partial_kernel  grouped-query records (d 128). A wave owns 16 query heads (the MFMA N
+//     dimension) and one 32-token chunk per iteration.
 //       S^T[token][head] = K[token][:] . Q^T[:][head]     v_mfma_f32_16x16x32_bf16, K from LDS
 //                                                        rows, Q resident in VGPRs
-//       online softmax in fp32 (exp2, running max/sum per head), P rounded to bf16
-//       O[head][dim]   += P[head][token] . V[token][dim]  v_mfma_f32_16x16x32_bf16, V^T from
-//                                                        LDS (transposed while staging)
+//       online softmax in fp32 (exp2, reference max per head), P rounded to bf16
+//       O[head][dim]   += P[head][token] . V[token][dim]  v_mfma_f32_16x16x32_bf16, V by LDS
+//                                                        transpose reads
 //     A lane's S^T accumulator holds tokens {4g..4g+3, 16+4g..16+4g+3} (g = lane/16) of its
 //     head, which is exactly one P operand when the PV contraction index runs over the tokens
-//     in that order, so P never leaves the lane; the V^T operand is read in the same order.
-//   attn_combine_kernel  merges the per-split (max, sum, unnormalised output) triples of each
-//     (unit, head) in ascending split order.
+//     in that order, so P never leaves the lane; the V operand is read in the same order.
+//   attn_mla_kernel  latent records (d_qk 576, d_v 512 = the key's first 512 dims): 32 heads
+//     per wave on v_mfma_f32_32x32x16_bf16, the output in accumulation registers.
+//   attn_combine_kernel / attn_combine_mla_kernel  merge the per-split (max, sum, unnormalised
+//     output) triples of each (unit, head) in ascending split order.
+//   Either attention kernel can carry an exact-prefetch replay: extra workgroups after the
+//   attention's copy records into other layers' caches and exit (replay_worker).
 // The reduction order depends only on token positions in the sequence, never on the slot
 // values, so any placement of the same records gives bit-identical outputs.
 #include <math.h>
