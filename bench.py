@@ -693,6 +693,12 @@ def main() -> int:
         if (miss_gbps and pinned_peak) else None,
         "pinned_h2d_peak_GBps": pinned_peak,
         "pinned_h2d_sweep_GBps": {str(s): v for s, v in sweep.items()},
+        # resolved selections per second of resolve + fetch kernel time (the resolve step alone,
+        # with its IO): anchor layer calls x units x k over the span-pass time of the resolve
+        # launches and the fetch launches (group launches include their replays)
+        "resolve_with_fetch_selections_per_s": (
+            anchor_calls * U_all * k / (t_tab + (t_fet + t_grp if moves_data else 0.0))
+            if t_tab else None),
         "hit_rate": hits_anchor / max(1, hits_anchor + misses_anchor),
         "misses_per_unit_step": misses_anchor / max(1, anchor_calls * U_all),
         "cold_step_ms": cold_ms,
