@@ -8,8 +8,8 @@ pinned host memory. Default workload: 32 requests x 8 layers, 32K-token context,
 B=4096 slots, 128 latent-attention heads.
 
 Prints one JSON line: value = selections served per second (layers x units x k per step)
-over the wall time of K decode steps replayed from one captured HIP graph (the deployment
-form; --no-graph: the eager GPU time), with miss-fetch GB/s against the in-process pinned
+over the wall time of K decode steps replayed from a captured HIP graph of several steps (the
+deployment form; --no-graph: the eager GPU time), with miss-fetch GB/s against the in-process pinned
 hipMemcpy H2D peak, decode tokens/s, per-kernel HIP-event timings, the roofline of the dominant
 kernel and the CPU oracle baseline.
 
@@ -52,6 +52,10 @@ def parse():
     ap.add_argument("--transfer-block", type=int, default=0)
     ap.add_argument("--splits", type=int, default=0, help="attention splits (0 = auto)")
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay")
+    ap.add_argument("--graph-steps", type=int, default=4,
+                    help="decode steps captured in one HIP graph (the largest even divisor of "
+                         "--steps and --warmup up to this; 1 = one step per graph, queries "
+                         "copied into place each step)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-sweep", action="store_true")
@@ -407,7 +411,7 @@ def main() -> int:
                      layers[i + 1], 1, ms)
             decode(layers[-1])
 
-    def step(t, ev=None, spans=None, sel_override=None, q_override=None):
+    def step(t, ev=None, spans=None, sel_override=None, q_override=None, fork=True, join=True):
         """Enqueue decode step t of every micro-batch: forked from the root stream, joined back
         into it. Micro-batches take turns on the host link: the transfer of group g of
         micro-batch i waits for that of micro-batch i-1 (and micro-batch 0's for the last
@@ -415,7 +419,7 @@ def main() -> int:
         others resolve and attend instead of splitting the link and falling into lockstep.
         With --turns first only the first group is ordered this way; from that offset the
         chains run free, with no cross-stream wait per layer."""
-        if n_mb > 1:
+        if n_mb > 1 and fork:
             rec(fork_ev, root_s)
             for mb in mbs[1:]:
                 wait(mb.main, fork_ev, 0)
@@ -427,7 +431,7 @@ def main() -> int:
                             (mbs[-1].link[gi - 1] if gi > 0 else None))
                     link = (prev, mb.link[gi])
                 group_step(mb, gi, t, ev, spans, sel_override, q_override, link)
-        if n_mb > 1:
+        if n_mb > 1 and join:
             for mb, je in zip(mbs[1:], join_evs[1:]):
                 rec(je, mb.main)
                 wait(root_s, je, 0)
@@ -626,36 +630,52 @@ def main() -> int:
     miss_gbps = ((fetch_bytes + replay_bytes + group_bytes + carried_bytes) / io_busy / 1e9
                  if (io_busy and moves_data) else None)
 
-    # the same steps replayed from one captured HIP graph (cold reset, same warmup)
+    # the same steps replayed from a captured HIP graph (cold reset, same warmup)
     graph = None
     if not args.no_graph and fetch != hs.HISPARSE_FETCH_SDMA:
-        stage_sel = torch.empty_like(sel[0])
-        stage_q = torch.empty_like(q_all[0])
+        # One graph covers S consecutive steps (S even, so every replay sees the same query
+        # parity per position): the steps' selections are staged from a device-side step
+        # counter at the start, the queries are read in place, and the micro-batches fork once
+        # and join once per replay, so one micro-batch's next step can start while another
+        # finishes its last layer.
+        S = max(1, args.graph_steps)  # the largest even divisor of steps and warmup up to it
+        while S > 1 and (args.steps % S or args.warmup % S or S % n_qv):
+            S -= 1
+        stage_sel = torch.empty((S,) + tuple(sel.shape[1:]), dtype=sel.dtype, device=dev)
+        stage_q = torch.empty_like(q_all[0]) if S == 1 else None
         tidx = torch.zeros(1, dtype=torch.int64, device=dev)
-        sel_stage_p = {mb.u0: [stage_sel[(a // G) * U_all + mb.u0:(a // G) * U_all + mb.u0 + mb.U]
-                               .data_ptr() for a in range(w.num_layers)] for mb in mbs}
-        q_stage_p = {mb.u0: [stage_q[l, mb.u0:mb.u0 + mb.U].data_ptr()
-                             for l in range(w.num_layers)] for mb in mbs}
+        offs = torch.arange(S, dtype=torch.int64, device=dev)
+        sel_stage_p = [{mb.u0: [stage_sel[j, (a // G) * U_all + mb.u0:(a // G) * U_all + mb.u0
+                                          + mb.U].data_ptr() for a in range(w.num_layers)]
+                        for mb in mbs} for j in range(S)]
+        if S == 1:
+            q_stage_p = [{mb.u0: [stage_q[l, mb.u0:mb.u0 + mb.U].data_ptr()
+                                  for l in range(w.num_layers)] for mb in mbs}]
+        else:
+            q_stage_p = [{mb.u0: mb.q_p[j % n_qv] for mb in mbs} for j in range(S)]
         g = torch.cuda.CUDAGraph()
         torch.cuda.synchronize()
         with torch.cuda.graph(g, stream=root_t):
-            stage_sel.copy_(sel.index_select(0, tidx).squeeze(0))
-            stage_q.copy_(q_all.index_select(0, torch.remainder(tidx, n_qv)).squeeze(0))
-            tidx.add_(1)
-            step(0, sel_override=sel_stage_p, q_override=q_stage_p)
+            torch.index_select(sel, 0, tidx + offs, out=stage_sel)
+            if S == 1:
+                stage_q.copy_(q_all.index_select(0, torch.remainder(tidx, n_qv)).squeeze(0))
+            tidx.add_(S)
+            for j in range(S):
+                step(j, sel_override=sel_stage_p[j], q_override=q_stage_p[j], fork=(j == 0),
+                     join=(j == S - 1))
         torch.cuda.synchronize()
         for mb in mbs:
             hs.hisparse_reset(mb.h, root_s)
         tidx.zero_()
-        for _ in range(args.warmup):
+        for _ in range(args.warmup // S):
             g.replay()
         torch.cuda.synchronize()
         tg = time.perf_counter()
-        for _ in range(args.steps):
+        for _ in range(args.steps // S):
             g.replay()
         torch.cuda.synchronize()
         gwall = time.perf_counter() - tg
-        graph = {"ms_per_step": gwall / K * 1e3}
+        graph = {"ms_per_step": gwall / K * 1e3, "steps_per_graph": S}
         for mb in mbs:
             st, info = mb.cache.check_errors()
             if st != hs.HISPARSE_OK:
@@ -686,7 +706,8 @@ def main() -> int:
                    "micro_batches": n_mb, "schedule": args.schedule,
                    "records_per_unit": w.L, "record_bytes": R, "top_k": k, "capacity": w.B,
                    "share_group": G, "q_heads": w.q_heads, "fetch": args.fetch,
-                   "host_memory": args.host_memory, "mode": mode},
+                   "host_memory": args.host_memory, "mode": mode,
+                   "steps_per_graph": graph["steps_per_graph"] if graph else None},
         "decode_tokens_per_s": w.num_requests * K / wall,
         "miss_fetch_GBps": miss_gbps,
         "miss_fetch_pct_of_pinned_h2d_peak": (100 * miss_gbps / pinned_peak)
