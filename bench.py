@@ -479,6 +479,8 @@ def main() -> int:
     rec(end, root_s)
     torch.cuda.synchronize()
     eager_gpu_ms = hip.ms(ref, end) / args.steps
+    # slot vectors and attention outputs of the last step, to check the graph replays against
+    eager_final = [(mb.slots.clone(), out[:, mb.u0:mb.u0 + mb.U].clone()) for mb in mbs]
     for mb in mbs:
         st, info = mb.cache.check_errors()
         if st != hs.HISPARSE_OK:
@@ -676,10 +678,16 @@ def main() -> int:
         torch.cuda.synchronize()
         gwall = time.perf_counter() - tg
         graph = {"ms_per_step": gwall / K * 1e3, "steps_per_graph": S}
-        for mb in mbs:
+        for mb, (slots_e, out_e) in zip(mbs, eager_final):
             st, info = mb.cache.check_errors()
             if st != hs.HISPARSE_OK:
                 print(json.dumps({"error": f"device-side selection error in graph replay {info}"}))
+                return 1
+            # the replays ran the same steps from a cold cache: identical last-step results
+            same_out = fetch == hs.HISPARSE_FETCH_NONE or torch.equal(
+                out[:, mb.u0:mb.u0 + mb.U], out_e)
+            if not (torch.equal(mb.slots, slots_e) and same_out):
+                print(json.dumps({"error": "graph replay differs from the eager run"}))
                 return 1
 
     if graph is not None:
