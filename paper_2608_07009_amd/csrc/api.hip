@@ -382,13 +382,15 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
     }
     if (n == 0) return HISPARSE_OK;
     if (batch_copy_fn fn = batch_copy()) {
-      size_t fail = 0;
-      if (fn(c->dma_dst.data(), c->dma_src.data(), c->dma_size.data(), n, nullptr, nullptr, 0,
-             &fail, stream) != hipSuccess) {
-        (void)hipGetLastError();
-        return HISPARSE_ERR_HIP;
-      }
-      return HISPARSE_OK;
+      // one copy-engine batch; a runtime that refuses the call (e.g. wants explicit copy
+      // attributes) gets the copies one by one below instead
+      hipMemcpyAttributes attr;
+      memset(&attr, 0, sizeof(attr));
+      size_t attr_idx = 0, fail = 0;
+      if (fn(c->dma_dst.data(), c->dma_src.data(), c->dma_size.data(), n, &attr, &attr_idx, 1,
+             &fail, stream) == hipSuccess)
+        return HISPARSE_OK;
+      (void)hipGetLastError();
     }
     for (size_t i = 0; i < n; ++i)
       if (hipMemcpyAsync(c->dma_dst[i], c->dma_src[i], c->dma_size[i], hipMemcpyHostToDevice,
