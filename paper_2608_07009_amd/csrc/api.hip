@@ -386,6 +386,10 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
       // attributes) gets the copies one by one below instead
       hipMemcpyAttributes attr;
       memset(&attr, 0, sizeof(attr));
+      attr.srcAccessOrder = hipMemcpySrcAccessOrderStream;  // sources read in stream order
+      attr.srcLocHint.type = hipMemLocationTypeHost;
+      attr.dstLocHint.type = hipMemLocationTypeDevice;
+      attr.dstLocHint.id = c->device;
       size_t attr_idx = 0, fail = 0;
       if (fn(c->dma_dst.data(), c->dma_src.data(), c->dma_size.data(), n, &attr, &attr_idx, 1,
              &fail, stream) == hipSuccess)
