@@ -108,6 +108,24 @@ class OracleCache:
         return rc, slots, counts, plan_pos[:m].copy(), plan_slot[:m].copy()
 
 
+    def admit_unit(self, u: int, pos: int):
+        """Write-through admission of a newly generated record at position `pos` (Section 3.3
+        (4)), read as a one-entry resolve event of the unit: the clock advances, a resident
+        position is refreshed, otherwise the least-recent slot by (timestamp, slot) takes it
+        with the event's miss stamp. Returns (rc, slot, was_hit)."""
+        sel = np.array([pos], dtype=np.int32)
+        slots = np.empty(1, dtype=np.int32)
+        counts = np.zeros(2, dtype=np.int32)
+        plan_pos = np.full(1, -1, dtype=np.int32)
+        plan_slot = np.full(1, -1, dtype=np.int32)
+        rc = lib().oracle_resolve(self.L, self.B, 1, _ptr(self.pt[u]), _ptr(self.slot_pos[u]),
+                                  _ptr(self.slot_ts[u]), _ptr(self.clock[u:u + 1]), _ptr(sel),
+                                  _ptr(slots), _ptr(counts), _ptr(plan_pos), _ptr(plan_slot))
+        if rc not in (OK, BAD_SELECTION):
+            raise RuntimeError(f"oracle_resolve failed ({rc})")
+        return rc, int(slots[0]), bool(counts[0])
+
+
 def apply_plan(host_unit: np.ndarray, cache_unit: np.ndarray, plan_pos, plan_slot) -> None:
     """cache_unit[slot] <- host_unit[pos]; both uint8/uint16 arrays [records][...]."""
     plan_pos = np.ascontiguousarray(plan_pos, dtype=np.int32)

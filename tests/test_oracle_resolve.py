@@ -219,3 +219,55 @@ def test_apply_plan_copies_records():
         assert (cache[slots] == host[sel]).all()
         res = np.nonzero(c.slot_pos[0] >= 0)[0]
         assert (cache[res] == host[c.slot_pos[0][res]]).all()
+
+
+def test_admission_worked_example():
+    """Write-through admission (Section 3.3 (4)) as a one-entry resolve event, by hand: B = 3,
+    k = 2, cold start. Step 1 [9, 5]: misses 5 -> slot 0, 9 -> slot 1 (stamp 1). Admit 12
+    (event 2): the empty slot 2 (stamp 0) is least recent -> 12 -> 2, stamp 3. Step 3 [12, 7]:
+    12 hits slot 2 (stamp 6); 7 misses and takes the least recent non-hit slot, 0 (stamp 1, tie
+    with slot 1 broken by slot), evicting 5. Admit 13 (event 4): slot 1 (9, stamp 1) is least
+    recent -> 13 -> 1. Admit 7 (event 5): resident, refreshed in place."""
+    c = oracle.OracleCache(1, 16, 3, 2)
+    rc, slots, counts, _, _ = c.resolve_unit(0, np.array([9, 5]))
+    assert rc == oracle.OK and slots.tolist() == [1, 0]
+    assert c.admit_unit(0, 12) == (oracle.OK, 2, False)
+    assert c.slot_ts[0].tolist() == [1, 1, 3]
+    rc, slots, counts, _, _ = c.resolve_unit(0, np.array([12, 7]))
+    assert slots.tolist() == [2, 0] and counts.tolist() == [1, 1]
+    assert c.pt[0, 5] == -1
+    assert c.admit_unit(0, 13) == (oracle.OK, 1, False)
+    assert c.pt[0, 9] == -1 and c.slot_pos[0].tolist() == [7, 13, 12]
+    assert c.admit_unit(0, 7) == (oracle.OK, 0, True)
+    assert c.slot_ts[0].tolist() == [10, 7, 6] and int(c.clock[0]) == 5
+    assert c.admit_unit(0, 16)[0] == oracle.BAD_SELECTION  # outside [0, L): state unchanged
+    assert int(c.clock[0]) == 5
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_admission_matches_list_lru(seed):
+    """Resolve steps interleaved with admissions agree with the independent list model, where an
+    admission is an access of the one-position set {p}; an admitted position is resident and,
+    holding the newest stamp, survives until B other slots have been touched after it."""
+    rng = np.random.default_rng(300 + seed)
+    for trial in range(40):
+        L = int(rng.integers(8, 64))
+        B = int(rng.integers(2, 17))
+        k = int(rng.integers(1, min(B, L) + 1))
+        model = ListLRU(B)
+        c = oracle.OracleCache(1, L, B, k)
+        for t in range(int(rng.integers(2, 30))):
+            if rng.random() < 0.4:
+                p = int(rng.integers(0, L))
+                rc, slot, was_hit = c.admit_unit(0, p)
+                e_slots, e_counts, _ = model.step(np.array([p]))
+                assert rc == oracle.OK and slot == e_slots[0]
+                assert was_hit == (e_counts[0] == 1)
+                assert c.pt[0, p] == slot and c.slot_pos[0, slot] == p
+                assert c.slot_ts[0, slot] == c.slot_ts[0].max()
+            else:
+                sel = rng.choice(L, size=k, replace=False).astype(np.int32)
+                rc, slots, counts, pp, ps = c.resolve_unit(0, sel)
+                e_slots, e_counts, e_plan = model.step(sel)
+                assert rc == oracle.OK and slots.tolist() == e_slots
+                assert list(zip(pp.tolist(), ps.tolist())) == e_plan
