@@ -56,6 +56,8 @@ void free_all(hisparse_cache* c) {
     (void)hipFree(a.plan);
     (void)hipFree(a.plan_count);
     (void)hipFree(a.counts);
+    (void)hipFree(a.append_plan);
+    (void)hipFree(a.append_count);
   }
   if (c->err) (void)hipFree(c->err);
   if (c->h_plan_count) (void)hipHostFree(c->h_plan_count);
@@ -218,6 +220,8 @@ hisparse_status_t hisparse_cache_create(const hisparse_cache_desc_t* desc, int32
     if ((st = dmalloc(&an.plan, U * K * sizeof(int2))) != HISPARSE_OK) break;
     if ((st = dmalloc(&an.plan_count, U * 4)) != HISPARSE_OK) break;
     if ((st = dmalloc(&an.counts, U * 2 * 4)) != HISPARSE_OK) break;
+    if ((st = dmalloc(&an.append_plan, U * sizeof(int2))) != HISPARSE_OK) break;
+    if ((st = dmalloc(&an.append_count, U * 4)) != HISPARSE_OK) break;
   }
   if (st == HISPARSE_OK) st = dmalloc(&c->err, hisparse::kErrWords * 4);
   if (st == HISPARSE_OK && desc->fetch == HISPARSE_FETCH_SDMA) {
@@ -279,6 +283,56 @@ hisparse_status_t hisparse_reset(hisparse_cache_t c, void* stream) {
   for (auto& a : c->anchors)
     if (hisparse::launch_reset_state(state_args(c, a), as_stream(stream)) != hipSuccess)
       return HISPARSE_ERR_HIP;
+  return HISPARSE_OK;
+}
+
+hisparse_status_t hisparse_append(hisparse_cache_t c, int32_t anchor_layer, int32_t num_layers,
+                                  const int32_t* d_pos, const void* d_records, int32_t* d_slots,
+                                  void* stream) {
+  if (!c || !d_pos || !d_records || !d_slots || !is_anchor(c, anchor_layer) || num_layers < 1 ||
+      num_layers > c->desc.share_group || num_layers > c->desc.num_layers - anchor_layer)
+    return HISPARSE_ERR_INVALID_ARG;
+  auto& an = c->anchors[anchor_layer / c->desc.share_group];
+  // the new position enters the anchor's cache as a one-entry resolve event: same kernel,
+  // same canonical LRU, its own plan buffer (the step's plan may still be replayed)
+  hisparse::ResolveArgs a{};
+  a.sel = d_pos;
+  a.pt = an.pt;
+  a.slot_pos = an.slot_pos;
+  a.slot_ts = an.slot_ts;
+  a.order = an.order;
+  a.clock = an.clock;
+  a.slots_out = d_slots;
+  a.counts_out = an.counts;
+  a.plan = an.append_plan;
+  a.plan_count = an.append_count;
+  a.err = c->err;
+  a.L = c->desc.num_records;
+  a.B = c->desc.capacity;
+  a.k = 1;
+  a.layer = anchor_layer;
+  a.units = c->units;
+  if (hisparse::launch_resolve(a, as_stream(stream)) != hipSuccess) return HISPARSE_ERR_HIP;
+  if (c->desc.fetch == HISPARSE_FETCH_NONE) return HISPARSE_OK;  // tables only, no record moved
+  const int64_t U = c->units, R = c->desc.record_bytes;
+  for (int32_t j0 = 0; j0 < num_layers; j0 += hisparse::kMaxFetchLayers) {
+    hisparse::AppendArgs w{};
+    w.pos = d_pos;
+    w.slots = d_slots;
+    w.records = reinterpret_cast<const uint8_t*>(d_records) + (int64_t)j0 * U * R;
+    w.cache = c->cache[anchor_layer + j0];
+    w.cache_stride = (int64_t)c->cache_layer_bytes;
+    w.n_layers = std::min(num_layers - j0, hisparse::kMaxFetchLayers);
+    for (int32_t j = 0; j < w.n_layers; ++j)
+      w.host[j] = reinterpret_cast<uint8_t*>(c->host_dev[anchor_layer + j0 + j]);
+    w.L = c->desc.num_records;
+    w.B = c->desc.capacity;
+    w.R = (int32_t)R;
+    w.units = c->units;
+    w.write_cache = 1;
+    w.write_host = 1;
+    if (hisparse::launch_append(w, as_stream(stream)) != hipSuccess) return HISPARSE_ERR_HIP;
+  }
   return HISPARSE_OK;
 }
 

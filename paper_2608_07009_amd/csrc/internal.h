@@ -45,6 +45,20 @@ struct FetchArgs {
   int32_t B, k, R, units, n_layers;
 };
 
+// Write-through of generated records: record (z, u) goes to the slot of unit u's appended
+// position in layer z's cache and to that position in layer z's host pool.
+struct AppendArgs {
+  const int32_t* pos;       // [units] appended position per unit (< 0: none)
+  const int32_t* slots;     // [units] its slot, from the anchor's one-entry resolve (< 0: none)
+  const uint8_t* records;   // [n_layers][units][R] the new records
+  uint8_t* cache;           // first target layer's GPU cache [units][B][R]
+  int64_t cache_stride;     // bytes from one target layer's cache to the next
+  uint8_t* host[kMaxFetchLayers];  // per target layer: device-visible host pool [units][L][R]
+  int64_t L;
+  int32_t B, R, units, n_layers;
+  int32_t write_cache, write_host;
+};
+
 struct StateArgs {
   int32_t* pt;
   int32_t* slot_pos;
@@ -60,6 +74,7 @@ hipError_t launch_resolve(const ResolveArgs& a, hipStream_t stream);
 hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgroups,
                         hipStream_t stream);
 hipError_t launch_reset_state(const StateArgs& a, hipStream_t stream);
+hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
 size_t resolve_lds_bytes(int32_t k, int32_t B);
 int resolve_threads(int32_t B);
 
@@ -103,6 +118,8 @@ struct hisparse_cache {
     int2* plan = nullptr;
     int32_t* plan_count = nullptr;
     int32_t* counts = nullptr;   // used when the caller passes no counts buffer
+    int2* append_plan = nullptr;      // [units] plan of the latest append (kept apart from
+    int32_t* append_count = nullptr;  // the resolve's plan, which replays still read)
   };
   std::vector<Anchor> anchors;   // per anchor layer (layer / share_group)
   int32_t* err = nullptr;        // device error word

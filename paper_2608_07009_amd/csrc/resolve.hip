@@ -326,6 +326,23 @@ __global__ __launch_bounds__(kFetchThreads) void fetch_kernel(FetchArgs a, FastD
                  gridDim.x * (uint32_t)kFetchThreads);
 }
 
+// Write-through (Section 3.3 (4)): one workgroup per (unit, target layer) copies the caller's
+// new record into the slot its position was given and through to the host pool.
+__global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
+  typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+  const int unit = blockIdx.x, z = blockIdx.y;
+  const int32_t s = a.slots[unit], p = a.pos[unit];
+  if (s < 0 || p < 0) return;
+  const uint8_t* src = a.records + ((int64_t)z * a.units + unit) * a.R;
+  uint8_t* cache = a.cache + (int64_t)z * a.cache_stride + ((int64_t)unit * a.B + s) * a.R;
+  uint8_t* host = a.host[z] + ((int64_t)unit * a.L + p) * a.R;
+  for (int c = threadIdx.x; c < (a.R >> 4); c += blockDim.x) {
+    const v4u v = *reinterpret_cast<const v4u*>(src + 16 * c);
+    if (a.write_cache) *reinterpret_cast<v4u*>(cache + 16 * c) = v;
+    if (a.write_host) *reinterpret_cast<v4u*>(host + 16 * c) = v;
+  }
+}
+
 __global__ void reset_state_kernel(StateArgs a) {
   const int64_t n_pt = (int64_t)a.units * a.L;
   const int64_t n_slots = (int64_t)a.units * a.B;
@@ -394,6 +411,11 @@ hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgr
     case 8: hipLaunchKernelGGL(fetch_kernel<8>, grid, dim3(kFetchThreads), 0, stream, a, f); break;
     default: hipLaunchKernelGGL(fetch_kernel<16>, grid, dim3(kFetchThreads), 0, stream, a, f); break;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_append(const AppendArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(append_kernel, dim3(a.units, a.n_layers), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

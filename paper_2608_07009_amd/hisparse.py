@@ -37,7 +37,7 @@ EXPORTED = (
     "hisparse_cache_create", "hisparse_cache_destroy", "hisparse_host_pool",
     "hisparse_layer_cache", "hisparse_reset", "hisparse_resolve", "hisparse_resolve_tables",
     "hisparse_fetch", "hisparse_fetch_units", "hisparse_fetch_group", "hisparse_prefetch_layer",
-    "hisparse_prefetch_layers",
+    "hisparse_prefetch_layers", "hisparse_append",
     "hisparse_decode_workspace_bytes", "hisparse_sparse_decode", "hisparse_sparse_decode_layers",
     "hisparse_sparse_decode_prefetch",
     "hisparse_sparse_decode_pool",
@@ -98,6 +98,7 @@ def lib() -> ctypes.CDLL:
             "hisparse_fetch_group": (_I32, [_V, _I32, _I32, _V]),
             "hisparse_prefetch_layer": (_I32, [_V, _I32, _I32, _V]),
             "hisparse_prefetch_layers": (_I32, [_V, _I32, _I32, _I32, _V]),
+            "hisparse_append": (_I32, [_V, _I32, _I32, _V, _V, _V, _V]),
             "hisparse_decode_workspace_bytes": (ctypes.c_size_t, [_I32, _I32, _I32,
                                                                   ctypes.POINTER(AttnDesc)]),
             "hisparse_sparse_decode": (_I32, [_V, _I32, _V, _V, _V, ctypes.POINTER(AttnDesc), _V,
@@ -219,6 +220,13 @@ def hisparse_prefetch_layer(cache: int, anchor_layer: int, shared_layer: int,
                             stream=None) -> None:
     _check("hisparse_prefetch_layer",
            lib().hisparse_prefetch_layer(cache, anchor_layer, shared_layer, _s(stream)))
+
+
+def hisparse_append(cache: int, anchor_layer: int, num_layers: int, pos, records, slots,
+                    stream=None) -> None:
+    _check("hisparse_append",
+           lib().hisparse_append(cache, anchor_layer, num_layers, _p(pos), _p(records), _p(slots),
+                                 _s(stream)))
 
 
 def hisparse_prefetch_layers(cache: int, anchor_layer: int, first_shared: int, num_layers: int,

@@ -155,3 +155,80 @@ def test_graph_replay_shared_layers():
     finally:
         eager.close()
         graph.close()
+
+
+def test_graph_replay_append():
+    """Resolve + fetch + write-through append captured in a graph: the appended position and
+    record come from device buffers staged by the captured step itself; every replay matches
+    the eager run (slots, admission slots, caches, and the host pools' appended records)."""
+    steps = 8
+    base = W.workload(1, num_layers=2, share_group=2, num_requests=2)
+    L0 = base.L
+    w = W.workload(1, num_layers=2, share_group=2, num_requests=2, L=L0 + steps)
+    U, R = w.units, w.record_bytes
+    log(f"test_graph_replay_append {w.name} steps={steps}")
+    eager, graph = Run(w, steps, fill=False), Run(w, steps, fill=False)
+    try:
+        dev = eager.dev
+        for r in (eager, graph):
+            for l in range(2):
+                r.cache.host_view(l)[:] = 0
+                ptr = r.cache.host_pool(l)[0]
+                for u in range(U):
+                    W.fill_kv(ptr + u * w.L * R, base, l, u, 1)
+        sel = torch.from_numpy(W.selection_streams(base, steps=steps)).to(dev)
+        new = torch.from_numpy(np.stack([np.stack([np.stack(
+            [W.kv_records(base, l, u, [L0 + t])[0] for u in range(U)]) for l in range(2)])
+            for t in range(steps)]).view(np.int16)).to(dev)
+        pos_e = torch.empty(U, dtype=torch.int32, device=dev)
+        adm_e = torch.empty(U, dtype=torch.int32, device=dev)
+        ref = []
+        for t in range(steps):
+            hs.hisparse_resolve(eager.cache.handle, 0, sel[t], eager.slots[0], eager.counts[0],
+                                eager.stream)
+            hs.hisparse_prefetch_layer(eager.cache.handle, 0, 1, eager.stream)
+            pos_e.fill_(L0 + t)
+            hs.hisparse_append(eager.cache.handle, 0, 2, pos_e, new[t], adm_e, eager.stream)
+            torch.cuda.synchronize()
+            ref.append((eager.slots[0].clone(), adm_e.clone(),
+                        [layer_cache_host(eager, l) for l in range(2)]))
+
+        step = torch.zeros(1, dtype=torch.int64, device=dev)
+        sel_buf = torch.empty_like(sel[0])
+        rec_buf = torch.empty_like(new[0])
+        pos_buf = torch.empty(U, dtype=torch.int32, device=dev)
+        adm_g = torch.empty(U, dtype=torch.int32, device=dev)
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(g, stream=s):
+                cs = torch.cuda.current_stream()
+                sel_buf.copy_(sel.index_select(0, step).squeeze(0))
+                rec_buf.copy_(new.index_select(0, step).squeeze(0))
+                pos_buf.copy_((step + L0).to(torch.int32).expand(U))
+                step.add_(1)
+                hs.hisparse_resolve(graph.cache.handle, 0, sel_buf, graph.slots[0],
+                                    graph.counts[0], cs)
+                hs.hisparse_prefetch_layer(graph.cache.handle, 0, 1, cs)
+                hs.hisparse_append(graph.cache.handle, 0, 2, pos_buf, rec_buf, adm_g, cs)
+        torch.cuda.synchronize()
+        for t in range(steps):
+            g.replay()
+            torch.cuda.synchronize()
+            scratch = torch.randn(1 << 16, device=dev).sum()  # eager work between replays
+            e_slots, e_adm, e_caches = ref[t]
+            assert torch.equal(graph.slots[0], e_slots), f"slots differ at replay {t}"
+            assert torch.equal(adm_g, e_adm), f"admission slots differ at replay {t}"
+            for l in range(2):
+                assert (layer_cache_host(graph, l) == e_caches[l]).all(), f"replay {t} layer {l}"
+            del scratch
+        for l in range(2):
+            a = eager.cache.host_view(l)[:, L0:]
+            b = graph.cache.host_view(l)[:, L0:]
+            assert (a == b).all() and (a != 0).any()
+        assert graph.cache.check_errors()[0] == hs.HISPARSE_OK
+    finally:
+        torch.cuda.synchronize()
+        eager.close()
+        graph.close()

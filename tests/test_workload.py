@@ -58,3 +58,16 @@ def test_queries_deterministic():
     b = W.queries(w, 3, 2)
     assert (a == b).all() and a.shape == (w.units, w.q_heads, w.d_qk)
     assert not (W.queries(w, 4, 2) == a).all()
+
+
+def test_grow_streams_shift_window_only():
+    w = W.workload(1)
+    sel = W.selection_streams(w, steps=40)
+    g = W.grow_streams(w, sel)
+    lo = w.L - w.window
+    for t in range(40):
+        s, gs = sel[t, 0], g[t, 0]
+        drawn = s < lo
+        assert (gs[drawn] == s[drawn]).all()
+        assert sorted(gs[~drawn].tolist()) == list(range(lo + t, w.L + t))
+        assert len(set(gs.tolist())) == w.k

@@ -180,6 +180,19 @@ def selection_streams(w: Workload, steps: int | None = None, nthreads: int | Non
     return out
 
 
+def grow_streams(w: Workload, sel: np.ndarray) -> np.ndarray:
+    """Selections of a context that grows by one record per step (the write-through decode
+    loop): positions [0, L) are the prefill, and the record generated at step t sits at L + t.
+    The window [L - W, L) of step t becomes [L - W + t, L + t), so every step selects the
+    records appended in the previous W steps; drawn entries (all below L - W) are unchanged.
+    sel: int32 [steps][streams][k] from selection_streams."""
+    out = np.array(sel, dtype=np.int32, copy=True)
+    if w.window > 0:
+        t = np.arange(out.shape[0], dtype=np.int32).reshape(-1, 1, 1)
+        out = np.where(out >= w.L - w.window, out + t, out).astype(np.int32)
+    return out
+
+
 def fill_kv(ptr: int, w: Workload, layer: int, unit0: int = 0, n_units: int | None = None,
             rec0: int = 0, n_rec: int | None = None, nthreads: int | None = None) -> None:
     """Write records [unit0, unit0+n_units) x [rec0, rec0+n_rec) of `layer` to raw memory `ptr`
