@@ -79,6 +79,11 @@ def parse():
                          "the end of the resolve on; 'batched' (not realisable in a model: "
                          "later layers' queries depend on earlier layers) decodes the group's "
                          "layers in one attention launch")
+    ap.add_argument("--append", action="store_true",
+                    help="decode loop with a growing context: after each share group's "
+                         "attention, write the step's generated record of every layer through "
+                         "to the cache and the host pool (hisparse_append); token-record "
+                         "workloads only")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run one device-to-device copy of BYTES (calibrates the HBM "
                          "byte counters of a profiler run) and exit")
@@ -176,7 +181,7 @@ def union_length(intervals) -> float:
     return total
 
 
-def cpu_baseline(w, cache, sel_host, budget_s: float) -> dict:
+def cpu_baseline(w, cache, sel_host, budget_s: float, L: int) -> dict:
     """The oracle, as it stands, on a bounded sample: resolve + gather + float64 attention of
     units of layer 0, steps from cold, until the time budget is used."""
     import numpy as np
@@ -185,7 +190,7 @@ def cpu_baseline(w, cache, sel_host, budget_s: float) -> dict:
     import workload as W
 
     n_units = min(4, w.units)
-    orcs = [oracle.OracleCache(1, w.L, w.B, w.k) for _ in range(n_units)]
+    orcs = [oracle.OracleCache(1, L, w.B, w.k) for _ in range(n_units)]
     imgs = [np.zeros((w.B, w.record_bytes), dtype=np.uint8) for _ in range(n_units)]
     host = cache.host_view(0)
     done = 0
@@ -269,6 +274,14 @@ def main() -> int:
     U_all, k, G = w.units, w.k, w.share_group
     t0 = time.time()
     sel_host = W.selection_streams(w, steps=steps_needed)
+    if args.append:
+        if w.tokens_per_record != 1:
+            print(json.dumps({"error": "--append needs token records (configs 1, 2, 5)"}))
+            return 2
+        # the context grows by one record per step: step t's window follows the records
+        # appended by the previous steps, the record generated at step t goes to L + t
+        sel_host = W.grow_streams(w, sel_host)
+    L_pool = w.L + (steps_needed if args.append else 0)
     sel = torch.from_numpy(sel_host).to(dev)
     n_qv = 2  # queries vary by (layer, step parity)
     q_all = torch.stack([torch.stack([torch.from_numpy(W.queries(w, v, l).view(np.int16))
@@ -289,12 +302,18 @@ def main() -> int:
             self.r0 = i * n
             self.U = n * w.units_per_request
             self.u0 = self.r0 * w.units_per_request
-            wm = dataclasses.replace(w, num_requests=n)
+            wm = dataclasses.replace(w, num_requests=n, L=L_pool)
             self.cache = HiSparseCache.for_workload(
                 wm, fetch=fetch, host_memory=hmem, transfer_block_bytes=args.transfer_block,
                 fetch_workgroups=args.fetch_workgroups)
+            R = w.record_bytes
             for l in range(w.num_layers):
-                W.fill_kv(self.cache.host_pool(l)[0], w, l, self.u0, self.U)
+                ptr = self.cache.host_pool(l)[0]
+                if L_pool == w.L:
+                    W.fill_kv(ptr, w, l, self.u0, self.U)
+                else:  # prefill [0, L) of each unit; [L, L_pool) arrives by write-through
+                    for u in range(self.U):
+                        W.fill_kv(ptr + u * L_pool * R, w, l, self.u0 + u, 1)
             self.h = self.cache.handle
             self.main_t = root_t if i == 0 else torch.cuda.Stream()
             self.side_t = torch.cuda.Stream()
@@ -316,6 +335,17 @@ def main() -> int:
                         for v in range(n_qv)]
             self.out_p = [out[l, sl].data_ptr() for l in range(w.num_layers)]
             self.sync = [hip.event(timing=False) for _ in range(2)]  # side-stream fork / join
+            if args.append:
+                # the records generated at every step: [steps][layers][units][R], and the
+                # appended position of every unit, L + t
+                gen = np.empty((w.num_layers, U, steps_needed, R // 2), dtype=np.uint16)
+                for l in range(w.num_layers):
+                    W.fill_kv(gen[l].ctypes.data, w, l, self.u0, U, w.L, steps_needed)
+                self.new = torch.from_numpy(
+                    np.ascontiguousarray(gen.transpose(2, 0, 1, 3)).view(np.int16)).to(dev)
+                self.pos = (torch.arange(steps_needed, dtype=torch.int32, device=dev)
+                            .add_(w.L).unsqueeze(1).repeat(1, U).contiguous())
+                self.adm = torch.empty((len(groups), U), dtype=torch.int32, device=dev)
             self.link = [hip.event(timing=False) for _ in groups]
 
     mbs = [MicroBatch(i) for i in range(n_mb)]
@@ -329,6 +359,7 @@ def main() -> int:
     f_tables, f_fetch = L.hisparse_resolve_tables, L.hisparse_fetch
     f_prefetch_layers, f_decode = L.hisparse_prefetch_layers, L.hisparse_sparse_decode
     f_decode_prefetch = L.hisparse_sparse_decode_prefetch
+    f_append = L.hisparse_append
     f_decode_layers, f_fetch_group = L.hisparse_sparse_decode_layers, L.hisparse_fetch_group
     rec = hip.L.hipEventRecord
     wait = hip.L.hipStreamWaitEvent
@@ -411,7 +442,8 @@ def main() -> int:
                      layers[i + 1], 1, ms)
             decode(layers[-1])
 
-    def step(t, ev=None, spans=None, sel_override=None, q_override=None, fork=True, join=True):
+    def step(t, ev=None, spans=None, sel_override=None, q_override=None, fork=True, join=True,
+             app_override=None):
         """Enqueue decode step t of every micro-batch: forked from the root stream, joined back
         into it. Micro-batches take turns on the host link: the transfer of group g of
         micro-batch i waits for that of micro-batch i-1 (and micro-batch 0's for the last
@@ -431,6 +463,15 @@ def main() -> int:
                             (mbs[-1].link[gi - 1] if gi > 0 else None))
                     link = (prev, mb.link[gi])
                 group_step(mb, gi, t, ev, spans, sel_override, q_override, link)
+        if args.append:
+            # write-through of the step's generated record of every layer, one launch per
+            # micro-batch after its last attention (an admission may evict a slot the step
+            # read; the next step's resolves come after it on the same stream)
+            for mb in mbs:
+                pos_p, rec_p = app_override[mb.u0] if app_override else (
+                    mb.pos[t].data_ptr(), mb.new[t].data_ptr())
+                call("append", mb.main, ev, spans, f_append, mb.h, 0, w.num_layers, pos_p,
+                     rec_p, mb.adm.data_ptr(), mb.main)
         if n_mb > 1 and join:
             for mb, je in zip(mbs[1:], join_evs[1:]):
                 rec(je, mb.main)
@@ -461,7 +502,7 @@ def main() -> int:
     # its kernel, not a host launch gap. Its GPU time per step is reported beside the timed
     # region's. With several micro-batches the spans of concurrent kernels overlap: each span
     # is that kernel's duration while sharing the GPU.
-    per_step_events = n_mb * sum(2 * (3 + 2 * len(sh)) for _, sh in groups)
+    per_step_events = n_mb * (2 + sum(2 * (3 + 2 * len(sh)) for _, sh in groups))
     events = [hip.event() for _ in range(per_step_events * args.steps)]
     ref, end = hip.event(), hip.event()
     spans = []
@@ -562,6 +603,14 @@ def main() -> int:
                                       "layers_per_launch": len(groups[0][1]),
                                       "bytes_per_launch": replay_bytes / n_rep,
                                       "GBps": replay_bytes / t_rep / 1e9}
+    t_app, n_app = kernel("append")
+    if n_app:
+        app_bytes = K * w.num_layers * U_all * R  # one record per layer and unit per step
+        kernels["append"] = {
+            "launches": n_app, "avg_us": t_app / n_app * 1e6,
+            "write_through_bytes_per_launch": app_bytes / n_app if moves_data else 0,
+            "note": "every anchor's one-entry admission + every layer's record into its "
+                    "cache and through to its host pool, one launch per micro-batch and step"}
     if n_pf and moves_data:
         kernels["sparse_decode_prefetch"] = {
             "launches": n_pf, "avg_us": t_pf / n_pf * 1e6,
@@ -655,16 +704,29 @@ def main() -> int:
                                   for l in range(w.num_layers)] for mb in mbs}]
         else:
             q_stage_p = [{mb.u0: mb.q_p[j % n_qv] for mb in mbs} for j in range(S)]
+        app_stage_p = [None] * S
+        if args.append:  # the steps' appended positions and records, staged like selections
+            for mb in mbs:
+                mb.pos_stage = torch.empty((S,) + tuple(mb.pos.shape[1:]), dtype=mb.pos.dtype,
+                                           device=dev)
+                mb.rec_stage = torch.empty((S,) + tuple(mb.new.shape[1:]), dtype=mb.new.dtype,
+                                           device=dev)
+            app_stage_p = [{mb.u0: (mb.pos_stage[j].data_ptr(), mb.rec_stage[j].data_ptr())
+                            for mb in mbs} for j in range(S)]
         g = torch.cuda.CUDAGraph()
         torch.cuda.synchronize()
         with torch.cuda.graph(g, stream=root_t):
             torch.index_select(sel, 0, tidx + offs, out=stage_sel)
+            if args.append:
+                for mb in mbs:
+                    torch.index_select(mb.pos, 0, tidx + offs, out=mb.pos_stage)
+                    torch.index_select(mb.new, 0, tidx + offs, out=mb.rec_stage)
             if S == 1:
                 stage_q.copy_(q_all.index_select(0, torch.remainder(tidx, n_qv)).squeeze(0))
             tidx.add_(S)
             for j in range(S):
                 step(j, sel_override=sel_stage_p[j], q_override=q_stage_p[j], fork=(j == 0),
-                     join=(j == S - 1))
+                     join=(j == S - 1), app_override=app_stage_p[j])
         torch.cuda.synchronize()
         for mb in mbs:
             hs.hisparse_reset(mb.h, root_s)
@@ -712,6 +774,7 @@ def main() -> int:
         "config": {"workload": w.name, "requests": w.num_requests, "layers": w.num_layers,
                    "layers_in_workload": w0.num_layers, "units_per_layer": U_all,
                    "micro_batches": n_mb, "schedule": args.schedule,
+                   "append": args.append,
                    "records_per_unit": w.L, "record_bytes": R, "top_k": k, "capacity": w.B,
                    "share_group": G, "q_heads": w.q_heads, "fetch": args.fetch,
                    "host_memory": args.host_memory, "mode": mode,
@@ -738,7 +801,8 @@ def main() -> int:
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle baseline")
-        result["cpu_baseline"] = cpu_baseline(w, cache, sel_host[:, :mbs[0].U], args.cpu_budget)
+        result["cpu_baseline"] = cpu_baseline(w, cache, sel_host[:, :mbs[0].U], args.cpu_budget,
+                                              L_pool)
     for mb in mbs:
         for e in mb.sync + mb.link:
             hip.L.hipEventDestroy(e)

@@ -224,23 +224,24 @@ hisparse_status_t hisparse_prefetch_layers(hisparse_cache_t cache, int32_t ancho
                                            void* stream);
 
 /* [async] Write-through of generated records (Section 3.3 (4)): each unit's newly generated
- * record enters the GPU cache of every layer of a share group and is written through to those
- * layers' host pools.
+ * record enters the GPU caches of layers [first_layer, first_layer + num_layers) and is written
+ * through to those layers' host pools, in one launch. The range covers whole share groups:
+ * first_layer is an anchor and the range ends at a group boundary or at the last layer.
  *   d_pos     int32 [units]: the new record's position per unit (< 0: nothing for that unit;
  *             >= num_records: HISPARSE_ERR_BAD_SELECTION latched, state unchanged).
- *   d_records bf16 records [num_layers][units][R] for layers anchor_layer ..
- *             anchor_layer + num_layers - 1 (1 <= num_layers <= share_group).
- *   d_slots   int32 [units], out: the slot the position now occupies (-1: none).
- * The position is admitted as a one-entry resolve event of the anchor: the unit's clock
+ *   d_records bf16 records [num_layers][units][R].
+ *   d_slots   int32 [groups in the range][units], out: the slot the position now occupies in
+ *             each group (-1: none).
+ * Each group's anchor admits the position as a one-entry resolve event: the unit's clock
  * advances by one; a resident position is refreshed in place, otherwise the least-recent slot
  * by (timestamp, slot) takes it with the event's miss stamp, exactly as the canonical LRU does
- * for a selection {pos}. The record is then stored into that slot of each layer's cache and
- * into position pos of each layer's host pool, by the GPU over the mapped pool, so any later
+ * for a selection {pos}. Each layer's record is then stored into that slot of the layer's cache
+ * and into position pos of the layer's host pool, by the GPU over the mapped pool, so any later
  * fetch of pos on a stream ordered after this call reads it. Order the call after every
- * attention that reads the anchor's slots of the current step (the admission may evict one of
- * them) and before the anchor's next resolve. The resolve's own miss plan is left intact.
+ * attention that reads the slots of the groups' current step (an admission may evict one of
+ * them) and before those anchors' next resolve; the resolves' miss plans are left intact.
  * HISPARSE_FETCH_NONE updates the tables only. */
-hisparse_status_t hisparse_append(hisparse_cache_t cache, int32_t anchor_layer,
+hisparse_status_t hisparse_append(hisparse_cache_t cache, int32_t first_layer,
                                   int32_t num_layers, const int32_t* d_pos,
                                   const void* d_records, int32_t* d_slots, void* stream);
 

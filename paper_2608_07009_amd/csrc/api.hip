@@ -56,10 +56,10 @@ void free_all(hisparse_cache* c) {
     (void)hipFree(a.plan);
     (void)hipFree(a.plan_count);
     (void)hipFree(a.counts);
-    (void)hipFree(a.append_plan);
-    (void)hipFree(a.append_count);
   }
   if (c->err) (void)hipFree(c->err);
+  if (c->d_states) (void)hipFree(c->d_states);
+  if (c->d_layers) (void)hipFree(c->d_layers);
   if (c->h_plan_count) (void)hipHostFree(c->h_plan_count);
   if (c->h_plan) (void)hipHostFree(c->h_plan);
   (void)hipSetDevice(prev);
@@ -220,10 +220,26 @@ hisparse_status_t hisparse_cache_create(const hisparse_cache_desc_t* desc, int32
     if ((st = dmalloc(&an.plan, U * K * sizeof(int2))) != HISPARSE_OK) break;
     if ((st = dmalloc(&an.plan_count, U * 4)) != HISPARSE_OK) break;
     if ((st = dmalloc(&an.counts, U * 2 * 4)) != HISPARSE_OK) break;
-    if ((st = dmalloc(&an.append_plan, U * sizeof(int2))) != HISPARSE_OK) break;
-    if ((st = dmalloc(&an.append_count, U * 4)) != HISPARSE_OK) break;
   }
   if (st == HISPARSE_OK) st = dmalloc(&c->err, hisparse::kErrWords * 4);
+  if (st == HISPARSE_OK) st = dmalloc(&c->d_states, sizeof(hisparse::AnchorState) * c->n_anchors);
+  if (st == HISPARSE_OK)
+    st = dmalloc(&c->d_layers, sizeof(hisparse::LayerIO) * (size_t)desc->num_layers);
+  if (st == HISPARSE_OK) {
+    std::vector<hisparse::AnchorState> hs_states(c->n_anchors);
+    for (int a = 0; a < c->n_anchors; ++a) {
+      const auto& an = c->anchors[a];
+      hs_states[a] = hisparse::AnchorState{an.pt, an.slot_pos, an.slot_ts, an.order, an.clock};
+    }
+    std::vector<hisparse::LayerIO> hs_layers(desc->num_layers);
+    for (int l = 0; l < desc->num_layers; ++l)
+      hs_layers[l] = hisparse::LayerIO{c->cache[l], reinterpret_cast<uint8_t*>(c->host_dev[l])};
+    if (hipMemcpy(c->d_states, hs_states.data(), sizeof(hisparse::AnchorState) * c->n_anchors,
+                  hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(c->d_layers, hs_layers.data(), sizeof(hisparse::LayerIO) * desc->num_layers,
+                  hipMemcpyHostToDevice) != hipSuccess)
+      st = HISPARSE_ERR_HIP;
+  }
   if (st == HISPARSE_OK && desc->fetch == HISPARSE_FETCH_SDMA) {
     if (hipHostMalloc(reinterpret_cast<void**>(&c->h_plan_count), U * 4, 0) != hipSuccess ||
         hipHostMalloc(reinterpret_cast<void**>(&c->h_plan), U * K * sizeof(int2), 0) !=
@@ -286,53 +302,31 @@ hisparse_status_t hisparse_reset(hisparse_cache_t c, void* stream) {
   return HISPARSE_OK;
 }
 
-hisparse_status_t hisparse_append(hisparse_cache_t c, int32_t anchor_layer, int32_t num_layers,
+hisparse_status_t hisparse_append(hisparse_cache_t c, int32_t first_layer, int32_t num_layers,
                                   const int32_t* d_pos, const void* d_records, int32_t* d_slots,
                                   void* stream) {
-  if (!c || !d_pos || !d_records || !d_slots || !is_anchor(c, anchor_layer) || num_layers < 1 ||
-      num_layers > c->desc.share_group || num_layers > c->desc.num_layers - anchor_layer)
+  if (!c || !d_pos || !d_records || !d_slots || !is_anchor(c, first_layer) || num_layers < 1 ||
+      num_layers > c->desc.num_layers - first_layer)
     return HISPARSE_ERR_INVALID_ARG;
-  auto& an = c->anchors[anchor_layer / c->desc.share_group];
-  // the new position enters the anchor's cache as a one-entry resolve event: same kernel,
-  // same canonical LRU, its own plan buffer (the step's plan may still be replayed)
-  hisparse::ResolveArgs a{};
-  a.sel = d_pos;
-  a.pt = an.pt;
-  a.slot_pos = an.slot_pos;
-  a.slot_ts = an.slot_ts;
-  a.order = an.order;
-  a.clock = an.clock;
+  const int32_t G = c->desc.share_group, end = first_layer + num_layers;
+  if (end % G != 0 && end != c->desc.num_layers) return HISPARSE_ERR_INVALID_ARG;  // whole groups
+  hisparse::AdmitArgs a{};
+  a.pos = d_pos;
+  a.states = c->d_states;
+  a.layers = c->d_layers;
+  a.records = reinterpret_cast<const uint8_t*>(d_records);
   a.slots_out = d_slots;
-  a.counts_out = an.counts;
-  a.plan = an.append_plan;
-  a.plan_count = an.append_count;
   a.err = c->err;
   a.L = c->desc.num_records;
   a.B = c->desc.capacity;
-  a.k = 1;
-  a.layer = anchor_layer;
+  a.R = c->desc.record_bytes;
   a.units = c->units;
-  if (hisparse::launch_resolve(a, as_stream(stream)) != hipSuccess) return HISPARSE_ERR_HIP;
-  if (c->desc.fetch == HISPARSE_FETCH_NONE) return HISPARSE_OK;  // tables only, no record moved
-  const int64_t U = c->units, R = c->desc.record_bytes;
-  for (int32_t j0 = 0; j0 < num_layers; j0 += hisparse::kMaxFetchLayers) {
-    hisparse::AppendArgs w{};
-    w.pos = d_pos;
-    w.slots = d_slots;
-    w.records = reinterpret_cast<const uint8_t*>(d_records) + (int64_t)j0 * U * R;
-    w.cache = c->cache[anchor_layer + j0];
-    w.cache_stride = (int64_t)c->cache_layer_bytes;
-    w.n_layers = std::min(num_layers - j0, hisparse::kMaxFetchLayers);
-    for (int32_t j = 0; j < w.n_layers; ++j)
-      w.host[j] = reinterpret_cast<uint8_t*>(c->host_dev[anchor_layer + j0 + j]);
-    w.L = c->desc.num_records;
-    w.B = c->desc.capacity;
-    w.R = (int32_t)R;
-    w.units = c->units;
-    w.write_cache = 1;
-    w.write_host = 1;
-    if (hisparse::launch_append(w, as_stream(stream)) != hipSuccess) return HISPARSE_ERR_HIP;
-  }
+  a.G = G;
+  a.first = first_layer;
+  a.n_layers = num_layers;
+  a.write = c->desc.fetch != HISPARSE_FETCH_NONE;  // NONE: tables only, no record moved
+  if (hisparse::launch_admit(a, (num_layers + G - 1) / G, as_stream(stream)) != hipSuccess)
+    return HISPARSE_ERR_HIP;
   return HISPARSE_OK;
 }
 

@@ -45,18 +45,33 @@ struct FetchArgs {
   int32_t B, k, R, units, n_layers;
 };
 
-// Write-through of generated records: record (z, u) goes to the slot of unit u's appended
-// position in layer z's cache and to that position in layer z's host pool.
-struct AppendArgs {
-  const int32_t* pos;       // [units] appended position per unit (< 0: none)
-  const int32_t* slots;     // [units] its slot, from the anchor's one-entry resolve (< 0: none)
-  const uint8_t* records;   // [n_layers][units][R] the new records
-  uint8_t* cache;           // first target layer's GPU cache [units][B][R]
-  int64_t cache_stride;     // bytes from one target layer's cache to the next
-  uint8_t* host[kMaxFetchLayers];  // per target layer: device-visible host pool [units][L][R]
+// Device tables the write-through kernel indexes: per anchor its resolve state, per layer its
+// GPU cache and the device-visible address of its host pool.
+struct AnchorState {
+  int32_t* pt;          // [units][L]
+  int32_t* slot_pos;    // [units][B]
+  uint32_t* slot_ts;    // [units][B]
+  int32_t* order;       // [units][B]
+  uint32_t* clock;      // [units]
+};
+struct LayerIO {
+  uint8_t* cache;       // [units][B][R]
+  uint8_t* host;        // [units][L][R]
+};
+
+// Write-through of generated records for layers [first, first + n_layers), whole share groups:
+// each group's anchor admits the unit's new position (the canonical LRU on the one-entry
+// selection {pos}) and the group's layers receive their records in that slot and at pos in
+// their host pools.
+struct AdmitArgs {
+  const int32_t* pos;          // [units] the new position (< 0: none this event)
+  const AnchorState* states;   // [anchors]
+  const LayerIO* layers;       // [num_layers]
+  const uint8_t* records;      // [n_layers][units][R]
+  int32_t* slots_out;          // [groups in range][units]
+  int32_t* err;                // [kErrWords]
   int64_t L;
-  int32_t B, R, units, n_layers;
-  int32_t write_cache, write_host;
+  int32_t B, R, units, G, first, n_layers, write;  // write = 0: tables only
 };
 
 struct StateArgs {
@@ -74,7 +89,7 @@ hipError_t launch_resolve(const ResolveArgs& a, hipStream_t stream);
 hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgroups,
                         hipStream_t stream);
 hipError_t launch_reset_state(const StateArgs& a, hipStream_t stream);
-hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
+hipError_t launch_admit(const AdmitArgs& a, int32_t n_groups, hipStream_t stream);
 size_t resolve_lds_bytes(int32_t k, int32_t B);
 int resolve_threads(int32_t B);
 
@@ -118,9 +133,9 @@ struct hisparse_cache {
     int2* plan = nullptr;
     int32_t* plan_count = nullptr;
     int32_t* counts = nullptr;   // used when the caller passes no counts buffer
-    int2* append_plan = nullptr;      // [units] plan of the latest append (kept apart from
-    int32_t* append_count = nullptr;  // the resolve's plan, which replays still read)
   };
+  hisparse::AnchorState* d_states = nullptr;  // device copies of every anchor's state pointers
+  hisparse::LayerIO* d_layers = nullptr;      // and of every layer's cache / host pool address
   std::vector<Anchor> anchors;   // per anchor layer (layer / share_group)
   int32_t* err = nullptr;        // device error word
   // HISPARSE_FETCH_SDMA: pinned readback of a plan and the host-side copy lists

@@ -326,20 +326,81 @@ __global__ __launch_bounds__(kFetchThreads) void fetch_kernel(FetchArgs a, FastD
                  gridDim.x * (uint32_t)kFetchThreads);
 }
 
-// Write-through (Section 3.3 (4)): one workgroup per (unit, target layer) copies the caller's
-// new record into the slot its position was given and through to the host pool.
-__global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
+// Write-through (Section 3.3 (4)). One workgroup per (unit, share group). The table side is
+// the canonical LRU applied to the one-position selection {pos}, specialised: the anchor's
+// clock advances; a resident position has its stamp refreshed to 2t and its slot moved to the
+// most-recent end of the recency index; a new position takes the least-recent slot order[0]
+// (no slot is hit, so none is exempt) with the miss stamp 2t-1, and the index rotates by one.
+// Then the unit's record of each of the group's layers is stored into that slot of the layer's
+// cache and at pos in the layer's host pool. The index is staged in LDS for the shift.
+__global__ __launch_bounds__(256) void admit_kernel(AdmitArgs a) {
+  extern __shared__ uint16_t s_order[];  // [B] (slots < kMaxCapacity = 2^14)
+  __shared__ int s_idx;
   typedef unsigned int v4u __attribute__((ext_vector_type(4)));
-  const int unit = blockIdx.x, z = blockIdx.y;
-  const int32_t s = a.slots[unit], p = a.pos[unit];
-  if (s < 0 || p < 0) return;
-  const uint8_t* src = a.records + ((int64_t)z * a.units + unit) * a.R;
-  uint8_t* cache = a.cache + (int64_t)z * a.cache_stride + ((int64_t)unit * a.B + s) * a.R;
-  uint8_t* host = a.host[z] + ((int64_t)unit * a.L + p) * a.R;
-  for (int c = threadIdx.x; c < (a.R >> 4); c += blockDim.x) {
-    const v4u v = *reinterpret_cast<const v4u*>(src + 16 * c);
-    if (a.write_cache) *reinterpret_cast<v4u*>(cache + 16 * c) = v;
-    if (a.write_host) *reinterpret_cast<v4u*>(host + 16 * c) = v;
+  const int unit = blockIdx.x, grp = blockIdx.y, tid = threadIdx.x, B = a.B;
+  const int anchor = a.first + grp * a.G;
+  const AnchorState st = a.states[anchor / a.G];
+  const int32_t p = a.pos[unit];
+  int32_t* slot_out = a.slots_out + (int64_t)grp * a.units + unit;
+  if ((int64_t)p >= a.L) {  // invalid: latch the error, leave the unit's state untouched
+    if (tid == 0) {
+      *slot_out = -1;
+      if (atomicCAS(&a.err[0], 0, (int)HISPARSE_ERR_BAD_SELECTION) == 0) {
+        a.err[1] = anchor;
+        a.err[2] = unit;
+      }
+      atomicAdd(&a.err[3], 1);
+    }
+    return;
+  }
+  const uint32_t t = st.clock[unit] + 1u;
+  if (p < 0) {  // nothing to admit this event: only the clock advances
+    if (tid == 0) {
+      *slot_out = -1;
+      st.clock[unit] = t;
+    }
+    return;
+  }
+  int32_t* pt = st.pt + (int64_t)unit * a.L;
+  int32_t* slot_pos = st.slot_pos + (int64_t)unit * B;
+  int32_t* order = st.order + (int64_t)unit * B;
+  const int32_t hit = pt[p];
+  if (tid == 0) s_idx = 0;  // stays in bounds even if the index were inconsistent
+  __syncthreads();
+  for (int j = tid; j < B; j += blockDim.x) {
+    const int32_t s = order[j];
+    s_order[j] = (uint16_t)s;
+    if (s == hit) s_idx = j;  // the hit slot's place in the index (at most one thread)
+  }
+  __syncthreads();
+  const int idx = hit >= 0 ? s_idx : 0;  // the entry that moves to the most-recent end
+  const int32_t slot = (int32_t)s_order[idx];
+  for (int j = idx + tid; j < B - 1; j += blockDim.x) order[j] = (int32_t)s_order[j + 1];
+  if (tid == 0) {
+    order[B - 1] = slot;
+    if (hit >= 0) {
+      st.slot_ts[(int64_t)unit * B + slot] = 2u * t;
+    } else {
+      const int32_t old = slot_pos[slot];
+      if (old >= 0) pt[old] = -1;  // the evicted record becomes host-only
+      pt[p] = slot;
+      slot_pos[slot] = p;
+      st.slot_ts[(int64_t)unit * B + slot] = 2u * t - 1u;
+    }
+    *slot_out = slot;
+    st.clock[unit] = t;
+  }
+  if (!a.write) return;
+  const int z_end = min(anchor + a.G, a.first + a.n_layers);
+  for (int z = anchor; z < z_end; ++z) {
+    const uint8_t* src = a.records + ((int64_t)(z - a.first) * a.units + unit) * a.R;
+    uint8_t* cache = a.layers[z].cache + ((int64_t)unit * B + slot) * a.R;
+    uint8_t* host = a.layers[z].host + ((int64_t)unit * a.L + p) * a.R;
+    for (int q = tid; q < (a.R >> 4); q += blockDim.x) {
+      const v4u v = *reinterpret_cast<const v4u*>(src + 16 * q);
+      *reinterpret_cast<v4u*>(cache + 16 * q) = v;
+      *reinterpret_cast<v4u*>(host + 16 * q) = v;
+    }
   }
 }
 
@@ -414,8 +475,10 @@ hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgr
   return hipGetLastError();
 }
 
-hipError_t launch_append(const AppendArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(append_kernel, dim3(a.units, a.n_layers), dim3(256), 0, stream, a);
+hipError_t launch_admit(const AdmitArgs& a, int32_t n_groups, hipStream_t stream) {
+  static_assert(kMaxCapacity <= 65536, "16-bit slots in the admission kernel's LDS");
+  hipLaunchKernelGGL(admit_kernel, dim3(a.units, n_groups), dim3(256), (size_t)a.B * 2, stream,
+                     a);
   return hipGetLastError();
 }
 

@@ -222,10 +222,10 @@ def hisparse_prefetch_layer(cache: int, anchor_layer: int, shared_layer: int,
            lib().hisparse_prefetch_layer(cache, anchor_layer, shared_layer, _s(stream)))
 
 
-def hisparse_append(cache: int, anchor_layer: int, num_layers: int, pos, records, slots,
+def hisparse_append(cache: int, first_layer: int, num_layers: int, pos, records, slots,
                     stream=None) -> None:
     _check("hisparse_append",
-           lib().hisparse_append(cache, anchor_layer, num_layers, _p(pos), _p(records), _p(slots),
+           lib().hisparse_append(cache, first_layer, num_layers, _p(pos), _p(records), _p(slots),
                                  _s(stream)))
 
 
