@@ -84,6 +84,9 @@ def parse():
                          "attention, write the step's generated record of every layer through "
                          "to the cache and the host pool (hisparse_append); token-record "
                          "workloads only")
+    ap.add_argument("--resolve-sweep", action="store_true",
+                    help="only time resolve (no IO) across cache sizes B/k = 1..8 and 1..64 "
+                         "units on the 32K-context DSA/MLA streams, one JSON line per point")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run one device-to-device copy of BYTES (calibrates the HBM "
                          "byte counters of a profiler run) and exit")
@@ -216,6 +219,45 @@ def cpu_baseline(w, cache, sel_host, budget_s: float, L: int) -> dict:
                       f"over {w.q_heads} heads, single thread, {dt:.1f} s"}
 
 
+def resolve_sweep(args, torch, hs, W, HiSparseCache) -> int:
+    """Resolve (metadata phases only, no IO) of the 32K-context DSA/MLA selection streams
+    across cache sizes B/k and batch sizes: µs per layer call, misses per unit and step, and
+    selections/s. One JSON line per point."""
+    import numpy as np
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    warm, steps = 8, 32
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for units in (1, 8, 32, 64):
+        w = W.workload(2, num_requests=units, num_layers=1)
+        sel = torch.from_numpy(W.selection_streams(w, steps=warm + steps)).to(dev)
+        for ratio in (1, 1.5, 2, 4, 8):
+            B = int(w.k * ratio)
+            cache = HiSparseCache.for_workload(dataclasses.replace(w, B=B),
+                                               fetch=hs.HISPARSE_FETCH_NONE)
+            slots = torch.empty((units, w.k), dtype=torch.int32, device=dev)
+            counts = torch.empty((steps, units, 2), dtype=torch.int32, device=dev)
+            for t in range(warm):
+                hs.hisparse_resolve_tables(cache.handle, 0, sel[t], slots, counts[0], stream)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for t in range(steps):
+                hs.hisparse_resolve_tables(cache.handle, 0, sel[warm + t], slots, counts[t],
+                                           stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / steps
+            c = counts.cpu().numpy().astype(np.int64)
+            print(json.dumps({"sweep": "resolve", "units": units, "k": w.k, "B": B,
+                              "B_over_k": ratio, "resolve_us_per_call": us,
+                              "misses_per_unit_step": float(c[:, :, 1].mean()),
+                              "hit_rate": float(c[:, :, 0].sum() / c.sum()),
+                              "selections_per_s": units * w.k / (us * 1e-6)}), flush=True)
+            cache.close()
+    return 0
+
+
 def main() -> int:
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -247,6 +289,8 @@ def main() -> int:
         print(json.dumps({"error": "no GPU visible"}))
         return 1
     L = hs.lib()  # fails loudly if the HIP library is missing
+    if args.resolve_sweep:
+        return resolve_sweep(args, torch, hs, W, HiSparseCache)
     hip = Hip()
     w0 = W.workload(args.config)
     w = W.fit_pinned(w0)
