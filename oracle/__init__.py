@@ -108,6 +108,14 @@ class OracleCache:
         return rc, slots, counts, plan_pos[:m].copy(), plan_slot[:m].copy()
 
 
+    def reset_unit(self, u: int) -> None:
+        """Admission of a new request into unit u (Section 3.3 (2)): the unit's cache starts
+        cold, exactly as at creation; the other units are untouched."""
+        self.pt[u] = -1
+        self.slot_pos[u] = -1
+        self.slot_ts[u] = 0
+        self.clock[u] = 0
+
     def admit_unit(self, u: int, pos: int):
         """Write-through admission of a newly generated record at position `pos` (Section 3.3
         (4)), read as a one-entry resolve event of the unit: the clock advances, a resident

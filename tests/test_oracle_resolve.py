@@ -271,3 +271,37 @@ def test_admission_matches_list_lru(seed):
                 e_slots, e_counts, e_plan = model.step(sel)
                 assert rc == oracle.OK and slots.tolist() == e_slots
                 assert list(zip(pp.tolist(), ps.tolist())) == e_plan
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_request_readmission_is_a_cold_cache(seed):
+    """Releasing a unit and admitting a new request into it (Section 3.3 (2)) starts that unit
+    from the cold state: from then on it agrees with a fresh independent list model fed only
+    the new request's selections, while the other units keep agreeing with the models that
+    have seen their whole history."""
+    rng = np.random.default_rng(400 + seed)
+    for trial in range(20):
+        U = 3
+        L = int(rng.integers(8, 64))
+        B = int(rng.integers(2, 17))
+        k = int(rng.integers(1, min(B, L) + 1))
+        models = [ListLRU(B) for _ in range(U)]
+        c = oracle.OracleCache(U, L, B, k)
+        steps = int(rng.integers(4, 30))
+        swap = int(rng.integers(1, steps))
+        victim = int(rng.integers(0, U))
+        for t in range(steps):
+            if t == swap:
+                c.reset_unit(victim)
+                models[victim] = ListLRU(B)
+                assert (c.pt[victim] == -1).all() and (c.slot_pos[victim] == -1).all()
+                assert c.clock[victim] == 0 and (c.slot_ts[victim] == 0).all()
+            sel = np.stack([rng.choice(L, size=k, replace=False) for _ in range(U)])
+            slots, counts, pp, ps, bad = c.resolve(sel.astype(np.int32))
+            assert bad == 0
+            for u in range(U):
+                e_slots, e_counts, e_plan = models[u].step(sel[u])
+                assert slots[u].tolist() == e_slots, (trial, t, u)
+                assert counts[u].tolist() == list(e_counts)
+                m = int(counts[u][1])
+                assert list(zip(pp[u][:m].tolist(), ps[u][:m].tolist())) == e_plan
