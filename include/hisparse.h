@@ -55,7 +55,8 @@ typedef enum {
   HISPARSE_ERR_OOM = -2,           /* device or pinned host allocation failed */
   HISPARSE_ERR_HIP = -3,           /* a HIP runtime call failed */
   HISPARSE_ERR_UNSUPPORTED = -4,   /* valid request this build does not implement */
-  HISPARSE_ERR_BAD_SELECTION = -5  /* latched device-side selection error (see above) */
+  HISPARSE_ERR_BAD_SELECTION = -5, /* latched device-side selection error (see above) */
+  HISPARSE_ERR_FULL = -6           /* every request slot is taken (hisparse_request_acquire) */
 } hisparse_status_t;
 
 /* How missed records travel from the host pool to the GPU cache (Section 3.4 Phase 4). */
@@ -160,6 +161,48 @@ hisparse_status_t hisparse_layer_cache(hisparse_cache_t cache, int32_t layer, vo
 
 /* [async] Return every anchor layer's units to the cold state (all slots empty, clocks 0). */
 hisparse_status_t hisparse_reset(hisparse_cache_t cache, void* stream);
+
+/* ---- Request lifecycle (Section 3.3 (1) prefill and staging, (2) admission) ----
+ * A cache reserves every unit's slot caches and tables for all its layers when it is created
+ * (num_layers * B * R bytes of slots per unit, the per-request reservation Section 3.3 (2)
+ * sizes by B rather than by context length), so admitting a request allocates nothing: it takes
+ * one of num_requests request slots, whose units are
+ * [request * units_per_request, (request + 1) * units_per_request). */
+
+/* Take a free request slot, lowest index first (host bookkeeping; no GPU work, and the kernels
+ * do not consult it). All slots are free after creation. Returns HISPARSE_ERR_FULL, leaving
+ * *request = -1, when every slot is taken. */
+hisparse_status_t hisparse_request_acquire(hisparse_cache_t cache, int32_t* request);
+
+/* [async] Give a request slot back: its units go back to the cold state in every anchor layer
+ * (hisparse_reset_units on `stream`) and the slot is free for the next acquire at once, so
+ * work for the next request on those units must be ordered after this call by `stream`.
+ * Returns INVALID_ARG for a slot that is out of range or not taken. */
+hisparse_status_t hisparse_request_release(hisparse_cache_t cache, int32_t request,
+                                           void* stream);
+
+/* [async] Cold state for units [first_unit, first_unit + num_units) of every anchor layer, as
+ * after creation: page-table rows cleared, slots empty, stamps and clocks 0, recency index in
+ * slot order, miss plans empty. Other units, the GPU caches' bytes and the host pools are
+ * untouched. 1 <= num_units, first_unit + num_units <= units. */
+hisparse_status_t hisparse_reset_units(hisparse_cache_t cache, int32_t first_unit,
+                                       int32_t num_units, void* stream);
+
+/* [async] Prefill staging (Section 3.3 (1)): copy records [first_record, first_record +
+ * num_records) of units [first_unit, first_unit + num_units) of layers [first_layer,
+ * first_layer + num_layers) from device memory into the host pools with the copy engines
+ * (device-to-host hipMemcpyAsync, one per layer when num_records = L or num_units = 1, else one
+ * per unit and layer).
+ *   d_src  device; layer first_layer + j at d_src + j * src_layer_stride, laid out
+ *          [num_units][num_records][R] (not modified).
+ *   src_layer_stride  bytes, >= num_units * num_records * R; ignored when num_layers = 1.
+ * The records may be resolved once this work has completed (the staging acknowledgement: an
+ * event the caller records on `stream` after the call). The staged range must not be read by
+ * fetches in flight. Capturable in a HIP graph. */
+hisparse_status_t hisparse_stage(hisparse_cache_t cache, int32_t first_layer, int32_t num_layers,
+                                 int32_t first_unit, int32_t num_units, int64_t first_record,
+                                 int64_t num_records, const void* d_src,
+                                 int64_t src_layer_stride, void* stream);
 
 /* [async] Resolve one step of an anchor layer (Section 3.4 phases 1-5).
  *   d_sel    int32 [units][k]: selected positions per unit, in the indexer's order.

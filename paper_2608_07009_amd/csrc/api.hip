@@ -103,6 +103,7 @@ const char* hisparse_status_string(hisparse_status_t s) {
     case HISPARSE_ERR_HIP: return "HISPARSE_ERR_HIP";
     case HISPARSE_ERR_UNSUPPORTED: return "HISPARSE_ERR_UNSUPPORTED";
     case HISPARSE_ERR_BAD_SELECTION: return "HISPARSE_ERR_BAD_SELECTION";
+    case HISPARSE_ERR_FULL: return "HISPARSE_ERR_FULL";
   }
   return "HISPARSE_ERR_UNKNOWN";
 }
@@ -176,6 +177,7 @@ hisparse_status_t hisparse_cache_create(const hisparse_cache_desc_t* desc, int32
   c->desc = *desc;
   c->device = device;
   c->units = desc->num_requests * desc->units_per_request;
+  c->request_taken.assign(desc->num_requests, 0);
   c->n_anchors = (desc->num_layers + desc->share_group - 1) / desc->share_group;
   const size_t U = (size_t)c->units, L = (size_t)desc->num_records, B = (size_t)desc->capacity;
   const size_t R = (size_t)desc->record_bytes, K = (size_t)desc->top_k;
@@ -299,6 +301,73 @@ hisparse_status_t hisparse_reset(hisparse_cache_t c, void* stream) {
   for (auto& a : c->anchors)
     if (hisparse::launch_reset_state(state_args(c, a), as_stream(stream)) != hipSuccess)
       return HISPARSE_ERR_HIP;
+  return HISPARSE_OK;
+}
+
+hisparse_status_t hisparse_reset_units(hisparse_cache_t c, int32_t first_unit, int32_t num_units,
+                                       void* stream) {
+  if (!c || first_unit < 0 || num_units < 1 || num_units > c->units - first_unit)
+    return HISPARSE_ERR_INVALID_ARG;
+  const int64_t L = c->desc.num_records, B = c->desc.capacity;
+  for (auto& a : c->anchors) {
+    hisparse::StateArgs s = state_args(c, a);  // the same cold-state kernel on a unit range
+    s.pt += first_unit * L;
+    s.slot_pos += first_unit * B;
+    s.slot_ts += first_unit * B;
+    s.order += first_unit * B;
+    s.clock += first_unit;
+    s.plan_count += first_unit;
+    s.units = num_units;
+    if (hisparse::launch_reset_state(s, as_stream(stream)) != hipSuccess) return HISPARSE_ERR_HIP;
+  }
+  return HISPARSE_OK;
+}
+
+hisparse_status_t hisparse_request_acquire(hisparse_cache_t c, int32_t* request) {
+  if (!c || !request) return HISPARSE_ERR_INVALID_ARG;
+  *request = -1;
+  for (size_t r = 0; r < c->request_taken.size(); ++r)
+    if (!c->request_taken[r]) {
+      c->request_taken[r] = 1;
+      *request = (int32_t)r;
+      return HISPARSE_OK;
+    }
+  return HISPARSE_ERR_FULL;
+}
+
+hisparse_status_t hisparse_request_release(hisparse_cache_t c, int32_t request, void* stream) {
+  if (!c || request < 0 || request >= c->desc.num_requests || !c->request_taken[request])
+    return HISPARSE_ERR_INVALID_ARG;
+  const int32_t H = c->desc.units_per_request;
+  const hisparse_status_t st = hisparse_reset_units(c, request * H, H, stream);
+  if (st == HISPARSE_OK) c->request_taken[request] = 0;
+  return st;
+}
+
+hisparse_status_t hisparse_stage(hisparse_cache_t c, int32_t first_layer, int32_t num_layers,
+                                 int32_t first_unit, int32_t num_units, int64_t first_record,
+                                 int64_t num_records, const void* d_src,
+                                 int64_t src_layer_stride, void* stream) {
+  if (!c || !d_src || first_layer < 0 || num_layers < 1 ||
+      num_layers > c->desc.num_layers - first_layer || first_unit < 0 || num_units < 1 ||
+      num_units > c->units - first_unit)
+    return HISPARSE_ERR_INVALID_ARG;
+  const int64_t L = c->desc.num_records, R = c->desc.record_bytes;
+  if (first_record < 0 || num_records < 1 || num_records > L - first_record)
+    return HISPARSE_ERR_INVALID_ARG;
+  const int64_t unit_bytes = num_records * R, layer_bytes = num_units * unit_bytes;
+  if (num_layers > 1 && src_layer_stride < layer_bytes) return HISPARSE_ERR_INVALID_ARG;
+  const bool whole = num_records == L || num_units == 1;  // one contiguous range per layer
+  for (int32_t j = 0; j < num_layers; ++j) {
+    const uint8_t* src = reinterpret_cast<const uint8_t*>(d_src) + j * src_layer_stride;
+    uint8_t* dst = reinterpret_cast<uint8_t*>(c->host[first_layer + j]) +
+                   ((int64_t)first_unit * L + first_record) * R;
+    for (int32_t u = 0; u < (whole ? 1 : num_units); ++u)
+      if (hipMemcpyAsync(dst + u * L * R, src + u * unit_bytes,
+                         (size_t)(whole ? layer_bytes : unit_bytes), hipMemcpyDeviceToHost,
+                         as_stream(stream)) != hipSuccess)
+        return HISPARSE_ERR_HIP;
+  }
   return HISPARSE_OK;
 }
 

@@ -137,6 +137,7 @@ struct hisparse_cache {
   hisparse::AnchorState* d_states = nullptr;  // device copies of every anchor's state pointers
   hisparse::LayerIO* d_layers = nullptr;      // and of every layer's cache / host pool address
   std::vector<Anchor> anchors;   // per anchor layer (layer / share_group)
+  std::vector<uint8_t> request_taken;  // request slots handed out by hisparse_request_acquire
   int32_t* err = nullptr;        // device error word
   // HISPARSE_FETCH_SDMA: pinned readback of a plan and the host-side copy lists
   int32_t* h_plan_count = nullptr;

@@ -22,6 +22,7 @@ HISPARSE_ERR_OOM = -2
 HISPARSE_ERR_HIP = -3
 HISPARSE_ERR_UNSUPPORTED = -4
 HISPARSE_ERR_BAD_SELECTION = -5
+HISPARSE_ERR_FULL = -6
 
 HISPARSE_FETCH_ZERO_COPY = 0
 HISPARSE_FETCH_SDMA = 1
@@ -37,7 +38,8 @@ EXPORTED = (
     "hisparse_cache_create", "hisparse_cache_destroy", "hisparse_host_pool",
     "hisparse_layer_cache", "hisparse_reset", "hisparse_resolve", "hisparse_resolve_tables",
     "hisparse_fetch", "hisparse_fetch_units", "hisparse_fetch_group", "hisparse_prefetch_layer",
-    "hisparse_prefetch_layers", "hisparse_append",
+    "hisparse_prefetch_layers", "hisparse_append", "hisparse_request_acquire",
+    "hisparse_request_release", "hisparse_reset_units", "hisparse_stage",
     "hisparse_decode_workspace_bytes", "hisparse_sparse_decode", "hisparse_sparse_decode_layers",
     "hisparse_sparse_decode_prefetch",
     "hisparse_sparse_decode_pool",
@@ -91,6 +93,11 @@ def lib() -> ctypes.CDLL:
             "hisparse_layer_cache": (_I32, [_V, _I32, ctypes.POINTER(_V),
                                             ctypes.POINTER(ctypes.c_size_t)]),
             "hisparse_reset": (_I32, [_V, _V]),
+            "hisparse_request_acquire": (_I32, [_V, ctypes.POINTER(_I32)]),
+            "hisparse_request_release": (_I32, [_V, _I32, _V]),
+            "hisparse_reset_units": (_I32, [_V, _I32, _I32, _V]),
+            "hisparse_stage": (_I32, [_V, _I32, _I32, _I32, _I32, ctypes.c_int64,
+                                      ctypes.c_int64, _V, ctypes.c_int64, _V]),
             "hisparse_resolve": (_I32, [_V, _I32, _V, _V, _V, _V]),
             "hisparse_resolve_tables": (_I32, [_V, _I32, _V, _V, _V, _V]),
             "hisparse_fetch": (_I32, [_V, _I32, _V]),
@@ -187,6 +194,30 @@ def hisparse_layer_cache(cache: int, layer: int) -> tuple[int, int]:
 
 def hisparse_reset(cache: int, stream=None) -> None:
     _check("hisparse_reset", lib().hisparse_reset(cache, _s(stream)))
+
+
+def hisparse_request_acquire(cache: int) -> int:
+    r = _I32()
+    _check("hisparse_request_acquire", lib().hisparse_request_acquire(cache, ctypes.byref(r)))
+    return r.value
+
+
+def hisparse_request_release(cache: int, request: int, stream=None) -> None:
+    _check("hisparse_request_release", lib().hisparse_request_release(cache, request,
+                                                                     _s(stream)))
+
+
+def hisparse_reset_units(cache: int, first_unit: int, num_units: int, stream=None) -> None:
+    _check("hisparse_reset_units", lib().hisparse_reset_units(cache, first_unit, num_units,
+                                                             _s(stream)))
+
+
+def hisparse_stage(cache: int, first_layer: int, num_layers: int, first_unit: int,
+                   num_units: int, first_record: int, num_records: int, d_src,
+                   src_layer_stride: int = 0, stream=None) -> None:
+    _check("hisparse_stage", lib().hisparse_stage(cache, first_layer, num_layers, first_unit,
+                                                 num_units, first_record, num_records,
+                                                 _p(d_src), src_layer_stride, _s(stream)))
 
 
 def hisparse_resolve(cache: int, layer: int, d_sel, d_slots, d_counts=None, stream=None) -> None:

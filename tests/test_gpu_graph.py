@@ -232,3 +232,74 @@ def test_graph_replay_append():
         torch.cuda.synchronize()
         eager.close()
         graph.close()
+
+
+def test_graph_replay_lifecycle():
+    """Request turnover captured in a graph: every replay releases unit 1's request (cold reset
+    of its tables), stages a new request's records into unit 1's host pools from a device
+    buffer picked by a device-side step counter, then resolves and fetches a step for both
+    units. Every replay matches the eager run (slots, counts, tables, caches, host pools)."""
+    steps = 4
+    w = W.workload(1, num_layers=2, share_group=2, num_requests=2)
+    U, L, R = w.units, w.L, w.record_bytes
+    log(f"test_graph_replay_lifecycle {w.name} steps={steps}")
+    eager, graph = Run(w, steps), Run(w, steps)
+    try:
+        dev = eager.dev
+        srcs = np.empty((steps, 2, L, R), dtype=np.uint8)  # per replay: unit 1's new records
+        for t in range(steps):
+            wt = W.workload(1, num_layers=2, share_group=2, num_requests=2, seed=w.seed + 11 + t)
+            for l in range(2):
+                W.fill_kv(srcs[t, l].ctypes.data, wt, l, 1, 1)
+        srcs_d = torch.from_numpy(srcs).to(dev)
+        sel = eager.sel
+        ref = []
+        for t in range(steps):
+            h = eager.cache.handle
+            hs.hisparse_reset_units(h, 1, 1, eager.stream)
+            hs.hisparse_stage(h, 0, 2, 1, 1, 0, L, srcs_d[t], L * R, eager.stream)
+            hs.hisparse_resolve(h, 0, sel[t], eager.slots[0], eager.counts[0], eager.stream)
+            hs.hisparse_prefetch_layer(h, 0, 1, eager.stream)
+            torch.cuda.synchronize()
+            ref.append((eager.slots[0].clone(), eager.counts[0].clone(),
+                        eager.cache.read_state(0), [layer_cache_host(eager, l) for l in range(2)],
+                        [eager.cache.host_view(l).copy() for l in range(2)]))
+
+        step = torch.zeros(1, dtype=torch.int64, device=dev)
+        sel_buf = torch.empty_like(sel[0])
+        src_buf = torch.empty_like(srcs_d[0])
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(g, stream=s):
+                cs = torch.cuda.current_stream()
+                sel_buf.copy_(sel.index_select(0, step).squeeze(0))
+                src_buf.copy_(srcs_d.index_select(0, step).squeeze(0))
+                step.add_(1)
+                h = graph.cache.handle
+                hs.hisparse_reset_units(h, 1, 1, cs)
+                hs.hisparse_stage(h, 0, 2, 1, 1, 0, L, src_buf, L * R, cs)
+                hs.hisparse_resolve(h, 0, sel_buf, graph.slots[0], graph.counts[0], cs)
+                hs.hisparse_prefetch_layer(h, 0, 1, cs)
+        torch.cuda.synchronize()
+        for t in range(steps):
+            g.replay()
+            torch.cuda.synchronize()
+            scratch = torch.randn(1 << 16, device=dev).sum()  # eager work between replays
+            e_slots, e_counts, e_st, e_caches, e_pools = ref[t]
+            assert torch.equal(graph.slots[0], e_slots), f"slots differ at replay {t}"
+            assert torch.equal(graph.counts[0], e_counts), f"counts differ at replay {t}"
+            st = graph.cache.read_state(0)
+            for key in ("slot_pos", "slot_ts", "order", "clock", "page_table"):
+                assert (st[key] == e_st[key]).all(), f"{key} differs at replay {t}"
+            for l in range(2):
+                assert (layer_cache_host(graph, l) == e_caches[l]).all(), f"replay {t} layer {l}"
+                assert (graph.cache.host_view(l) == e_pools[l]).all(), f"pool {t} layer {l}"
+                assert (graph.cache.host_view(l)[1] == srcs[t, l]).all()
+            del scratch
+        assert graph.cache.check_errors()[0] == hs.HISPARSE_OK
+    finally:
+        torch.cuda.synchronize()
+        eager.close()
+        graph.close()
