@@ -84,6 +84,13 @@ def parse():
                          "attention, write the step's generated record of every layer through "
                          "to the cache and the host pool (hisparse_append); token-record "
                          "workloads only")
+    ap.add_argument("--speculate", action="store_true",
+                    help="speculative cross-layer prefetch (models whose layers do not share "
+                         "selections): layer l's selection is prefetched into layer l+1 as a "
+                         "hint (hisparse_speculate) on a side stream during layer l's attention")
+    ap.add_argument("--xlayer-overlap", type=float, default=0.0, metavar="RHO",
+                    help="make adjacent layers' selections share a fraction RHO of their drawn "
+                         "entries within a step (workload.correlate_layers); default 0")
     ap.add_argument("--stage", action="store_true",
                     help="also measure prefill staging (hisparse_stage): one request's records "
                          "of every layer copied device-to-host into the host pools, alone against "
@@ -405,6 +412,12 @@ def main() -> int:
         # the context grows by one record per step: step t's window follows the records
         # appended by the previous steps, the record generated at step t goes to L + t
         sel_host = W.grow_streams(w, sel_host)
+    if args.xlayer_overlap > 0:
+        sel_host = W.correlate_layers(w, sel_host, args.xlayer_overlap, seed=w.seed)
+    if args.speculate and (G != 1 or w.num_layers < 2):
+        print(json.dumps({"error": "--speculate needs layers that do not share selections "
+                          "(share group 1) and at least two layers"}))
+        return 2
     L_pool = w.L + (steps_needed if args.append else 0)
     sel = torch.from_numpy(sel_host).to(dev)
     n_qv = 2  # queries vary by (layer, step parity)
@@ -471,6 +484,9 @@ def main() -> int:
                             .add_(w.L).unsqueeze(1).repeat(1, U).contiguous())
                 self.adm = torch.empty((len(groups), U), dtype=torch.int32, device=dev)
             self.link = [hip.event(timing=False) for _ in groups]
+            if args.speculate:  # {already resident, fetched} of every hint event
+                self.spec_counts = torch.zeros((steps_needed, w.num_layers, U, 2),
+                                               dtype=torch.int32, device=dev)
 
     mbs = [MicroBatch(i) for i in range(n_mb)]
     cache = mbs[0].cache
@@ -483,7 +499,7 @@ def main() -> int:
     f_tables, f_fetch = L.hisparse_resolve_tables, L.hisparse_fetch
     f_prefetch_layers, f_decode = L.hisparse_prefetch_layers, L.hisparse_sparse_decode
     f_decode_prefetch = L.hisparse_sparse_decode_prefetch
-    f_append = L.hisparse_append
+    f_append, f_speculate = L.hisparse_append, L.hisparse_speculate
     f_decode_layers, f_fetch_group = L.hisparse_sparse_decode_layers, L.hisparse_fetch_group
     rec = hip.L.hipEventRecord
     wait = hip.L.hipStreamWaitEvent
@@ -527,7 +543,18 @@ def main() -> int:
 
         if not shared:
             transfer("fetch", f_fetch, h, a, ms)
+            nxt = a + 1
+            if args.speculate and nxt < w.num_layers:
+                # this layer's selection as a hint for the next layer, on the side stream
+                # under this layer's attention; the next layer's resolve waits for it
+                rec(mb.sync[0], ms)
+                wait(ss, mb.sync[0], 0)
+                scp = None if sel_override else mb.spec_counts[t, nxt].data_ptr()
+                call("speculate", ss, ev, spans, f_speculate, h, nxt, sp, scp, ss)
+                rec(mb.sync[1], ss)
             decode(a)
+            if args.speculate and nxt < w.num_layers:
+                wait(ms, mb.sync[1], 0)
         elif args.schedule == "serial":
             # the anchor's fetch and its shared layers' replays in one launch, then the
             # layers' attention in order
@@ -626,7 +653,8 @@ def main() -> int:
     # its kernel, not a host launch gap. Its GPU time per step is reported beside the timed
     # region's. With several micro-batches the spans of concurrent kernels overlap: each span
     # is that kernel's duration while sharing the GPU.
-    per_step_events = n_mb * (2 + sum(2 * (3 + 2 * len(sh)) for _, sh in groups))
+    per_step_events = n_mb * (2 + sum(2 * (3 + 2 * len(sh) + int(args.speculate))
+                                      for _, sh in groups))
     events = [hip.event() for _ in range(per_step_events * args.steps)]
     ref, end = hip.event(), hip.event()
     spans = []
@@ -658,7 +686,8 @@ def main() -> int:
         d = hip.ms(e0, e1) * 1e-3
         t_sum, n = tot.get(name, (0.0, 0))
         tot[name] = (t_sum + d, n + 1)
-        if name in ("fetch", "prefetch_replay", "fetch_group", "sparse_decode_prefetch"):
+        if name in ("fetch", "prefetch_replay", "fetch_group", "sparse_decode_prefetch",
+                    "speculate"):
             io_intervals.append((hip.ms(ref, e0) * 1e-3, hip.ms(ref, e1) * 1e-3))
     for e in events:
         hip.L.hipEventDestroy(e)
@@ -742,6 +771,18 @@ def main() -> int:
             "GBps": carried_bytes / t_pf / 1e9,
             "note": "attention of one layer with the replay into the next shared layer in the "
                     "same launch; also counted in sparse_decode"}
+    t_spc, n_spc = kernel("speculate")
+    spec_bytes = 0
+    if n_spc:
+        sc = np.concatenate([mb.spec_counts[args.warmup:steps_needed].cpu().numpy()
+                             for mb in mbs], axis=2).astype(np.int64)
+        spec_bytes = int(sc[..., 1].sum()) * R if moves_data else 0
+        kernels["speculate"] = {
+            "launches": n_spc, "avg_us": t_spc / n_spc * 1e6,
+            "bytes_per_launch": spec_bytes / n_spc, "GBps": spec_bytes / t_spc / 1e9,
+            "hint_resident_rate": float(sc[..., 0].sum() / max(1, sc.sum())),
+            "note": "resolve of the next layer's cache with this layer's selection as a hint, "
+                    "plus the fetch of the hinted records it lacked, on a side stream"}
     n_tok = k * w.tokens_per_record
     att_flops_call = 2.0 * U * w.q_heads * n_tok * (w.d_qk + w.d_v)
     att_bytes_call = (U * n_tok * (R // w.tokens_per_record) + U * w.q_heads * w.d_qk * 2
@@ -802,7 +843,8 @@ def main() -> int:
                 "unit": "GB/s", "frac": kd["hbm_GBps"] / HBM_PEAK_GBPS, "traffic": None}
 
     io_busy = union_length(io_intervals)
-    miss_gbps = ((fetch_bytes + replay_bytes + group_bytes + carried_bytes) / io_busy / 1e9
+    miss_gbps = ((fetch_bytes + replay_bytes + group_bytes + carried_bytes + spec_bytes)
+                 / io_busy / 1e9
                  if (io_busy and moves_data) else None)
 
     # the same steps replayed from a captured HIP graph (cold reset, same warmup)
@@ -927,6 +969,7 @@ def main() -> int:
                    "append": args.append,
                    "records_per_unit": w.L, "record_bytes": R, "top_k": k, "capacity": w.B,
                    "share_group": G, "q_heads": w.q_heads, "fetch": args.fetch,
+                   "speculate": args.speculate, "xlayer_overlap": args.xlayer_overlap,
                    "host_memory": args.host_memory, "mode": mode,
                    "steps_per_graph": graph["steps_per_graph"] if graph else None},
         "decode_tokens_per_s": w.num_requests * K / wall,

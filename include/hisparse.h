@@ -68,7 +68,7 @@ typedef enum {
    * copy (hipMemcpyBatchAsync) of the missed records. Not capturable in a HIP graph: calls
    * that fetch return HISPARSE_ERR_UNSUPPORTED while `stream` is capturing. */
   HISPARSE_FETCH_SDMA = 1,
-  /* Timing mode (Section 4.6's "no-IO oracle"): tables and slot outputs are exact, but no
+  /* Timing mode (the no-IO oracle of Section 4.6): tables and slot outputs are exact, but no
    * record is copied, so the cache holds stale data and attention outputs are not valid. */
   HISPARSE_FETCH_NONE = 2
 } hisparse_fetch_t;
@@ -265,6 +265,22 @@ hisparse_status_t hisparse_prefetch_layer(hisparse_cache_t cache, int32_t anchor
 hisparse_status_t hisparse_prefetch_layers(hisparse_cache_t cache, int32_t anchor_layer,
                                            int32_t first_shared, int32_t num_layers,
                                            void* stream);
+
+/* [async] Speculative cross-layer prefetch for models whose layers do not share selections
+ * (Section 3.5, the speculative alternative to exact prefetch): anchor layer `layer` takes a
+ * hint, typically the previous layer's selection of the same step, as one access event of its
+ * canonical LRU, exactly as hisparse_resolve would take it as a selection: the layer's clock
+ * advances, hinted records already resident are refreshed, the others are fetched into its
+ * least-recent slots. Its own resolve later in the step then finds them resident. No slot
+ * vector is written.
+ *   d_hint   int32 [units][k], positions in [0, L) or -1 for padding (invalid entries latch
+ *            HISPARSE_ERR_BAD_SELECTION as in hisparse_resolve).
+ *   d_counts int32 [units][2]: out, {already resident, fetched} per unit; may be NULL.
+ * A wrong hint costs transfers and evictions, never correctness: the layer's resolve still
+ * makes every selected record resident. The hint replaces the layer's miss plan, so replays
+ * into shared layers (hisparse_prefetch_layer) must follow the layer's own resolve. */
+hisparse_status_t hisparse_speculate(hisparse_cache_t cache, int32_t layer,
+                                     const int32_t* d_hint, int32_t* d_counts, void* stream);
 
 /* [async] Write-through of generated records (Section 3.3 (4)): each unit's newly generated
  * record enters the GPU caches of layers [first_layer, first_layer + num_layers) and is written

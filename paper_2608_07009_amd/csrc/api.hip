@@ -399,10 +399,10 @@ hisparse_status_t hisparse_append(hisparse_cache_t c, int32_t first_layer, int32
   return HISPARSE_OK;
 }
 
-hisparse_status_t hisparse_resolve_tables(hisparse_cache_t c, int32_t layer,
-                                          const int32_t* d_sel, int32_t* d_slots,
-                                          int32_t* d_counts, void* stream) {
-  if (!c || !d_sel || !d_slots || !is_anchor(c, layer)) return HISPARSE_ERR_INVALID_ARG;
+namespace {
+// Phases 1-3 and 5 of an anchor layer; d_slots may be null (no slot vector is written).
+hisparse_status_t resolve_tables(hisparse_cache_t c, int32_t layer, const int32_t* d_sel,
+                                 int32_t* d_slots, int32_t* d_counts, void* stream) {
   auto& an = c->anchors[layer / c->desc.share_group];
   hisparse::ResolveArgs a{};
   a.sel = d_sel;
@@ -423,6 +423,14 @@ hisparse_status_t hisparse_resolve_tables(hisparse_cache_t c, int32_t layer,
   a.units = c->units;
   if (hisparse::launch_resolve(a, as_stream(stream)) != hipSuccess) return HISPARSE_ERR_HIP;
   return HISPARSE_OK;
+}
+}  // namespace
+
+hisparse_status_t hisparse_resolve_tables(hisparse_cache_t c, int32_t layer,
+                                          const int32_t* d_sel, int32_t* d_slots,
+                                          int32_t* d_counts, void* stream) {
+  if (!c || !d_sel || !d_slots || !is_anchor(c, layer)) return HISPARSE_ERR_INVALID_ARG;
+  return resolve_tables(c, layer, d_sel, d_slots, d_counts, stream);
 }
 
 namespace {
@@ -554,6 +562,14 @@ hisparse_status_t hisparse_fetch_group(hisparse_cache_t c, int32_t anchor_layer,
 hisparse_status_t hisparse_resolve(hisparse_cache_t c, int32_t layer, const int32_t* d_sel,
                                    int32_t* d_slots, int32_t* d_counts, void* stream) {
   hisparse_status_t st = hisparse_resolve_tables(c, layer, d_sel, d_slots, d_counts, stream);
+  if (st != HISPARSE_OK) return st;
+  return enqueue_fetch(c, layer, layer, as_stream(stream));
+}
+
+hisparse_status_t hisparse_speculate(hisparse_cache_t c, int32_t layer, const int32_t* d_hint,
+                                     int32_t* d_counts, void* stream) {
+  if (!c || !d_hint || !is_anchor(c, layer)) return HISPARSE_ERR_INVALID_ARG;
+  hisparse_status_t st = resolve_tables(c, layer, d_hint, nullptr, d_counts, stream);
   if (st != HISPARSE_OK) return st;
   return enqueue_fetch(c, layer, layer, as_stream(stream));
 }

@@ -100,7 +100,7 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   int32_t* slot_pos = a.slot_pos + (int64_t)unit * B;
   uint32_t* slot_ts = a.slot_ts + (int64_t)unit * B;
   int32_t* order = a.order + (int64_t)unit * B;
-  int32_t* slots_out = a.slots_out + (int64_t)unit * k;
+  int32_t* slots_out = a.slots_out ? a.slots_out + (int64_t)unit * k : nullptr;  // null: no slot vector
   int2* plan = a.plan + (int64_t)unit * k;
 
   for (int i = tid; i < bw; i += NT) {
@@ -216,7 +216,8 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   __syncthreads();
 
   if (s_bad) {  // invalid selection: publish -1 and leave the unit's state untouched
-    for (int i = tid; i < k; i += NT) slots_out[i] = -1;
+    if (slots_out)
+      for (int i = tid; i < k; i += NT) slots_out[i] = -1;
     if (tid == 0) {
       if (a.counts_out) {
         a.counts_out[2 * unit] = 0;
@@ -307,7 +308,8 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
     s_out[i] = v;
   }
   __syncthreads();
-  for (int i = tid; i < k; i += NT) slots_out[i] = s_out[i];
+  if (slots_out)
+    for (int i = tid; i < k; i += NT) slots_out[i] = s_out[i];
   if (tid == 0) {
     if (a.counts_out) {
       a.counts_out[2 * unit] = hits;

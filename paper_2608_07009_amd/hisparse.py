@@ -39,7 +39,7 @@ EXPORTED = (
     "hisparse_layer_cache", "hisparse_reset", "hisparse_resolve", "hisparse_resolve_tables",
     "hisparse_fetch", "hisparse_fetch_units", "hisparse_fetch_group", "hisparse_prefetch_layer",
     "hisparse_prefetch_layers", "hisparse_append", "hisparse_request_acquire",
-    "hisparse_request_release", "hisparse_reset_units", "hisparse_stage",
+    "hisparse_request_release", "hisparse_reset_units", "hisparse_stage", "hisparse_speculate",
     "hisparse_decode_workspace_bytes", "hisparse_sparse_decode", "hisparse_sparse_decode_layers",
     "hisparse_sparse_decode_prefetch",
     "hisparse_sparse_decode_pool",
@@ -96,6 +96,7 @@ def lib() -> ctypes.CDLL:
             "hisparse_request_acquire": (_I32, [_V, ctypes.POINTER(_I32)]),
             "hisparse_request_release": (_I32, [_V, _I32, _V]),
             "hisparse_reset_units": (_I32, [_V, _I32, _I32, _V]),
+            "hisparse_speculate": (_I32, [_V, _I32, _V, _V, _V]),
             "hisparse_stage": (_I32, [_V, _I32, _I32, _I32, _I32, ctypes.c_int64,
                                       ctypes.c_int64, _V, ctypes.c_int64, _V]),
             "hisparse_resolve": (_I32, [_V, _I32, _V, _V, _V, _V]),
@@ -218,6 +219,11 @@ def hisparse_stage(cache: int, first_layer: int, num_layers: int, first_unit: in
     _check("hisparse_stage", lib().hisparse_stage(cache, first_layer, num_layers, first_unit,
                                                  num_units, first_record, num_records,
                                                  _p(d_src), src_layer_stride, _s(stream)))
+
+
+def hisparse_speculate(cache: int, layer: int, d_hint, d_counts=None, stream=None) -> None:
+    _check("hisparse_speculate", lib().hisparse_speculate(cache, layer, _p(d_hint), _p(d_counts),
+                                                         _s(stream)))
 
 
 def hisparse_resolve(cache: int, layer: int, d_sel, d_slots, d_counts=None, stream=None) -> None:

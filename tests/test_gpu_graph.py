@@ -303,3 +303,62 @@ def test_graph_replay_lifecycle():
         torch.cuda.synchronize()
         eager.close()
         graph.close()
+
+
+def test_graph_replay_speculate():
+    """Resolve of layer 0, its selection as a hint for layer 1 (hisparse_speculate), resolve of
+    layer 1, captured in a graph: every replay matches the eager run (slots, counts, hint
+    counts, tables, caches)."""
+    steps = 6
+    w = W.workload(1, num_layers=2, share_group=1, num_requests=2)
+    U = w.units
+    log(f"test_graph_replay_speculate {w.name} steps={steps}")
+    eager, graph = Run(w, steps), Run(w, steps)
+    try:
+        dev = eager.dev
+        sel = torch.from_numpy(W.correlate_layers(w, eager.sel_host, 0.5, seed=5)).to(dev)
+        hc_e = torch.empty((U, 2), dtype=torch.int32, device=dev)
+        ref = []
+        for t in range(steps):
+            h = eager.cache.handle
+            hs.hisparse_resolve(h, 0, sel[t, :U], eager.slots[0], eager.counts[0], eager.stream)
+            hs.hisparse_speculate(h, 1, sel[t, :U], hc_e, eager.stream)
+            hs.hisparse_resolve(h, 1, sel[t, U:], eager.slots[1], eager.counts[1], eager.stream)
+            torch.cuda.synchronize()
+            ref.append((eager.slots.clone(), eager.counts.clone(), hc_e.clone(),
+                        eager.cache.read_state(1), [layer_cache_host(eager, l) for l in range(2)]))
+        step = torch.zeros(1, dtype=torch.int64, device=dev)
+        sel_buf = torch.empty_like(sel[0])
+        hc_g = torch.empty((U, 2), dtype=torch.int32, device=dev)
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(g, stream=s):
+                cs = torch.cuda.current_stream()
+                sel_buf.copy_(sel.index_select(0, step).squeeze(0))
+                step.add_(1)
+                h = graph.cache.handle
+                hs.hisparse_resolve(h, 0, sel_buf[:U], graph.slots[0], graph.counts[0], cs)
+                hs.hisparse_speculate(h, 1, sel_buf[:U], hc_g, cs)
+                hs.hisparse_resolve(h, 1, sel_buf[U:], graph.slots[1], graph.counts[1], cs)
+        torch.cuda.synchronize()
+        for t in range(steps):
+            g.replay()
+            torch.cuda.synchronize()
+            scratch = torch.randn(1 << 16, device=dev).sum()  # eager work between replays
+            e_slots, e_counts, e_hc, e_st, e_caches = ref[t]
+            assert torch.equal(graph.slots, e_slots), f"slots differ at replay {t}"
+            assert torch.equal(graph.counts, e_counts), f"counts differ at replay {t}"
+            assert torch.equal(hc_g, e_hc), f"hint counts differ at replay {t}"
+            st = graph.cache.read_state(1)
+            for key in ("slot_pos", "slot_ts", "order", "clock", "page_table"):
+                assert (st[key] == e_st[key]).all(), f"{key} differs at replay {t}"
+            for l in range(2):
+                assert (layer_cache_host(graph, l) == e_caches[l]).all(), f"replay {t} layer {l}"
+            del scratch
+        assert graph.cache.check_errors()[0] == hs.HISPARSE_OK
+    finally:
+        torch.cuda.synchronize()
+        eager.close()
+        graph.close()

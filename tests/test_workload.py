@@ -71,3 +71,31 @@ def test_grow_streams_shift_window_only():
         assert (gs[drawn] == s[drawn]).all()
         assert sorted(gs[~drawn].tolist()) == list(range(lo + t, w.L + t))
         assert len(set(gs.tolist())) == w.k
+
+
+def test_correlate_layers_overlap_and_distinct():
+    w = W.workload(2, num_requests=2, num_layers=3, k=64, window=8, carry=40, L=4096, B=128)
+    sel = W.selection_streams(w, steps=8)
+    out = W.correlate_layers(w, sel, 0.5, seed=1)
+    U, lo = w.units, w.L - w.window
+
+    def drawn(x):
+        return set(x[x < lo].tolist())
+
+    assert (out[:, :U] == sel[:, :U]).all()  # the first anchor is unchanged
+    common, steady_out, steady_in = [], [], []
+    for t in range(out.shape[0]):
+        for s in range(out.shape[1]):
+            cur, orig = out[t, s], sel[t, s]
+            assert len(set(cur.tolist())) == w.k and (cur >= 0).all()  # distinct, k entries
+            assert set(cur[cur >= lo].tolist()) == set(orig[orig >= lo].tolist())  # window kept
+            if s >= U:
+                common.append(len(drawn(cur) & drawn(out[t, s - U])))
+                if t:
+                    steady_out.append(len(drawn(cur) & drawn(out[t - 1, s])))
+                    steady_in.append(len(drawn(orig) & drawn(sel[t - 1, s])))
+    # about half of the drawn entries are shared with the previous layer (binomial spread)
+    assert 0.35 * (w.k - w.window) < np.mean(common) < 0.65 * (w.k - w.window)
+    # the step-to-step overlap of each layer is mostly kept
+    assert np.mean(steady_out) > 0.8 * np.mean(steady_in)
+    assert (W.correlate_layers(w, sel, 0.0) == sel).all()

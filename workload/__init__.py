@@ -193,6 +193,55 @@ def grow_streams(w: Workload, sel: np.ndarray) -> np.ndarray:
     return out
 
 
+def correlate_layers(w: Workload, sel: np.ndarray, rho: float, seed: int = 0) -> np.ndarray:
+    """Selections of adjacent layers that overlap within a step (the cross-layer locality that
+    a speculative hint from layer l to layer l+1 relies on), keeping each layer's overlap
+    across steps. For anchor i >= 1 a seeded mask marks a fraction rho of the positions below
+    the window [L - W, L) as taken from anchor i-1: at every step anchor i selects its own
+    window, anchor i-1's (already correlated) drawn entries at marked positions, and its own
+    drawn entries at unmarked positions; the count is brought back to k by dropping random
+    own entries or adding its own entries at marked positions (then random unselected
+    positions). The mask is fixed per layer, so entries that persist across steps in either
+    layer keep persisting. The set is emitted in shuffled order. sel: int32
+    [steps][anchors * units][k] without padding."""
+    out = np.array(sel, dtype=np.int32, copy=True)
+    if rho <= 0:
+        return out
+    rng = np.random.default_rng(seed)
+    U, lo, k = w.units, w.L - w.window, w.k
+    for i in range(1, out.shape[1] // U):
+        marked = rng.random(w.L) < rho
+        marked[lo:] = False
+        for t in range(out.shape[0]):
+            for u in range(U):
+                prev, own = out[t, (i - 1) * U + u], sel[t, i * U + u]
+                if (own < 0).any():
+                    raise ValueError("correlate_layers expects selections without padding")
+                win = own[own >= lo]
+                a = prev[(prev >= 0) & (prev < lo)]
+                a = a[marked[a]]
+                b = own[(own < lo) & ~marked[np.minimum(own, w.L - 1)]]
+                need = k - len(win)
+                if len(a) + len(b) > need:
+                    drop = len(a) + len(b) - need
+                    if drop <= len(b):
+                        b = np.delete(b, rng.choice(len(b), drop, replace=False))
+                    else:
+                        a = np.delete(a, rng.choice(len(a), drop - len(b), replace=False))
+                        b = b[:0]
+                fill = need - len(a) - len(b)
+                c = own[(own < lo) & marked[np.minimum(own, w.L - 1)]]
+                c = c[~np.isin(c, a)][:fill]
+                parts = [win, a, b, c]
+                short = fill - len(c)
+                if short > 0:
+                    used = np.concatenate(parts)
+                    pool = np.setdiff1d(np.arange(lo, dtype=np.int32), used)
+                    parts.append(rng.choice(pool, short, replace=False).astype(np.int32))
+                out[t, i * U + u] = rng.permutation(np.concatenate(parts))
+    return out
+
+
 def fill_kv(ptr: int, w: Workload, layer: int, unit0: int = 0, n_units: int | None = None,
             rec0: int = 0, n_rec: int | None = None, nthreads: int | None = None) -> None:
     """Write records [unit0, unit0+n_units) x [rec0, rec0+n_rec) of `layer` to raw memory `ptr`
