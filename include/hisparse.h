@@ -121,8 +121,14 @@ typedef struct {
   int32_t num_splits;            /* partitions of the token sequence reduced in a fixed order;
                                     0 = chosen from the shape alone */
   float scale;                   /* softmax scale applied to q.k */
-  int32_t reserved;              /* must be 0 */
+  int32_t flags;                 /* 0 or HISPARSE_ATTN_DEFER_MERGE */
 } hisparse_attn_desc_t;
+
+/* hisparse_attn_desc_t.flags: the attention call runs only its per-split workgroups (and any
+ * replay it carries) and leaves the splits' partial results in d_workspace without writing
+ * d_out; hisparse_attention_merge then writes d_out from them. For callers that schedule,
+ * overlap or time the two kernels apart. */
+#define HISPARSE_ATTN_DEFER_MERGE 1
 
 /* Human-readable name of a status code (static storage). */
 const char* hisparse_status_string(hisparse_status_t status);
@@ -325,6 +331,17 @@ hisparse_status_t hisparse_sparse_decode(hisparse_cache_t cache, int32_t layer, 
                                          const int32_t* d_slots, float* d_out,
                                          const hisparse_attn_desc_t* attn, void* d_workspace,
                                          size_t workspace_bytes, void* stream);
+
+/* [async] The merge of an attention call made with HISPARSE_ATTN_DEFER_MERGE: combines the
+ * per-split partial results in d_workspace into d_out (float32 [units][q_heads][d_v]), in
+ * the fixed split order, so deferred call + merge == the same call without the flag, bit for
+ * bit. units, top_k, record_bytes and attn (flags aside) must be those of the deferred call,
+ * whose `units` is the cache's units times the layer count for hisparse_sparse_decode_layers;
+ * the workspace must not be reused in between. */
+hisparse_status_t hisparse_attention_merge(int32_t units, int32_t top_k, int32_t record_bytes,
+                                           const hisparse_attn_desc_t* attn, float* d_out,
+                                           const void* d_workspace, size_t workspace_bytes,
+                                           void* stream);
 
 /* [async] hisparse_sparse_decode of `layer` and, in the same launch, the exact-prefetch replay
  * of `anchor_layer`'s latest plan into shared layers [first_shared, first_shared + num_shared)

@@ -140,7 +140,8 @@ hisparse_status_t hisparse_validate_desc(const hisparse_cache_desc_t* d) {
 hisparse_status_t hisparse_validate_attn(int32_t record_bytes, int32_t top_k,
                                          const hisparse_attn_desc_t* a) {
   if (!a) return HISPARSE_ERR_INVALID_ARG;
-  if (a->reserved != 0 || a->q_heads < 1 || a->q_heads > 256 || a->num_splits < 0)
+  if ((a->flags & ~HISPARSE_ATTN_DEFER_MERGE) != 0 || a->q_heads < 1 || a->q_heads > 256 ||
+      a->num_splits < 0)
     return HISPARSE_ERR_INVALID_ARG;
   if (top_k < 1 || top_k > kMaxTopK) return HISPARSE_ERR_INVALID_ARG;
   const int tpr = a->tokens_per_record;
@@ -619,6 +620,21 @@ hisparse_status_t hisparse_sparse_decode_pool(const void* d_pool, int64_t record
                                  records_per_unit, record_bytes, units, top_k,
                                  reinterpret_cast<const uint16_t*>(d_q), d_idx, d_out, d_workspace,
                                  as_stream(stream)) != hipSuccess)
+    return HISPARSE_ERR_HIP;
+  return HISPARSE_OK;
+}
+
+hisparse_status_t hisparse_attention_merge(int32_t units, int32_t top_k, int32_t record_bytes,
+                                           const hisparse_attn_desc_t* attn, float* d_out,
+                                           const void* d_workspace, size_t workspace_bytes,
+                                           void* stream) {
+  if (!d_out || !d_workspace) return HISPARSE_ERR_INVALID_ARG;
+  hisparse::AttnPlan p{};
+  hisparse_status_t st = hisparse::plan_attention(units, top_k, record_bytes, attn, &p);
+  if (st != HISPARSE_OK) return st;
+  if (workspace_bytes < p.workspace_bytes) return HISPARSE_ERR_INVALID_ARG;
+  if (hisparse::launch_merge(p, *attn, units, d_out, d_workspace, as_stream(stream)) !=
+      hipSuccess)
     return HISPARSE_ERR_HIP;
   return HISPARSE_OK;
 }

@@ -1023,16 +1023,28 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (attn.flags & HISPARSE_ATTN_DEFER_MERGE) return hipSuccess;
+  return launch_merge(p, attn, units, out, workspace, stream);
+}
+
+hipError_t launch_merge(const AttnPlan& p, const hisparse_attn_desc_t& attn, int32_t units,
+                        float* out, const void* workspace, hipStream_t stream) {
+  // the same workspace layout as launch_attention: partial outputs, then (max, sum) pairs
+  const int Hp = is_mla(attn) ? (attn.q_heads + 31) / 32 * 32 : attn.q_heads;
+  const size_t o_bytes = (size_t)units * p.n_parts * Hp * attn.d_v * sizeof(float);
+  const float* part_o = reinterpret_cast<const float*>(workspace);
+  const float2* part_ml = reinterpret_cast<const float2*>(
+      reinterpret_cast<const uint8_t*>(workspace) + ((o_bytes + 255) & ~(size_t)255));
   if (is_mla(attn)) {
-    const int nb = a.Hp / 32;
-    CombineMlaArgs c{a.part_o, a.part_ml, out, attn.q_heads, a.Hp, p.n_parts};
+    const int nb = Hp / 32;
+    CombineMlaArgs c{part_o, part_ml, out, attn.q_heads, Hp, p.n_parts};
     if ((int64_t)units * nb * 16 >= 2 * kTargetWorkgroups)
       hipLaunchKernelGGL(attn_combine_mla_kernel<1>, dim3(units * nb * 16), dim3(256), 0, stream, c);
     else
       hipLaunchKernelGGL(attn_combine_mla_kernel<4>, dim3(units * nb * 64), dim3(256), 0, stream, c);
     return hipGetLastError();
   }
-  CombineArgs c{a.part_o, a.part_ml, out, attn.q_heads, p.n_parts, units * attn.q_heads};
+  CombineArgs c{part_o, part_ml, out, attn.q_heads, p.n_parts, units * attn.q_heads};
   const int n_cwg = (units * attn.q_heads + 3) / 4;
   hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(n_cwg), dim3(256), 0, stream, c);
   return hipGetLastError();

@@ -104,6 +104,10 @@ struct AttnPlan {
 };
 hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_bytes,
                                  const hisparse_attn_desc_t* attn, AttnPlan* plan);
+// The merge of the per-split partials in `workspace` into out (skipped by launch_attention
+// when attn.flags has HISPARSE_ATTN_DEFER_MERGE).
+hipError_t launch_merge(const AttnPlan& p, const hisparse_attn_desc_t& attn, int32_t units,
+                        float* out, const void* workspace, hipStream_t stream);
 hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
                             const uint8_t* pool, int64_t records_per_unit, int32_t record_bytes,
                             int32_t units, int32_t top_k, const uint16_t* q, const int32_t* idx,

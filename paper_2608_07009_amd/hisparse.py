@@ -28,6 +28,8 @@ HISPARSE_FETCH_ZERO_COPY = 0
 HISPARSE_FETCH_SDMA = 1
 HISPARSE_FETCH_NONE = 2
 
+HISPARSE_ATTN_DEFER_MERGE = 1
+
 HISPARSE_HOST_COHERENT = 0
 HISPARSE_HOST_NONCOHERENT = 1
 HISPARSE_HOST_UNCACHED = 2
@@ -41,6 +43,7 @@ EXPORTED = (
     "hisparse_prefetch_layers", "hisparse_append", "hisparse_request_acquire",
     "hisparse_request_release", "hisparse_reset_units", "hisparse_stage", "hisparse_speculate",
     "hisparse_decode_workspace_bytes", "hisparse_sparse_decode", "hisparse_sparse_decode_layers",
+    "hisparse_attention_merge",
     "hisparse_sparse_decode_prefetch",
     "hisparse_sparse_decode_pool",
     "hisparse_read_state", "hisparse_read_plan", "hisparse_check_errors",
@@ -60,7 +63,7 @@ class AttnDesc(ctypes.Structure):
     _fields_ = [("q_heads", ctypes.c_int32), ("d_qk", ctypes.c_int32), ("d_v", ctypes.c_int32),
                 ("v_offset", ctypes.c_int32), ("tokens_per_record", ctypes.c_int32),
                 ("num_splits", ctypes.c_int32), ("scale", ctypes.c_float),
-                ("reserved", ctypes.c_int32)]
+                ("flags", ctypes.c_int32)]
 
 
 class HisparseError(RuntimeError):
@@ -111,6 +114,8 @@ def lib() -> ctypes.CDLL:
                                                                   ctypes.POINTER(AttnDesc)]),
             "hisparse_sparse_decode": (_I32, [_V, _I32, _V, _V, _V, ctypes.POINTER(AttnDesc), _V,
                                               ctypes.c_size_t, _V]),
+            "hisparse_attention_merge": (_I32, [_I32, _I32, _I32, ctypes.POINTER(AttnDesc), _V,
+                                                _V, ctypes.c_size_t, _V]),
             "hisparse_sparse_decode_layers": (_I32, [_V, _I32, _I32, _V, _V, _V,
                                                      ctypes.POINTER(AttnDesc), _V,
                                                      ctypes.c_size_t, _V]),
@@ -284,6 +289,14 @@ def hisparse_sparse_decode(cache: int, layer: int, d_q, d_slots, d_out, attn: At
            lib().hisparse_sparse_decode(cache, layer, _p(d_q), _p(d_slots), _p(d_out),
                                         ctypes.byref(attn), _p(d_workspace), workspace_bytes,
                                         _s(stream)))
+
+
+def hisparse_attention_merge(units: int, top_k: int, record_bytes: int, attn: AttnDesc, d_out,
+                             d_workspace, workspace_bytes: int, stream=None) -> None:
+    _check("hisparse_attention_merge",
+           lib().hisparse_attention_merge(units, top_k, record_bytes, ctypes.byref(attn),
+                                          _p(d_out), _p(d_workspace), workspace_bytes,
+                                          _s(stream)))
 
 
 def hisparse_sparse_decode_layers(cache: int, first_layer: int, num_layers: int, q, slots, out,

@@ -74,15 +74,27 @@ def test_invalid_descriptors(field, value, status):
     (dict(q_heads=0), hs.HISPARSE_ERR_INVALID_ARG),
     (dict(scale=0.0), hs.HISPARSE_ERR_INVALID_ARG),
     (dict(num_splits=-1), hs.HISPARSE_ERR_INVALID_ARG),
-    (dict(reserved=2), hs.HISPARSE_ERR_INVALID_ARG),
+    (dict(flags=2), hs.HISPARSE_ERR_INVALID_ARG),
 ])
 def test_invalid_attention_descriptors(change, status):
     w = W.workload(2)
     d = dict(q_heads=w.q_heads, d_qk=w.d_qk, d_v=w.d_v, v_offset=w.v_offset,
-             tokens_per_record=w.tokens_per_record, num_splits=0, scale=w.scale, reserved=0)
+             tokens_per_record=w.tokens_per_record, num_splits=0, scale=w.scale, flags=0)
     d.update(change)
     assert hs.hisparse_validate_attn(w.record_bytes, w.k, hs.AttnDesc(**d)) == status
     assert hs.hisparse_decode_workspace_bytes(w.units, w.k, w.record_bytes, hs.AttnDesc(**d)) == 0
+
+
+def test_deferred_merge_flag_is_valid():
+    w = W.workload(2)
+    base = hs.AttnDesc(w.q_heads, w.d_qk, w.d_v, w.v_offset, w.tokens_per_record, 0, w.scale, 0)
+    d = hs.AttnDesc(w.q_heads, w.d_qk, w.d_v, w.v_offset, w.tokens_per_record, 0, w.scale,
+                    hs.HISPARSE_ATTN_DEFER_MERGE)
+    assert hs.hisparse_validate_attn(w.record_bytes, w.k, d) == hs.HISPARSE_OK
+    n = hs.hisparse_decode_workspace_bytes(w.units, w.k, w.record_bytes, d)
+    assert n > 0 and n == hs.hisparse_decode_workspace_bytes(w.units, w.k, w.record_bytes, base)
+    with pytest.raises(hs.HisparseError):  # null output / workspace: rejected on the host
+        hs.hisparse_attention_merge(w.units, w.k, w.record_bytes, d, None, None, n)
 
 
 def test_record_too_small_for_attention():

@@ -287,3 +287,53 @@ def test_decode_prefetch_equals_separate(cfg, fetch):
         torch.cuda.synchronize()
         fused.close()
         apart.close()
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_deferred_merge_equals_fused(cfg):
+    """HISPARSE_ATTN_DEFER_MERGE + hisparse_attention_merge gives bit-identical outputs to the
+    fused call for one layer, a replay-carrying layer and a batched group of layers, for the
+    latent (MLA) and the grouped-query kernels."""
+    G = 4
+    w = W.workload(cfg, num_layers=G, share_group=G, num_requests=2)
+    log(f"test_deferred_merge_equals_fused {w.name}")
+    run = Run(w, 2)
+    try:
+        U, k, H, R, dev = w.units, w.k, w.q_heads, w.record_bytes, run.dev
+        h = run.cache.handle
+        hs.hisparse_resolve(h, 0, run.sel_ptr(0, 0), run.slots[0], run.counts[0], run.stream)
+        ad = attn_desc(w)
+        adf = attn_desc(w)
+        adf.flags = hs.HISPARSE_ATTN_DEFER_MERGE
+        nb = max(hs.hisparse_decode_workspace_bytes(n, k, R, ad) for n in (U, G * U))
+        ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+        q = torch.from_numpy(np.stack([W.queries(w, 0, l) for l in range(G)]).view(np.int16)).to(dev)
+        fused = torch.empty((G, U, H, w.d_v), dtype=torch.float32, device=dev)
+        deferred = torch.full_like(fused, float("nan"))
+        # one layer
+        hs.hisparse_sparse_decode(h, 0, q[0], run.slots[0], fused[0], ad, ws, nb, run.stream)
+        hs.hisparse_sparse_decode(h, 0, q[0], run.slots[0], deferred[0], adf, ws, nb, run.stream)
+        torch.cuda.synchronize()
+        assert torch.isnan(deferred[0]).all()  # the deferred call leaves the output alone
+        hs.hisparse_attention_merge(U, k, R, adf, deferred[0], ws, nb, run.stream)
+        # attention of layer 0 carrying the replay into layers 1..3 (idempotent: same plan)
+        hs.hisparse_sparse_decode_prefetch(h, 0, q[0], run.slots[0], fused[1], ad, ws, nb, 0, 1,
+                                           G - 1, run.stream)
+        hs.hisparse_sparse_decode_prefetch(h, 0, q[0], run.slots[0], deferred[1], adf, ws, nb, 0,
+                                           1, G - 1, run.stream)
+        hs.hisparse_attention_merge(U, k, R, adf, deferred[1], ws, nb, run.stream)
+        torch.cuda.synchronize()
+        assert torch.equal(fused[:2], deferred[:2])
+        assert torch.equal(fused[0], fused[1])
+        # the whole group in one launch: units = G * U
+        f_all, d_all = torch.empty_like(fused), torch.full_like(fused, float("nan"))
+        hs.hisparse_sparse_decode_layers(h, 0, G, q, run.slots[0], f_all, ad, ws, nb, run.stream)
+        hs.hisparse_sparse_decode_layers(h, 0, G, q, run.slots[0], d_all, adf, ws, nb, run.stream)
+        hs.hisparse_attention_merge(G * U, k, R, adf, d_all, ws, nb, run.stream)
+        torch.cuda.synchronize()
+        assert torch.equal(f_all, d_all)  # (its split plan is that of G * U units)
+        with pytest.raises(hs.HisparseError):  # workspace smaller than the plan needs
+            hs.hisparse_attention_merge(G * U, k, R, adf, d_all, ws, 256, run.stream)
+    finally:
+        torch.cuda.synchronize()
+        run.close()
