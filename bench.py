@@ -124,8 +124,12 @@ class Hip:
         self.L = L
 
     def event(self, timing: bool = True) -> int:
+        """A timing event (hipEventDisableSystemFence: no system-scope cache writeback when it
+        is recorded, so a span around a kernel measures the kernel, not the fence; the host
+        reads it only after a device synchronisation), or a synchronisation-only event
+        (hipEventDisableTiming)."""
         e = ctypes.c_void_p()
-        rc = self.L.hipEventCreateWithFlags(ctypes.byref(e), 0 if timing else 0x2)
+        rc = self.L.hipEventCreateWithFlags(ctypes.byref(e), 0x20000000 if timing else 0x2)
         if rc != 0:
             raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
         return e.value
@@ -173,10 +177,14 @@ def traffic_record(workload: str, kernel: str):
             kv = dict(f.split("=", 1) for f in line.split()[1:])
             if kv.get("workload") != workload or kv.get("kernel") != kernel:
                 continue
-            src = os.path.join(ROOT, kv["source"])
-            if not os.path.exists(src):
+            # source=a[,b...]: the kernel's source files; sha256 over their bytes in that order
+            srcs = [os.path.join(ROOT, x) for x in kv["source"].split(",")]
+            if not all(os.path.exists(x) for x in srcs):
                 continue
-            if hashlib.sha256(open(src, "rb").read()).hexdigest() != kv.get("sha256"):
+            h = hashlib.sha256()
+            for x in srcs:
+                h.update(open(x, "rb").read())
+            if h.hexdigest() != kv.get("sha256"):
                 continue  # the kernel changed since the counters were taken
             return {"fetch_bytes": int(kv["fetch_bytes"]), "write_bytes": int(kv["write_bytes"]),
                     "profile": os.path.relpath(path, ROOT)}
@@ -840,8 +848,13 @@ def main() -> int:
         kd = kernels.get(dom)
     if dom in ("fetch", "prefetch_replay", "fetch_group", "sparse_decode_prefetch"):
         tr = traffic_record(w.name, dom)
+        # HBM-side algorithmic bytes of one launch: the records moved (read over the link,
+        # written to HBM), plus, for a launch that also attends, the attention's own bytes
+        hbm_alg = kd["bytes_per_launch"] + (att_bytes_call if dom == "sparse_decode_prefetch"
+                                            else 0)
         if tr:
-            tr["read_vs_algorithmic"] = tr["fetch_bytes"] / kd["bytes_per_launch"]
+            tr["algorithmic_hbm_bytes_per_launch"] = hbm_alg
+            tr["read_vs_algorithmic"] = tr["fetch_bytes"] / hbm_alg
             tr["write_vs_algorithmic"] = tr["write_bytes"] / kd["bytes_per_launch"]
         roof = {"kernel": dom, "bound": "host_link", "achieved": kd["GBps"],
                 "peak": PCIE_PEAK_GBPS, "unit": "GB/s", "frac": kd["GBps"] / PCIE_PEAK_GBPS,
