@@ -674,13 +674,13 @@ def main() -> int:
         for e in ev_w or []:
             hip.L.hipEventDestroy(e)
 
-    # Kernel-span pass: the K steps are enqueued behind a bounded GPU delay (torch's clock
-    # spin), so the host is ahead of the GPU for the whole pass and each event pair brackets
-    # its kernel, not a host launch gap. Its GPU time per step is reported beside the timed
-    # region's. With several micro-batches the spans of concurrent kernels overlap: each span
-    # is that kernel's duration while sharing the GPU.
+    # Kernel-span pass: every step is enqueued behind a bounded GPU delay (torch's clock spin)
+    # and drained before the next, so the host is ahead of the GPU for the whole step and each
+    # event pair brackets its kernel, not a host launch gap. Its GPU time per step (without
+    # the overlap of consecutive steps) is reported beside the timed region's. With several
+    # micro-batches the spans of concurrent kernels overlap: each span is that kernel's
+    # duration while sharing the GPU.
     events = [hip.event() for _ in range(per_step_events * args.steps)]
-    ref, end = hip.event(), hip.event()
     spans = []
     cal0, cal1 = hip.event(), hip.event()
     rec(cal0, root_s)
@@ -688,15 +688,22 @@ def main() -> int:
     rec(cal1, root_s)
     torch.cuda.synchronize()
     cycles_per_ms = 1_000_000 / max(1e-3, hip.ms(cal0, cal1))
-    delay_ms = min(4000.0, 3.0 * host_ms * args.steps + 20.0)
-    log(f"host enqueue {host_ms:.2f} ms per step with span events; GPU held {delay_ms:.0f} ms")
-    torch.cuda._sleep(int(delay_ms * cycles_per_ms))
-    rec(ref, root_s)
+    # each step is enqueued behind its own GPU hold and then drained, so the host is ahead of
+    # the GPU for the whole step and never blocks on a full command queue meanwhile
+    hold_ms = 3.0 * host_ms + 1.0
+    log(f"host enqueue {host_ms:.2f} ms per step with span events; GPU held {hold_ms:.1f} ms "
+        f"before each step of the span pass")
+    step_refs = []  # (start event, end event, index of the step's first span)
     for t in range(args.warmup, steps_needed):
+        r0, r1 = hip.event(), hip.event()
+        torch.cuda._sleep(int(hold_ms * cycles_per_ms))
+        rec(r0, root_s)
+        first = len(spans)
         step(t, events, spans)
-    rec(end, root_s)
-    torch.cuda.synchronize()
-    eager_gpu_ms = hip.ms(ref, end) / args.steps
+        rec(r1, root_s)
+        torch.cuda.synchronize()
+        step_refs.append((r0, r1, first))
+    eager_gpu_ms = sum(hip.ms(r0, r1) for r0, r1, _ in step_refs) / args.steps
     # slot vectors and attention outputs of the last step, to check the graph replays against
     eager_final = [(mb.slots.clone(), out[:, mb.u0:mb.u0 + mb.U].clone()) for mb in mbs]
     for mb in mbs:
@@ -706,20 +713,27 @@ def main() -> int:
             return 1
 
     tot = {}
-    io_intervals = []
-    for name, e0, e1 in spans:
-        d = hip.ms(e0, e1) * 1e-3
-        t_sum, n = tot.get(name, (0.0, 0))
-        tot[name] = (t_sum + d, n + 1)
-        if name in ("fetch", "prefetch_replay", "fetch_group", "sparse_decode_prefetch",
-                    "speculate"):
-            io_intervals.append((hip.ms(ref, e0) * 1e-3, hip.ms(ref, e1) * 1e-3))
+    io_busy = 0.0  # seconds in which some host-link transfer kernel ran, summed over the steps
+    for si, (r0, _, first) in enumerate(step_refs):
+        last = step_refs[si + 1][2] if si + 1 < len(step_refs) else len(spans)
+        io_intervals = []
+        for name, e0, e1 in spans[first:last]:
+            d = hip.ms(e0, e1) * 1e-3
+            t_sum, n = tot.get(name, (0.0, 0))
+            tot[name] = (t_sum + d, n + 1)
+            if name in ("fetch", "prefetch_replay", "fetch_group", "sparse_decode_prefetch",
+                        "speculate"):
+                io_intervals.append((hip.ms(r0, e0) * 1e-3, hip.ms(r0, e1) * 1e-3))
+        io_busy += union_length(io_intervals)
     for e in events:
         hip.L.hipEventDestroy(e)
     for _, e0, e1 in spans:
         hip.L.hipEventDestroy(e0)
         hip.L.hipEventDestroy(e1)
-    for e in (ref, end, cal0, cal1):
+    for r0, r1, _ in step_refs:
+        hip.L.hipEventDestroy(r0)
+        hip.L.hipEventDestroy(r1)
+    for e in (cal0, cal1):
         hip.L.hipEventDestroy(e)
 
     # [K][layers][units][2] over all micro-batches (units in global order)
@@ -878,7 +892,6 @@ def main() -> int:
         roof = {"kernel": dom, "bound": "hbm", "achieved": kd["hbm_GBps"], "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": kd["hbm_GBps"] / HBM_PEAK_GBPS, "traffic": None}
 
-    io_busy = union_length(io_intervals)
     miss_gbps = ((fetch_bytes + replay_bytes + group_bytes + carried_bytes + spec_bytes)
                  / io_busy / 1e9
                  if (io_busy and moves_data) else None)
