@@ -712,18 +712,38 @@ def main() -> int:
             print(json.dumps({"error": f"device-side selection error {info}"}))
             return 1
 
-    tot = {}
-    io_busy = 0.0  # seconds in which some host-link transfer kernel ran, summed over the steps
+    # Span statistics over the steps without a stall: now and then one transfer kernel takes
+    # tens of milliseconds instead of ~0.1 (the device stalls outside this program), and one
+    # such span would dominate an average, so a step that holds a span longer than 4x the
+    # median of its kind is left out of the span-derived figures (kernel averages, rates);
+    # the timed region above is unaffected and covers every step.
+    IO_KINDS = ("fetch", "prefetch_replay", "fetch_group", "sparse_decode_prefetch",
+                "speculate")
+    step_spans = []
     for si, (r0, _, first) in enumerate(step_refs):
         last = step_refs[si + 1][2] if si + 1 < len(step_refs) else len(spans)
+        step_spans.append([(name, hip.ms(e0, e1) * 1e-3, hip.ms(r0, e0) * 1e-3,
+                            hip.ms(r0, e1) * 1e-3) for name, e0, e1 in spans[first:last]])
+    by_kind = {}
+    for sp in step_spans:
+        for name, d, _, _ in sp:
+            by_kind.setdefault(name, []).append(d)
+    med = {name: float(np.median(v)) for name, v in by_kind.items()}
+    kept = [si for si, sp in enumerate(step_spans)
+            if all(d <= 4.0 * med[name] for name, d, _, _ in sp)]
+    stalled = [si for si in range(len(step_spans)) if si not in kept]
+    if stalled:
+        log(f"span pass: {len(stalled)} step(s) with a stalled span left out of the span "
+            f"statistics (longest span {max(d for si in stalled for _, d, _, _ in step_spans[si]) * 1e3:.1f} ms)")
+    tot = {}
+    io_busy = 0.0  # seconds in which some host-link transfer kernel ran, summed over the steps
+    for si in kept:
         io_intervals = []
-        for name, e0, e1 in spans[first:last]:
-            d = hip.ms(e0, e1) * 1e-3
+        for name, d, t0, t1 in step_spans[si]:
             t_sum, n = tot.get(name, (0.0, 0))
             tot[name] = (t_sum + d, n + 1)
-            if name in ("fetch", "prefetch_replay", "fetch_group", "sparse_decode_prefetch",
-                        "speculate"):
-                io_intervals.append((hip.ms(r0, e0) * 1e-3, hip.ms(r0, e1) * 1e-3))
+            if name in IO_KINDS:
+                io_intervals.append((t0, t1))
         io_busy += union_length(io_intervals)
     for e in events:
         hip.L.hipEventDestroy(e)
@@ -738,10 +758,11 @@ def main() -> int:
 
     # [K][layers][units][2] over all micro-batches (units in global order)
     c = np.concatenate([mb.counts[args.warmup:steps_needed].cpu().numpy() for mb in mbs],
-                       axis=2).astype(np.int64)
+                       axis=2).astype(np.int64)[kept]
     K = args.steps
+    Ks = len(kept)  # steps behind the span statistics
     U = U_all // n_mb  # units of one launch
-    anchor_calls = K * len(w.anchors)
+    anchor_calls = Ks * len(w.anchors)
     misses_anchor = int(c[:, w.anchors, :, 1].sum())
     hits_anchor = int(c[:, w.anchors, :, 0].sum())
     R = w.record_bytes
@@ -758,7 +779,7 @@ def main() -> int:
     # batched schedule: one attention launch per group; attention is accounted per layer call
     t_lay, n_lay = kernel("sparse_decode_layers")
     grouped = [(a, sh) for a, sh in groups if sh and args.schedule in ("serial", "batched")]
-    lay_calls = K * n_mb * sum(1 + len(sh) for _, sh in grouped) if n_lay else 0
+    lay_calls = Ks * n_mb * sum(1 + len(sh) for _, sh in grouped) if n_lay else 0
     t_pf, n_pf = kernel("sparse_decode_prefetch")  # attention carrying a replay
     t_att_one, n_att_one = t_att, n_att
     t_att, n_att = t_att + t_lay + t_pf, n_att + lay_calls + n_pf
@@ -797,7 +818,7 @@ def main() -> int:
                                       "GBps": replay_bytes / t_rep / 1e9}
     t_app, n_app = kernel("append")
     if n_app:
-        app_bytes = K * w.num_layers * U_all * R  # one record per layer and unit per step
+        app_bytes = Ks * w.num_layers * U_all * R  # one record per layer and unit per step
         kernels["append"] = {
             "launches": n_app, "avg_us": t_app / n_app * 1e6,
             "write_through_bytes_per_launch": app_bytes / n_app if moves_data else 0,
@@ -814,7 +835,7 @@ def main() -> int:
     spec_bytes = 0
     if n_spc:
         sc = np.concatenate([mb.spec_counts[args.warmup:steps_needed].cpu().numpy()
-                             for mb in mbs], axis=2).astype(np.int64)
+                             for mb in mbs], axis=2).astype(np.int64)[kept]
         spec_bytes = int(sc[..., 1].sum()) * R if moves_data else 0
         kernels["speculate"] = {
             "launches": n_spc, "avg_us": t_spc / n_spc * 1e6,
@@ -1039,6 +1060,7 @@ def main() -> int:
         "kernels": kernels,
         "roofline": roof,
         "eager_gpu_ms_per_step": eager_gpu_ms,
+        "span_steps": Ks, "span_steps_with_stall": len(stalled),
         "hbm_footprint_GiB": (w0.num_layers * U_all * w.B * R) / 2**30,
     }
     if staging is not None:
