@@ -715,7 +715,8 @@ def main() -> int:
     # Span statistics over the steps without a stall: now and then one transfer kernel takes
     # tens of milliseconds instead of ~0.1 (the device stalls outside this program), and one
     # such span would dominate an average, so a step that holds a span longer than 4x the
-    # median of its kind is left out of the span-derived figures (kernel averages, rates);
+    # median of its kind (and 0.5 ms beyond it) is left out of the span-derived figures
+    # (kernel averages, rates);
     # the timed region above is unaffected and covers every step.
     IO_KINDS = ("fetch", "prefetch_replay", "fetch_group", "sparse_decode_prefetch",
                 "speculate")
@@ -730,11 +731,11 @@ def main() -> int:
             by_kind.setdefault(name, []).append(d)
     med = {name: float(np.median(v)) for name, v in by_kind.items()}
     kept = [si for si, sp in enumerate(step_spans)
-            if all(d <= 4.0 * med[name] for name, d, _, _ in sp)]
+            if all(d <= max(4.0 * med[name], med[name] + 5e-4) for name, d, _, _ in sp)]
     stalled = [si for si in range(len(step_spans)) if si not in kept]
     if stalled:
         log(f"span pass: {len(stalled)} step(s) with a stalled span left out of the span "
-            f"statistics (longest span {max(d for si in stalled for _, d, _, _ in step_spans[si]) * 1e3:.1f} ms)")
+            f"statistics (longest span {max(d for si in stalled for _, d, _, _ in step_spans[si]) * 1e3:.3f} ms)")
     tot = {}
     io_busy = 0.0  # seconds in which some host-link transfer kernel ran, summed over the steps
     for si in kept:
