@@ -54,7 +54,7 @@ typedef enum {
   HISPARSE_ERR_INVALID_ARG = -1,   /* bad descriptor, layer index, pointer or size */
   HISPARSE_ERR_OOM = -2,           /* device or pinned host allocation failed */
   HISPARSE_ERR_HIP = -3,           /* a HIP runtime call failed */
-  HISPARSE_ERR_UNSUPPORTED = -4,   /* valid request this build does not implement */
+  HISPARSE_ERR_UNSUPPORTED = -4,   /* valid request the library does not implement */
   HISPARSE_ERR_BAD_SELECTION = -5, /* latched device-side selection error (see above) */
   HISPARSE_ERR_FULL = -6           /* every request slot is taken (hisparse_request_acquire) */
 } hisparse_status_t;

@@ -104,7 +104,7 @@ def test_record_too_small_for_attention():
 
 def test_status_strings():
     for code, name in [(0, "HISPARSE_OK"), (-1, "HISPARSE_ERR_INVALID_ARG"),
-                       (-5, "HISPARSE_ERR_BAD_SELECTION")]:
+                       (-5, "HISPARSE_ERR_BAD_SELECTION"), (-6, "HISPARSE_ERR_FULL")]:
         assert hs.hisparse_status_string(code) == name
 
 
@@ -122,3 +122,23 @@ def test_loads_in_a_process_that_imported_torch_first():
     root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
     code = "import torch; from paper_2608_07009_amd import hisparse as hs; hs.lib()"
     subprocess.check_call([sys.executable, "-c", code], cwd=root)
+
+
+def test_entry_points_reject_a_null_handle_on_the_host():
+    """Every handle-taking call validates its arguments before any GPU work (no device here)."""
+    L = hs.lib()
+    dummy = ctypes.c_void_p(16)  # never dereferenced: the null handle is rejected first
+    r = ctypes.c_int32()
+    calls = [
+        lambda: L.hisparse_request_acquire(None, ctypes.byref(r)),
+        lambda: L.hisparse_request_release(None, 0, None),
+        lambda: L.hisparse_reset_units(None, 0, 1, None),
+        lambda: L.hisparse_stage(None, 0, 1, 0, 1, 0, 1, dummy, 0, None),
+        lambda: L.hisparse_speculate(None, 0, dummy, None, None),
+        lambda: L.hisparse_append(None, 0, 1, dummy, dummy, dummy, None),
+        lambda: L.hisparse_resolve(None, 0, dummy, dummy, None, None),
+        lambda: L.hisparse_prefetch_layer(None, 0, 1, None),
+        lambda: L.hisparse_reset(None, None),
+    ]
+    for call in calls:
+        assert call() == hs.HISPARSE_ERR_INVALID_ARG
