@@ -46,6 +46,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--requests", type=int, default=0, metavar="N",
+                    help="run the workload with N requests instead of its own count (a batch "
+                         "scan; every other shape is the workload's)")
     ap.add_argument("--fetch", choices=["zero_copy", "none", "sdma"], default="zero_copy")
     ap.add_argument("--host-memory", choices=["coherent", "noncoherent", "uncached"],
                     default="coherent")
@@ -388,6 +391,9 @@ def main() -> int:
         return resolve_sweep(args, torch, hs, W, HiSparseCache)
     hip = Hip()
     w0 = W.workload(args.config)
+    if args.requests > 0:  # a different workload: its own name (no profile record applies)
+        w0 = dataclasses.replace(w0, num_requests=args.requests,
+                                 name=f"{w0.name}_with_{args.requests}_requests")
     w = W.fit_pinned(w0)
     steps_needed = args.warmup + args.steps
     if steps_needed > w.steps:
