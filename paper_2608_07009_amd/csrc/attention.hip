@@ -930,11 +930,18 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
   if (attn->num_splits > 0) {
     splits = std::min(attn->num_splits, max_splits);
   } else {
-    // about one workgroup per CU, but at least four chunks per token group (two for latent
-    // attention) in every split so the load pipeline reaches steady state
+    // at most one workgroup per CU (a workgroup holds a CU's LDS, so one more would wait for a
+    // second round), and enough chunks per split for the load pipeline to reach steady state.
+    // For latent attention the split partials (fp32, 2 KB per head and split) grow with the
+    // splits, and measured over 1..32 units of 128 heads, longer splits win as the grid gets
+    // more workgroup columns: 2 chunks per split up to 4 columns, 4 up to 16, 8 beyond (12
+    // units: 39 against 55 us with 22 two-chunk splits). At 16 columns 8-chunk splits are 7%
+    // faster alone but a third slower beside a concurrent host-link fetch (half the
+    // workgroups, each twice as long), the case of two micro-batches taking turns.
     const int per_split = units * p.hb;
-    splits = (kTargetWorkgroups + per_split - 1) / per_split;
-    int chunks_per_split = is_mla(*attn) ? 2 : 4;
+    splits = std::max(1, kTargetWorkgroups / per_split);
+    int chunks_per_split = 4;
+    if (is_mla(*attn)) chunks_per_split = per_split <= 4 ? 2 : (per_split <= 16 ? 4 : 8);
     // a call too small to give even 64 such workgroups is all latency: one chunk per split
     if (is_mla(*attn) && (int64_t)per_split * (p.n_tok / (2 * chunk)) < 64) chunks_per_split = 1;
     const int min_work_splits = std::max(1, p.n_tok / (chunks_per_split * chunk));
