@@ -88,7 +88,9 @@ typedef struct {
   int32_t units_per_request;     /* 1 (token-level) or kv heads (block/page selection) */
   int32_t capacity;              /* B: slots per unit; top_k <= B <= 16384 */
   int64_t num_records;           /* L: records per unit, 1 .. 2^31-1 */
-  int32_t top_k;                 /* k: 1 .. 4096 */
+  int32_t top_k;                 /* k: 1 .. 4096. The resolve kernel takes 16 * round_up(k, 4)
+                                    + B / 4 + 8192 bytes of LDS (at most 76 KiB); create returns
+                                    UNSUPPORTED on a device whose workgroups get less */
   int32_t record_bytes;          /* R: multiple of 16, 16 .. 1 MiB */
   int32_t share_group;           /* G >= 1: layers with layer % G == 0 are anchors that resolve;
                                     layer l with l % G != 0 shares the selection of anchor

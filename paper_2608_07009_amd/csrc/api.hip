@@ -12,6 +12,10 @@ using hisparse::kMaxCapacity;
 using hisparse::kMaxRecordBytes;
 using hisparse::kMaxTopK;
 
+// Dynamic LDS the resolve kernel may take: a gfx950 workgroup's 160 KiB less 256 bytes for the
+// kernel's own scan scratch.
+constexpr size_t kMaxResolveLds = 160 * 1024 - 256;
+
 namespace {
 
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
@@ -130,7 +134,8 @@ hisparse_status_t hisparse_validate_desc(const hisparse_cache_desc_t* d) {
     return HISPARSE_ERR_INVALID_ARG;
   if (d->fetch_workgroups < 0 || d->fetch_workgroups > 4096) return HISPARSE_ERR_INVALID_ARG;
   // the resolve kernel keeps the sorted misses, the slot outputs and two slot bitmaps in LDS
-  if (hisparse::resolve_lds_bytes(d->top_k, d->capacity) > 64 * 1024)
+  // (dynamic), beside a few hundred bytes of its own: at most a gfx950 workgroup's 160 KiB
+  if (hisparse::resolve_lds_bytes(d->top_k, d->capacity) > kMaxResolveLds)
     return HISPARSE_ERR_INVALID_ARG;
   // per-unit host pool and cache offsets must fit comfortably in 64-bit byte offsets
   if ((double)d->num_records * d->record_bytes * units > 4.0e18) return HISPARSE_ERR_INVALID_ARG;
@@ -169,6 +174,13 @@ hisparse_status_t hisparse_cache_create(const hisparse_cache_desc_t* desc, int32
     (void)hipGetLastError();
     return HISPARSE_ERR_INVALID_ARG;
   }
+  // the resolve kernel's LDS must also fit what this device grants one workgroup
+  int max_lds = 0;
+  if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, device) !=
+      hipSuccess)
+    return HISPARSE_ERR_HIP;
+  if (hisparse::resolve_lds_bytes(desc->top_k, desc->capacity) + 256 > (size_t)max_lds)
+    return HISPARSE_ERR_UNSUPPORTED;
   int prev = 0;
   (void)hipGetDevice(&prev);
   if (hipSetDevice(device) != hipSuccess) return HISPARSE_ERR_HIP;

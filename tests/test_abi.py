@@ -142,3 +142,12 @@ def test_entry_points_reject_a_null_handle_on_the_host():
     ]
     for call in calls:
         assert call() == hs.HISPARSE_ERR_INVALID_ARG
+
+
+def test_largest_topk_and_capacity_are_valid():
+    w = W.workload(2)
+    assert hs.hisparse_validate_desc(desc_for(w, top_k=4096, capacity=16384)) == hs.HISPARSE_OK
+    assert hs.hisparse_validate_desc(desc_for(w, top_k=4097, capacity=16384)) == \
+        hs.HISPARSE_ERR_INVALID_ARG
+    assert hs.hisparse_validate_desc(desc_for(w, top_k=4096, capacity=16385)) == \
+        hs.HISPARSE_ERR_INVALID_ARG
