@@ -5,7 +5,8 @@
     oracle, bit-exact, and every resident slot holding its record;
   * the smallest record (16 B, one transfer block) and a large one (64 KiB): resident bytes;
   * the widest latent attention (256 heads) over the largest top-k: the cache path equals the
-    fully resident path bit for bit and the oracle within tolerance on sampled heads.
+    fully resident path bit for bit and the oracle within tolerance on sampled heads;
+  * the degenerate cache sizes B = k and B = L, with their closed forms.
 """
 import dataclasses
 
@@ -151,6 +152,50 @@ def test_attention_widest_mla_at_maximum_topk():
         err, rl2 = np.abs(o - ref).max(), float(np.linalg.norm(o - ref) / np.linalg.norm(ref))
         log(f"  max-abs {err:.2e} rel-L2 {rl2:.2e}")
         assert err <= MAX_ABS and rl2 <= REL_L2
+    finally:
+        torch.cuda.synchronize()
+        cache.close()
+
+
+@pytest.mark.parametrize("B,L", [(128, 4096), (512, 512)])
+def test_resolve_degenerate_cache_sizes(B, L):
+    """B = k: the cache holds exactly the step's selection (every non-selected record is
+    evicted at once); B = L: nothing is ever evicted. Bit-exact against the oracle, with the
+    closed forms of both cases checked on the GPU's own counts."""
+    U, k, R, steps = 3, 128, 32, 12
+    log(f"test_resolve_degenerate_cache_sizes B={B} L={L} k={k}")
+    rng = np.random.default_rng(94 + B)
+    sel = carried_stream(rng, steps, U, L, k, keep=0.6)
+    cache = HiSparseCache(num_requests=U, num_layers=1, units_per_request=1, capacity=B,
+                          num_records=L, top_k=k, record_bytes=R)
+    try:
+        host = cache.host_view(0)
+        host[:] = rng.integers(0, 256, size=host.shape, dtype=np.uint8)
+        dev = torch.device("cuda:0")
+        sel_d = torch.from_numpy(sel).to(dev)
+        slots = torch.empty((U, k), dtype=torch.int32, device=dev)
+        counts = torch.empty((U, 2), dtype=torch.int32, device=dev)
+        orc = oracle.OracleCache(U, L, B, k)
+        seen = [set() for _ in range(U)]
+        for t in range(steps):
+            hs.hisparse_resolve(cache.handle, 0, sel_d[t], slots, counts,
+                                torch.cuda.current_stream())
+            torch.cuda.synchronize()
+            e_slots, e_counts, _, _, _ = orc.resolve(sel[t])
+            got = counts.cpu().numpy()
+            assert (slots.cpu().numpy() == e_slots).all(), f"slots step {t}"
+            assert (got == e_counts).all(), f"counts step {t}"
+            for u in range(U):
+                cur = set(sel[t, u].tolist())
+                if B == k:  # top-k staging: misses = |S_t minus S_(t-1)|
+                    prev = set(sel[t - 1, u].tolist()) if t else set()
+                    assert got[u, 1] == len(cur - prev)
+                else:  # no eviction: misses = first touches only
+                    assert got[u, 1] == len(cur - seen[u])
+                seen[u] |= cur
+            check_resident(cache, 0, orc, U, B, R, host)
+        st = cache.read_state(0)
+        assert (st["page_table"] == orc.pt).all() and (st["slot_ts"] == orc.slot_ts).all()
     finally:
         torch.cuda.synchronize()
         cache.close()
