@@ -287,8 +287,8 @@ def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
 
 
 def pinned_budget_bytes() -> int:
-    """Pinned host memory the harness may use (HISPARSE_PINNED_BUDGET_GIB, default 63 GiB: the
-    MI355X boxes this was measured on refuse to pin more than about 65 GiB per process)."""
+    """Pinned host memory the inputs may use (HISPARSE_PINNED_BUDGET_GIB, default 63 GiB: a
+    host that grants one process about 65 GiB of pinned memory, as measured, then fits)."""
     return int(float(os.environ.get("HISPARSE_PINNED_BUDGET_GIB", "63")) * 2**30)
 
 
