@@ -90,10 +90,18 @@ __device__ __host__ inline int64_t mla_part_offset(int head, int dim) {
   return (int64_t)(head >> 5) * 32 * 512 + ((((dim >> 5) * 4 + q) * 64 + ln) * 4 + e);
 }
 
-__device__ inline uint16_t f32_to_bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two softmax weights 2^(s0 - m), 2^(s1 - m) rounded to bf16 (nearest even, one packed
+// v_cvt_pk_bf16_f32), the first in the low half; *psum accumulates the rounded values in that
+// order. The exponential is the hardware v_exp_f32: weights below 2^-126 flush to zero.
+__device__ inline uint32_t weights_bf16x2(float s0, float s1, float m, float* psum) {
+  const f32x2 e = {__builtin_amdgcn_exp2f(s0 - m), __builtin_amdgcn_exp2f(s1 - m)};
+  const uint32_t w = __builtin_bit_cast(uint32_t, __builtin_convertvector(e, bf16x2_t));
+  *psum += __uint_as_float(w << 16);
+  *psum += __uint_as_float(w & 0xFFFF0000u);
+  return w;
 }
 __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
@@ -301,13 +309,7 @@ void attn_partial_kernel(AttnArgs a) {
       pw[0] = pw[1] = pw[2] = pw[3] = 0u;
     } else {
 #pragma unroll
-      for (int j = 0; j < 8; j += 2) {
-        const uint16_t b0 = f32_to_bf16_rne(exp2f(sc[j] - m_run));
-        const uint16_t b1 = f32_to_bf16_rne(exp2f(sc[j + 1] - m_run));
-        psum += bf16_to_f32(b0);
-        psum += bf16_to_f32(b1);
-        pw[j >> 1] = (uint32_t)b0 | ((uint32_t)b1 << 16);
-      }
+      for (int j = 0; j < 8; j += 2) pw[j >> 1] = weights_bf16x2(sc[j], sc[j + 1], m_run, &psum);
     }
     psum += __shfl_xor(psum, 16, 64);
     psum += __shfl_xor(psum, 32, 64);
@@ -581,13 +583,7 @@ void attn_mla_kernel(AttnArgs a) {
       for (int j = 0; j < 8; ++j) pw[j] = 0u;
     } else {
 #pragma unroll
-      for (int j = 0; j < 16; j += 2) {
-        const uint16_t b0 = f32_to_bf16_rne(exp2f(sc[j] - m_run));
-        const uint16_t b1 = f32_to_bf16_rne(exp2f(sc[j + 1] - m_run));
-        psum += bf16_to_f32(b0);
-        psum += bf16_to_f32(b1);
-        pw[j >> 1] = (uint32_t)b0 | ((uint32_t)b1 << 16);
-      }
+      for (int j = 0; j < 16; j += 2) pw[j >> 1] = weights_bf16x2(sc[j], sc[j + 1], m_run, &psum);
     }
     psum += __shfl_xor(psum, 32, 64);
     l_run += psum;
