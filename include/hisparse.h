@@ -113,7 +113,9 @@ typedef struct {
  * [tokens_per_record][token_elems] bf16 with token_elems = record_bytes / 2 / tokens_per_record;
  * the key is the token's first d_qk elements and the value its d_v elements from v_offset.
  * Supported shapes: (d_qk, d_v, v_offset) = (576, 512, 0), latent MLA where the value is the
- * first 512 dims of the 576-dim latent record; and (128, 128, 128), GQA with K then V. */
+ * first 512 dims of the 576-dim latent record; and (128, 128, 128), GQA with K then V.
+ * top_k * tokens_per_record (tokens per unit) is at most 2^24, and at most 2^20 for latent MLA
+ * (HISPARSE_ERR_UNSUPPORTED above that). */
 typedef struct {
   int32_t q_heads;               /* query heads attending to one unit: 1 .. 256 */
   int32_t d_qk;

@@ -22,15 +22,18 @@ OK = 0
 BAD_SELECTION = -5
 
 
-def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (no HIP) into oracle/lib/libhisparse_oracle.so."""
-    os.makedirs(_LIB_DIR, exist_ok=True)
-    if force or not os.path.exists(_LIB_PATH):
-        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+def build(force: bool = True, path: str | None = None, extra_flags=()) -> str:
+    """Compile the oracle with gcc (no HIP) into oracle/lib/libhisparse_oracle.so, or into
+    `path` with extra compiler flags (e.g. a sanitizer build)."""
+    out = path or _LIB_PATH
+    os.makedirs(os.path.dirname(out), exist_ok=True)
+    if force or not os.path.exists(out):
+        tmp = out + ".tmp%d" % os.getpid()
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Wextra",
-                               "-fno-fast-math", "-ffp-contract=off", _SRC, "-o", tmp, "-lm"])
-        os.replace(tmp, _LIB_PATH)
-    return _LIB_PATH
+                               "-fno-fast-math", "-ffp-contract=off", *extra_flags, _SRC,
+                               "-o", tmp, "-lm"])
+        os.replace(tmp, out)
+    return out
 
 
 _lib = None
@@ -40,9 +43,10 @@ _P = ctypes.c_void_p
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB_PATH):
+        path = os.environ.get("HISPARSE_ORACLE_LIB") or _LIB_PATH  # another build, e.g. sanitized
+        if not os.path.exists(path):
             raise RuntimeError("oracle not built: run __graft_entry__.build()")
-        L = ctypes.CDLL(_LIB_PATH)
+        L = ctypes.CDLL(path)
         L.oracle_resolve.restype = ctypes.c_int
         L.oracle_resolve.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32] + [_P] * 9
         L.oracle_resolve_units.restype = ctypes.c_int

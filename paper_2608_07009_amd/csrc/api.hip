@@ -158,6 +158,9 @@ hisparse_status_t hisparse_validate_attn(int32_t record_bytes, int32_t top_k,
   const bool gqa = a->d_qk == 128 && a->d_v == 128 && a->v_offset == 128;
   if (!mla && !gqa) return HISPARSE_ERR_UNSUPPORTED;
   if (token_elems < std::max(a->d_qk, a->v_offset + a->d_v)) return HISPARSE_ERR_INVALID_ARG;
+  // latent attention merges at most kMlaMaxParts splits of at most kMaxSplitTokens tokens
+  if (mla && (int64_t)top_k * tpr > (int64_t)hisparse::kMlaMaxParts * hisparse::kMaxSplitTokens)
+    return HISPARSE_ERR_UNSUPPORTED;
   if ((record_bytes / tpr) % 16 != 0) return HISPARSE_ERR_INVALID_ARG;  // 16-byte token rows
   if (!(a->scale > 0.f) || a->scale > 1e6f) return HISPARSE_ERR_INVALID_ARG;
   return HISPARSE_OK;

@@ -42,7 +42,6 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kChunk = 32;            // tokens per wave per iteration
 constexpr int kTargetWorkgroups = 256;
 constexpr int kMaxSplitRecords = 1024;  // record indices of one split staged in LDS
-constexpr int kMaxSplitTokens = 8192;   // tokens of one split (validity bitmask in LDS)
 // Rescale the running output only when a head's running max grows by more than this (log2
 // units): exponentials are taken against a slightly stale max (values up to 2^8), which is
 // exact softmax arithmetic with a different reference point and keeps fp32/bf16 far from
@@ -794,8 +793,6 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(CombineArgs a) {
     *reinterpret_cast<float2*>(dst + e) = make_float2(acc[e] * inv, acc[e + 1] * inv);
 }
 
-constexpr int kMlaMaxParts = 128;
-
 struct CombineMlaArgs {
   const float* part_o;    // [units][n_parts][Hp * 512], block layout
   const float2* part_ml;  // [units][n_parts][H]
@@ -951,6 +948,9 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
   if (p.split_tokens > max_split_tokens) p.split_tokens = max_split_tokens / chunk * chunk;
   p.n_wg_splits = (p.n_tok + p.split_tokens - 1) / p.split_tokens;
   p.n_parts = p.n_wg_splits * p.tw;
+  // the latent-attention merge holds one weight per part in LDS (hisparse_validate_attn keeps the
+  // token count within reach of that limit)
+  if (is_mla(*attn) && p.n_parts > kMlaMaxParts) return HISPARSE_ERR_UNSUPPORTED;
   const int64_t n_wg = (int64_t)units * p.n_wg_splits * p.hb;
   if (n_wg > (1LL << 30)) return HISPARSE_ERR_INVALID_ARG;
   const int h_store = is_mla(*attn) ? (H + 31) / 32 * 32 : H;

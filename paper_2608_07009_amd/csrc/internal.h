@@ -13,6 +13,11 @@ namespace hisparse {
 constexpr int kMaxTopK = 4096;
 constexpr int kMaxCapacity = 16384;
 constexpr int kMaxRecordBytes = 1 << 20;
+// Sparse decode attention: tokens of one workgroup split (validity bitmask in LDS), and the most
+// split partial results the latent-attention merge takes per (unit, head) (weights in LDS). A
+// latent-attention call therefore covers at most kMlaMaxParts * kMaxSplitTokens tokens per unit.
+constexpr int kMaxSplitTokens = 8192;
+constexpr int kMlaMaxParts = 128;
 
 // Error word layout: [0] first error code, [1] layer, [2] unit, [3] failing unit-steps.
 constexpr int kErrWords = 4;

@@ -102,6 +102,27 @@ def test_record_too_small_for_attention():
     assert hs.hisparse_validate_attn(512, 64, ad) == hs.HISPARSE_ERR_INVALID_ARG
 
 
+def test_latent_attention_token_limit():
+    """Latent attention merges at most 128 splits of at most 8192 tokens: a call with more tokens
+    per unit is refused on the host (an unchecked one would index past the merge's LDS weights),
+    and every accepted call's plan fits those limits."""
+    R = 512 * 1152  # 512 latent tokens per record
+    big = hs.AttnDesc(128, 576, 512, 0, 512, 0, 0.07, 0)
+    for k in (2049, 3000, 4096):  # 2^20 + 512 .. 2^21 tokens
+        assert hs.hisparse_validate_attn(R, k, big) == hs.HISPARSE_ERR_UNSUPPORTED
+        assert hs.hisparse_decode_workspace_bytes(1, k, R, big) == 0
+    assert hs.hisparse_validate_attn(R, 2048, big) == hs.HISPARSE_OK  # exactly 2^20 tokens
+    for splits in (0, 1, 64, 200):
+        d = hs.AttnDesc(128, 576, 512, 0, 512, splits, 0.07, 0)
+        n = hs.hisparse_decode_workspace_bytes(1, 2048, R, d)
+        # [parts][128 heads][512] fp32 partials, then [parts][128] (max, sum) pairs
+        parts = n // (128 * 512 * 4 + 128 * 8)
+        assert n > 0 and 1 <= parts <= 128, (splits, n)
+    # token records and GQA pages are unaffected by the latent limit
+    g = hs.AttnDesc(4, 128, 128, 128, 4096, 0, 0.088, 0)
+    assert hs.hisparse_validate_attn(4096 * 512, 4096, g) == hs.HISPARSE_OK
+
+
 def test_status_strings():
     for code, name in [(0, "HISPARSE_OK"), (-1, "HISPARSE_ERR_INVALID_ARG"),
                        (-5, "HISPARSE_ERR_BAD_SELECTION"), (-6, "HISPARSE_ERR_FULL")]:

@@ -1,9 +1,6 @@
 """Host logic of the benchmark (no GPU): the busy time of overlapping transfer intervals, and the
 lookup of counter-measured traffic, which must return nothing once a kernel's source differs
 from the one the counters were taken on."""
-import os
-import shutil
-
 import numpy as np
 
 import bench
@@ -37,15 +34,24 @@ def test_union_length_matches_brute_force():
 
 
 def test_traffic_record_follows_the_kernel_sources(tmp_path, monkeypatch):
-    rec = bench.traffic_record("dsa_mla_32req_8L_ctx32K_k2048_B4096", "fetch")
-    assert rec is not None and rec["fetch_bytes"] > 0 and rec["write_bytes"] > 0
-    assert bench.traffic_record("no_such_workload", "fetch") is None
-    # a copy of the tree where one source of the kernel differs by a byte: no record applies
-    for d in ("profiles", "paper_2608_07009_amd/csrc"):
-        shutil.copytree(os.path.join(bench.ROOT, d), tmp_path / d)
+    """A synthetic record over two synthetic source files: it applies while their bytes hash to
+    the recorded sha256 and stops applying as soon as one of them changes."""
+    import hashlib
+    (tmp_path / "profiles").mkdir()
+    (tmp_path / "src").mkdir()
+    a, b = tmp_path / "src" / "k.hip", tmp_path / "src" / "k.h"
+    a.write_bytes(b"__global__ void k() {}\n")
+    b.write_bytes(b"#pragma once\n")
+    sha = hashlib.sha256(a.read_bytes() + b.read_bytes()).hexdigest()
+    (tmp_path / "profiles" / "k.md").write_text(
+        "# synthetic\n\ntraffic-record workload=w1 kernel=fetch source=src/k.hip,src/k.h "
+        f"sha256={sha} fetch_bytes=1200 write_bytes=1100\n")
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
-    assert bench.traffic_record("dsa_mla_32req_8L_ctx32K_k2048_B4096", "fetch") == \
-        dict(rec, profile=rec["profile"])
-    src = tmp_path / "paper_2608_07009_amd/csrc/fetch_device.h"
-    src.write_bytes(src.read_bytes() + b"\n")
-    assert bench.traffic_record("dsa_mla_32req_8L_ctx32K_k2048_B4096", "fetch") is None
+    rec = bench.traffic_record("w1", "fetch")
+    assert rec == {"fetch_bytes": 1200, "write_bytes": 1100, "profile": "profiles/k.md"}
+    assert bench.traffic_record("w2", "fetch") is None
+    assert bench.traffic_record("w1", "sparse_decode") is None
+    b.write_bytes(b.read_bytes() + b"\n")  # one byte more in one source: the record is stale
+    assert bench.traffic_record("w1", "fetch") is None
+    b.unlink()  # a missing source: no record either
+    assert bench.traffic_record("w1", "fetch") is None

@@ -163,13 +163,35 @@ def test_attention_wide_score_range(kind, H, splits):
     q_f[:, :, growth] = 1.0
     idx = np.stack([rng.choice(n_rec, size=k, replace=False) for _ in range(units)]).astype(np.int32)
     n_tok = k * tpr
+    rate = 40.0 if kind == "mla" else 25.0
     for u in range(units):
         for i in range(k):
             t = i * tpr + np.arange(tpr)                    # selection-order token numbers
-            pool_f[u, idx[u, i], :, growth] = (t * (25.0 / n_tok))[:, None]
+            pool_f[u, idx[u, i], :, growth] = (t * (rate / n_tok))[:, None]
     to_bf16 = lambda a: torch.from_numpy(a).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
     pool = to_bf16(pool_f.reshape(units, n_rec, tpr * te))
     q = to_bf16(q_f)
+    # The scores really do leave the kernels' reference slack (so the rescale / exact-fallback
+    # path runs): the float64 scores in log2 units, in selection order, of the bf16 inputs.
+    widen = lambda a: (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    keys = widen(pool).reshape(units, n_rec, tpr, te)[..., :d_qk]
+    sc = np.stack([np.einsum("hd,itd->hit", widen(q[u]), keys[u][idx[u]]).reshape(H, n_tok)
+                   for u in range(units)]) * (scale * np.log2(np.e))
+    if kind == "mla":
+        # latent kernel: explicit splits of whole 32-token chunks, reference = the max of the
+        # split's first chunk; a score more than 64 above it sends the split to the fallback
+        per = -(-n_tok // splits)
+        st = -(-per // 32) * 32
+        over = max(float((sc[:, :, b:b + st].max(axis=2) - sc[:, :, b:b + 32].max(axis=2)).max())
+                   for b in range(0, n_tok, st))
+        assert over > 64.0, over
+    else:
+        # grouped-query kernel: the running max moves (a rescale) when a later 32-token chunk
+        # outgrows it by more than 8; every chunk outgrows the previous one by more than that,
+        # and each part holds at least two chunks
+        cmax = sc.reshape(units, H, n_tok // 32, 32).max(axis=3)
+        assert (cmax[:, :, 1:] - cmax[:, :, :-1]).min() > 8.0
+        assert n_tok >= 2 * 32 * 4
     dev = torch.device("cuda:0")
     ad = attn_desc(w, splits)
     ws = torch.empty(hs.hisparse_decode_workspace_bytes(units, k, R, ad), dtype=torch.uint8,

@@ -27,16 +27,18 @@ _LIB_PATH = os.path.join(_LIB_DIR, "libhs_workload.so")
 _SRC = os.path.join(_HERE, "hs_workload.c")
 
 
-def build(force: bool = True) -> str:
-    """Compile the generator with gcc into workload/lib/libhs_workload.so."""
-    os.makedirs(_LIB_DIR, exist_ok=True)
-    if force or not os.path.exists(_LIB_PATH):
-        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+def build(force: bool = True, path: str | None = None, extra_flags=()) -> str:
+    """Compile the generator with gcc into workload/lib/libhs_workload.so, or into `path` with
+    extra compiler flags (e.g. a sanitizer build)."""
+    out = path or _LIB_PATH
+    os.makedirs(os.path.dirname(out), exist_ok=True)
+    if force or not os.path.exists(out):
+        tmp = out + ".tmp%d" % os.getpid()
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread",
-                               "-Wall", "-Wextra", "-Wno-unused-parameter",
+                               "-Wall", "-Wextra", "-Wno-unused-parameter", *extra_flags,
                                _SRC, "-o", tmp, "-lm"])
-        os.replace(tmp, _LIB_PATH)
-    return _LIB_PATH
+        os.replace(tmp, out)
+    return out
 
 
 class _StreamParams(ctypes.Structure):
@@ -52,9 +54,10 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB_PATH):
+        path = os.environ.get("HS_WORKLOAD_LIB") or _LIB_PATH  # another build, e.g. sanitized
+        if not os.path.exists(path):
             raise RuntimeError("workload generator not built: run __graft_entry__.build()")
-        L = ctypes.CDLL(_LIB_PATH)
+        L = ctypes.CDLL(path)
         L.hs_key.restype = ctypes.c_uint64
         L.hs_key.argtypes = [ctypes.c_uint64] * 5
         L.hs_splitmix64.restype = ctypes.c_uint64
