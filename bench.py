@@ -45,7 +45,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=8)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=None, choices=[1, 2, 3, 4, 5],
+                    help="run this workload only, in this process (default: every workload, "
+                         "each in a child process; the DSA/MLA workload's line is the headline)")
+    ap.add_argument("--child", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--requests", type=int, default=0, metavar="N",
                     help="run the workload with N requests instead of its own count (a batch "
                          "scan; every other shape is the workload's)")
@@ -57,8 +60,8 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay")
     ap.add_argument("--graph-steps", type=int, default=4,
                     help="decode steps captured in one HIP graph (the largest even divisor of "
-                         "--steps and --warmup up to this; 1 = one step per graph, queries "
-                         "copied into place each step)")
+                         "--steps up to this; 1 = one step per graph, queries copied into "
+                         "place each step); the warm-up steps run eagerly before the replays")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-sweep", action="store_true")
@@ -206,39 +209,121 @@ def union_length(intervals) -> float:
     return total
 
 
-def cpu_baseline(w, cache, sel_host, budget_s: float, L: int) -> dict:
-    """The oracle, as it stands, on a bounded sample: resolve + gather + float64 attention of
-    units of layer 0, steps from cold, until the time budget is used."""
+def host_cores() -> int:
+    """Cores this process may use: its CPU affinity, capped by OMP_NUM_THREADS when set (the
+    host's share per GPU)."""
+    n = len(os.sched_getaffinity(0))
+    try:
+        n = min(n, int(os.environ.get("OMP_NUM_THREADS", n)))
+    except ValueError:
+        pass
+    return max(1, n)
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, host_unit, budget_s: float) -> dict:
+    """The oracle, as it stands, timed on the host's cores: a thread pool over independent cache
+    units (every (anchor layer, unit) stream of the workload) runs the canonical-LRU resolve of
+    every step, with each step's misses gathered from the host pool into the unit's cache image,
+    until the time budget is used; then float64 attention, timed separately, over a sample of
+    units of the last resolved step. host_unit(layer, unit) -> uint8 [L][R] host records."""
+    import threading
+
     import numpy as np
 
     import oracle
     import workload as W
 
-    n_units = min(4, w.units)
-    orcs = [oracle.OracleCache(1, L, w.B, w.k) for _ in range(n_units)]
-    imgs = [np.zeros((w.B, w.record_bytes), dtype=np.uint8) for _ in range(n_units)]
-    host = cache.host_view(0)
-    done = 0
+    T = host_cores()
+    sel_all = W.selection_streams(w, steps=w.steps)  # [steps][anchors * units][k]
+    n_streams = sel_all.shape[1]
+    G, U, k, B, R = w.share_group, w.units, w.k, w.B, w.record_bytes
+    T = min(T, n_streams)
+    bounds = [n_streams * i // T for i in range(T + 1)]
+    caches = [oracle.OracleCache(bounds[i + 1] - bounds[i], w.L, B, k) for i in range(T)]
+    imgs = [np.zeros((bounds[i + 1] - bounds[i], B, R), dtype=np.uint8) for i in range(T)]
+    done = [0] * T
+    last = [None] * T
+    errors = []
+    stop_at = [0.0]
+
+    def worker(i):
+        s0, s1 = bounds[i], bounds[i + 1]
+        try:
+            for t in range(sel_all.shape[0]):
+                if time.perf_counter() > stop_at[0]:
+                    break
+                slots, counts, pp, ps, bad = caches[i].resolve(sel_all[t, s0:s1])
+                if bad:
+                    raise RuntimeError(f"oracle resolve reported {bad} bad selections")
+                for j in range(s1 - s0):
+                    a, u = divmod(s0 + j, U)
+                    m = int(counts[j, 1])
+                    oracle.apply_plan(host_unit(a * G, u), imgs[i][j], pp[j, :m], ps[j, :m])
+                done[i] += 1
+                last[i] = (t, slots)
+        except Exception as e:  # reported by the caller
+            errors.append(repr(e))
+
     t0 = time.perf_counter()
-    t = 0
-    while time.perf_counter() - t0 < budget_s and t < sel_host.shape[0]:
-        q = W.queries(w, t, 0, 0, n_units)
-        for u in range(n_units):
-            rc, slots, _, pp, ps = orcs[u].resolve_unit(0, sel_host[t, u])
-            if rc != 0:
-                raise RuntimeError(f"oracle resolve failed ({rc}) at step {t}, unit {u}")
-            oracle.apply_plan(host[u], imgs[u], pp, ps)
-            oracle.sparse_decode(q[u], imgs[u].view(np.uint16).reshape(w.B, -1), slots,
-                                 d_qk=w.d_qk, d_v=w.d_v, v_off=w.v_offset,
-                                 token_elems=w.token_elems,
-                                 tokens_per_record=w.tokens_per_record, scale=w.scale)
-            done += 1
-        t += 1
+    stop_at[0] = t0 + budget_s
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(T)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
     dt = time.perf_counter() - t0
-    return {"value": done * w.k / dt, "unit": "selections/s", "cores": 1, "kind": "oracle",
-            "sample": f"{done} unit-steps (units 0..{n_units - 1} of layer 0, steps 0..{t - 1} "
-                      f"from cold): canonical-LRU resolve + record gather + float64 attention "
-                      f"over {w.q_heads} heads, single thread, {dt:.1f} s"}
+    if errors:
+        raise RuntimeError("CPU baseline: " + errors[0])
+    sels = sum(done[i] * (bounds[i + 1] - bounds[i]) * k for i in range(T))
+    steps_done = min(done)
+
+    # float64 attention over the cache images through the last step's slots, a sample of up to
+    # 2 units per thread (the first units of each thread's range), threads in parallel
+    n_att = [min(2, bounds[i + 1] - bounds[i]) for i in range(T)]
+    att_t = [0.0] * T
+
+    def att_worker(i):
+        t, slots = last[i]
+        for j in range(n_att[i]):
+            a, u = divmod(bounds[i] + j, U)
+            q = W.queries(w, t, a * G, u, 1)[0]
+            ts = time.perf_counter()
+            oracle.sparse_decode(q, imgs[i][j].view(np.uint16).reshape(B, -1), slots[j],
+                                 d_qk=w.d_qk, d_v=w.d_v, v_off=w.v_offset,
+                                 token_elems=w.token_elems, tokens_per_record=w.tokens_per_record,
+                                 scale=w.scale)
+            att_t[i] += time.perf_counter() - ts
+
+    ta = time.perf_counter()
+    threads = [threading.Thread(target=att_worker, args=(i,)) for i in range(T) if last[i]]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    dta = time.perf_counter() - ta
+    n_units_att = sum(n_att[i] for i in range(T) if last[i])
+    return {"value": sels / dt, "unit": "selections/s", "cores": T, "kind": "oracle",
+            "cpu_model": cpu_model(),
+            "sample": f"canonical-LRU resolve of steps 0..{steps_done - 1} (at least; "
+                      f"{sum(done)} thread-steps) of all {n_streams} (anchor layer, unit) "
+                      f"streams of {w.name}, each step's misses gathered from the host pool into "
+                      f"the unit's cache image, {T} threads over disjoint units, {dt:.1f} s",
+            "resolve_steps_done": steps_done, "resolve_steps_in_workload": int(sel_all.shape[0]),
+            "attention_us_per_unit": 1e6 * sum(att_t) / max(1, n_units_att),
+            "attention_units_per_s": n_units_att / dta if dta > 0 else None,
+            "attention_sample": f"float64 attention of {n_units_att} units ({w.q_heads} heads "
+                                f"over {k} records) of the last resolved step through their "
+                                f"slots, {T} threads, {dta:.1f} s"}
 
 
 def stage_probe(torch, hip: Hip, hs, w, cache, root_s: int, run_steps, warm: int,
@@ -356,6 +441,68 @@ def resolve_sweep(args, torch, hs, W, HiSparseCache) -> int:
     return 0
 
 
+# Workloads of the default run: the headline first, then the others; seconds each child may take.
+ALL_CONFIGS = ((2, 240), (1, 90), (3, 120), (4, 150), (5, 240))
+
+
+def compact(d: dict) -> dict:
+    """The figures of one workload's line kept in the headline line's `configs` object."""
+    keep = ("value", "unit", "steps", "warmup", "ms_per_step", "decode_tokens_per_s",
+            "miss_fetch_GBps", "miss_fetch_pct_of_pinned_h2d_peak", "pinned_h2d_peak_GBps",
+            "link_busy_fraction", "link_GBps_over_step", "link_pct_of_pinned_h2d_peak_over_step",
+            "hit_rate", "misses_per_unit_step", "cold_step_ms", "roofline", "eager_gpu_ms_per_step",
+            "resolve_with_fetch_selections_per_s", "span_steps_with_stall", "hbm_footprint_GiB")
+    out = {k: d[k] for k in keep if k in d}
+    c = d.get("config", {})
+    out.update({k: c[k] for k in ("workload", "requests", "layers", "layers_in_workload",
+                                  "micro_batches", "schedule", "steps_per_graph", "mode")
+                if k in c})
+    out["kernels_avg_us"] = {name: round(v["avg_us"], 2) for name, v in d.get("kernels", {}).items()}
+    return out
+
+
+def run_all(args) -> int:
+    """Every workload, each in a child process of its own (this process never touches the GPU,
+    so no child inherits a HIP context and the pinned pools of one workload are released before
+    the next one pins its own). The headline line is the DSA/MLA workload's; the others are
+    summarised under `configs`. A child that dies of a signal or a time limit ends the run."""
+    import subprocess
+
+    me = os.path.abspath(__file__)
+    rest = [a for a in sys.argv[1:]]
+    head, configs = None, {}
+    for c, limit in ALL_CONFIGS:
+        cmd = [sys.executable, me, *rest, "--config", str(c), "--child"]
+        if c != 2:
+            cmd.append("--no-cpu-baseline")
+        log(f"workload {c}: {' '.join(cmd[1:])}")
+        try:
+            r = subprocess.run(cmd, stdout=subprocess.PIPE, timeout=limit, text=True)
+        except subprocess.TimeoutExpired:
+            configs[str(c)] = {"error": f"no result within {limit} s"}
+            log(f"workload {c} exceeded {limit} s; no further GPU work in this run")
+            break
+        lines = [x for x in r.stdout.splitlines() if x.startswith("{")]
+        res = json.loads(lines[-1]) if lines else {}
+        if r.returncode != 0 or "error" in res or not lines:
+            configs[str(c)] = {"error": res.get("error", f"exit status {r.returncode}"),
+                               "returncode": r.returncode}
+            if r.returncode < 0 or r.returncode > 128:
+                log(f"workload {c} ended by signal / status {r.returncode}: stopping")
+                break
+            continue
+        if c == 2:
+            head = res
+        else:
+            configs[str(c)] = compact(res)
+    if head is None:
+        print(json.dumps({"error": "the DSA/MLA workload produced no result", "configs": configs}))
+        return 1
+    head["configs"] = configs
+    print(json.dumps(head), flush=True)
+    return 0
+
+
 def main() -> int:
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -364,6 +511,10 @@ def main() -> int:
                           "are independent caches, so more GPUs shard requests without any "
                           "exchange; run one process per GPU", "n_gpus": args.gpus}))
         return 2
+    if args.config is None and not (args.copy_probe or args.resolve_sweep):
+        return run_all(args)
+    if args.config is None:
+        args.config = 2
 
     import numpy as np
     import torch
@@ -395,6 +546,11 @@ def main() -> int:
         w0 = dataclasses.replace(w0, num_requests=args.requests,
                                  name=f"{w0.name}_with_{args.requests}_requests")
     w = W.fit_pinned(w0)
+    if args.child and args.warmup + args.steps > w.steps:
+        # a workload with fewer steps than asked for: as many timed steps as it has after the
+        # warm-up, a multiple of the graph's step count
+        args.steps = max(args.graph_steps, (w.steps - args.warmup) // max(1, args.graph_steps)
+                         * max(1, args.graph_steps))
     steps_needed = args.warmup + args.steps
     if steps_needed > w.steps:
         print(json.dumps({"error": f"warmup + steps = {steps_needed} exceeds the workload's "
@@ -709,7 +865,8 @@ def main() -> int:
         rec(r1, root_s)
         torch.cuda.synchronize()
         step_refs.append((r0, r1, first))
-    eager_gpu_ms = sum(hip.ms(r0, r1) for r0, r1, _ in step_refs) / args.steps
+    step_ms = [hip.ms(r0, r1) for r0, r1, _ in step_refs]
+    eager_gpu_ms = sum(step_ms) / args.steps
     # slot vectors and attention outputs of the last step, to check the graph replays against
     eager_final = [(mb.slots.clone(), out[:, mb.u0:mb.u0 + mb.U].clone()) for mb in mbs]
     for mb in mbs:
@@ -920,9 +1077,11 @@ def main() -> int:
         roof = {"kernel": dom, "bound": "hbm", "achieved": kd["hbm_GBps"], "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": kd["hbm_GBps"] / HBM_PEAK_GBPS, "traffic": None}
 
-    miss_gbps = ((fetch_bytes + replay_bytes + group_bytes + carried_bytes + spec_bytes)
-                 / io_busy / 1e9
-                 if (io_busy and moves_data) else None)
+    link_bytes = fetch_bytes + replay_bytes + group_bytes + carried_bytes + spec_bytes
+    miss_gbps = link_bytes / io_busy / 1e9 if (io_busy and moves_data) else None
+    # share of the span pass's step time in which some host-link transfer ran
+    kept_ms = sum(step_ms[si] for si in kept)
+    link_busy = io_busy * 1e3 / kept_ms if (kept_ms and moves_data) else None
 
     # the same steps replayed from a captured HIP graph (cold reset, same warmup)
     graph = None
@@ -932,8 +1091,8 @@ def main() -> int:
         # counter at the start, the queries are read in place, and the micro-batches fork once
         # and join once per replay, so one micro-batch's next step can start while another
         # finishes its last layer.
-        S = max(1, args.graph_steps)  # the largest even divisor of steps and warmup up to it
-        while S > 1 and (args.steps % S or args.warmup % S or S % n_qv):
+        S = max(1, args.graph_steps)  # the largest even divisor of the timed steps up to it
+        while S > 1 and (args.steps % S or S % n_qv):
             S -= 1
         stage_sel = torch.empty((S,) + tuple(sel.shape[1:]), dtype=sel.dtype, device=dev)
         stage_q = torch.empty_like(q_all[0]) if S == 1 else None
@@ -945,8 +1104,9 @@ def main() -> int:
         if S == 1:
             q_stage_p = [{mb.u0: [stage_q[l, mb.u0:mb.u0 + mb.U].data_ptr()
                                   for l in range(w.num_layers)] for mb in mbs}]
-        else:
-            q_stage_p = [{mb.u0: mb.q_p[j % n_qv] for mb in mbs} for j in range(S)]
+        else:  # replays start at step `warmup`: step warmup + j reads query parity of j + warmup
+            q_stage_p = [{mb.u0: mb.q_p[(args.warmup + j) % n_qv] for mb in mbs}
+                         for j in range(S)]
         app_stage_p = [None] * S
         if args.append:  # the steps' appended positions and records, staged like selections
             for mb in mbs:
@@ -971,11 +1131,17 @@ def main() -> int:
                 step(j, sel_override=sel_stage_p[j], q_override=q_stage_p[j], fork=(j == 0),
                      join=(j == S - 1), app_override=app_stage_p[j])
         torch.cuda.synchronize()
-        for mb in mbs:
-            hs.hisparse_reset(mb.h, root_s)
-        tidx.zero_()
-        for _ in range(args.warmup // S):
-            g.replay()
+
+        def warm_up():
+            """Cold reset, then the warm-up steps eagerly (any number of them), leaving the
+            graph's step counter at the first timed step."""
+            for mb in mbs:
+                hs.hisparse_reset(mb.h, root_s)
+            for t in range(args.warmup):
+                step(t)
+            tidx.fill_(args.warmup)
+
+        warm_up()
         torch.cuda.synchronize()
         tg = time.perf_counter()
         for _ in range(args.steps // S):
@@ -1004,9 +1170,7 @@ def main() -> int:
             for mb in mbs:
                 hs.hisparse_reset(mb.h, root_s)
             if graph is not None:
-                tidx.zero_()
-                for _ in range(args.warmup // S):
-                    g.replay()
+                warm_up()
                 rec(ev0, root_s)
                 for _ in range(args.steps // S):
                     g.replay()
@@ -1026,6 +1190,8 @@ def main() -> int:
     else:  # eager launches with the host ahead of the GPU
         mode, wall = "eager", eager_gpu_ms * K * 1e-3
     value = served / wall
+    # the host link's rate over the whole step of the timed region (not only inside transfers)
+    link_step_gbps = (link_bytes / max(1, Ks)) / (wall / K) / 1e9 if moves_data else None
 
     result = {
         "metric": "resolved selections/s + miss-fetch GB/s (% host-link peak), decode tokens/s",
@@ -1054,6 +1220,10 @@ def main() -> int:
         "miss_fetch_pct_of_pinned_h2d_peak": (100 * miss_gbps / pinned_peak)
         if (miss_gbps and pinned_peak) else None,
         "pinned_h2d_peak_GBps": pinned_peak,
+        "link_busy_fraction": link_busy,
+        "link_GBps_over_step": link_step_gbps,
+        "link_pct_of_pinned_h2d_peak_over_step": (100 * link_step_gbps / pinned_peak)
+        if (link_step_gbps and pinned_peak) else None,
         "pinned_h2d_sweep_GBps": {str(s): v for s, v in sweep.items()},
         # resolved selections per second of resolve + fetch kernel time (the resolve step alone,
         # with its IO): anchor layer calls x units x k over the span-pass time of the resolve
@@ -1074,8 +1244,16 @@ def main() -> int:
         result["staging"] = staging
     if not args.no_cpu_baseline:
         log("timing the CPU oracle baseline")
-        result["cpu_baseline"] = cpu_baseline(w, cache, sel_host[:, :mbs[0].U], args.cpu_budget,
-                                              L_pool)
+        U_mb = U_all // n_mb
+        views = {}
+
+        def host_unit(layer, unit):
+            key = (layer, unit // U_mb)
+            if key not in views:
+                views[key] = mbs[unit // U_mb].cache.host_view(layer)
+            return views[key][unit % U_mb]
+
+        result["cpu_baseline"] = cpu_baseline(w, host_unit, args.cpu_budget)
     for mb in mbs:
         for e in mb.sync + mb.link:
             hip.L.hipEventDestroy(e)
