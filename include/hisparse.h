@@ -347,6 +347,24 @@ hisparse_status_t hisparse_attention_merge(int32_t units, int32_t top_k, int32_t
                                            const void* d_workspace, size_t workspace_bytes,
                                            void* stream);
 
+/* Bytes of device scratch each GPU holds for hisparse_sparse_decode_noalloc (64 MiB). */
+#define HISPARSE_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* [async] hisparse_sparse_decode without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the split partial results go to a scratch array of HISPARSE_NOALLOC_SCRATCH_BYTES that the
+ * library holds on each GPU it runs on until the process ends, and the call allocates nothing.
+ * Same arguments, output and bits as hisparse_sparse_decode with a workspace.
+ *   - HISPARSE_ERR_UNSUPPORTED if the call needs more scratch than that
+ *     (hisparse_decode_workspace_bytes(units, k, R, attn) > HISPARSE_NOALLOC_SCRATCH_BYTES);
+ *   - HISPARSE_ERR_INVALID_ARG with HISPARSE_ATTN_DEFER_MERGE (the partials have no owner).
+ * Every call on one GPU shares that GPU's scratch, from any handle: calls that may overlap on
+ * one GPU (other streams, other host threads) race and must be ordered by the caller. */
+hisparse_status_t hisparse_sparse_decode_noalloc(hisparse_cache_t cache, int32_t layer,
+                                                 const void* d_q, const int32_t* d_slots,
+                                                 float* d_out, const hisparse_attn_desc_t* attn,
+                                                 void* stream);
+
 /* [async] hisparse_sparse_decode of `layer` and, in the same launch, the exact-prefetch replay
  * of `anchor_layer`'s latest plan into shared layers [first_shared, first_shared + num_shared)
  * (Section 3.5): equal to hisparse_prefetch_layers followed by hisparse_sparse_decode, but the

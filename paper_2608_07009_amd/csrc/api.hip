@@ -4,6 +4,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 
 #include "internal.h"
@@ -93,6 +94,35 @@ hisparse::StateArgs state_args(const hisparse_cache* c, const hisparse_cache::An
   s.B = c->desc.capacity;
   s.units = c->units;
   return s;
+}
+
+// Scratch of hisparse_sparse_decode_noalloc: one array per GPU, created with the code object
+// and kept until the process ends. In host code `scratch` names a host-side stand-in, not device
+// memory: its device address on each GPU comes from hipGetSymbolAddress, taken once per device
+// when a cache is created there.
+static __device__ __align__(256) uint8_t scratch[HISPARSE_NOALLOC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// With `device` current: the device address of its scratch array, looked up on first use.
+hisparse_status_t init_scratch(int device) {
+  if (device < 0 || device >= kMaxDevices) return HISPARSE_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[device]) return HISPARSE_OK;
+  void* ptr = nullptr;
+  if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+    (void)hipGetLastError();
+    return HISPARSE_ERR_HIP;
+  }
+  g_scratch_ptr[device] = ptr;
+  return HISPARSE_OK;
+}
+
+void* scratch_of(int device) {
+  if (device < 0 || device >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  return g_scratch_ptr[device];
 }
 
 }  // namespace
@@ -281,6 +311,8 @@ hisparse_status_t hisparse_cache_create(const hisparse_cache_desc_t* desc, int32
     }
     if (st == HISPARSE_OK && hipDeviceSynchronize() != hipSuccess) st = HISPARSE_ERR_HIP;
   }
+  // the allocation-free attention's scratch on this device (once per device)
+  if (st == HISPARSE_OK) st = init_scratch(device);
   (void)hipSetDevice(prev);
   if (st != HISPARSE_OK) {
     (void)hipGetLastError();
@@ -662,6 +694,31 @@ hisparse_status_t hisparse_sparse_decode(hisparse_cache_t c, int32_t layer, cons
   return hisparse_sparse_decode_pool(c->cache[layer], c->desc.capacity, c->desc.record_bytes,
                                      c->units, c->desc.top_k, d_q, d_slots, d_out, attn,
                                      d_workspace, workspace_bytes, stream);
+}
+
+hisparse_status_t hisparse_sparse_decode_noalloc(hisparse_cache_t c, int32_t layer,
+                                                 const void* d_q, const int32_t* d_slots,
+                                                 float* d_out, const hisparse_attn_desc_t* attn,
+                                                 void* stream) {
+  if (!c || layer < 0 || layer >= c->desc.num_layers) return HISPARSE_ERR_INVALID_ARG;
+  if (!d_q || !d_slots || !d_out || !attn) return HISPARSE_ERR_INVALID_ARG;
+  // the split partials must be merged within the call: nothing else can find them
+  if (attn->flags & HISPARSE_ATTN_DEFER_MERGE) return HISPARSE_ERR_INVALID_ARG;
+  hisparse::AttnPlan p{};
+  hisparse_status_t st =
+      hisparse::plan_attention(c->units, c->desc.top_k, c->desc.record_bytes, attn, &p);
+  if (st != HISPARSE_OK) return st;
+  if (p.workspace_bytes > HISPARSE_NOALLOC_SCRATCH_BYTES) return HISPARSE_ERR_UNSUPPORTED;
+  if ((int64_t)c->desc.capacity * c->desc.record_bytes > (int64_t)INT32_MAX)
+    return HISPARSE_ERR_UNSUPPORTED;
+  void* ws = scratch_of(c->device);
+  if (!ws) return HISPARSE_ERR_HIP;
+  if (hisparse::launch_attention(p, *attn, c->cache[layer], c->desc.capacity,
+                                 c->desc.record_bytes, c->units, c->desc.top_k,
+                                 reinterpret_cast<const uint16_t*>(d_q), d_slots, d_out, ws,
+                                 as_stream(stream)) != hipSuccess)
+    return HISPARSE_ERR_HIP;
+  return HISPARSE_OK;
 }
 
 hisparse_status_t hisparse_sparse_decode_prefetch(hisparse_cache_t c, int32_t layer,

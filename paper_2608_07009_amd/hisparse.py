@@ -29,6 +29,7 @@ HISPARSE_FETCH_SDMA = 1
 HISPARSE_FETCH_NONE = 2
 
 HISPARSE_ATTN_DEFER_MERGE = 1
+HISPARSE_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 HISPARSE_HOST_COHERENT = 0
 HISPARSE_HOST_NONCOHERENT = 1
@@ -45,7 +46,7 @@ EXPORTED = (
     "hisparse_decode_workspace_bytes", "hisparse_sparse_decode", "hisparse_sparse_decode_layers",
     "hisparse_attention_merge",
     "hisparse_sparse_decode_prefetch",
-    "hisparse_sparse_decode_pool",
+    "hisparse_sparse_decode_pool", "hisparse_sparse_decode_noalloc",
     "hisparse_read_state", "hisparse_read_plan", "hisparse_check_errors",
 )
 
@@ -122,6 +123,8 @@ def lib() -> ctypes.CDLL:
             "hisparse_sparse_decode_prefetch": (_I32, [_V, _I32, _V, _V, _V,
                                                        ctypes.POINTER(AttnDesc), _V,
                                                        ctypes.c_size_t, _I32, _I32, _I32, _V]),
+            "hisparse_sparse_decode_noalloc": (_I32, [_V, _I32, _V, _V, _V,
+                                                      ctypes.POINTER(AttnDesc), _V]),
             "hisparse_sparse_decode_pool": (_I32, [_V, ctypes.c_int64, _I32, _I32, _I32, _V, _V,
                                                    _V, ctypes.POINTER(AttnDesc), _V,
                                                    ctypes.c_size_t, _V]),
@@ -289,6 +292,13 @@ def hisparse_sparse_decode(cache: int, layer: int, d_q, d_slots, d_out, attn: At
            lib().hisparse_sparse_decode(cache, layer, _p(d_q), _p(d_slots), _p(d_out),
                                         ctypes.byref(attn), _p(d_workspace), workspace_bytes,
                                         _s(stream)))
+
+
+def hisparse_sparse_decode_noalloc(cache: int, layer: int, d_q, d_slots, d_out, attn: AttnDesc,
+                                   stream=None) -> None:
+    _check("hisparse_sparse_decode_noalloc",
+           lib().hisparse_sparse_decode_noalloc(cache, layer, _p(d_q), _p(d_slots), _p(d_out),
+                                                ctypes.byref(attn), _s(stream)))
 
 
 def hisparse_attention_merge(units: int, top_k: int, record_bytes: int, attn: AttnDesc, d_out,
