@@ -74,6 +74,11 @@ def parse():
                          "first only (then run free from that offset: 1-2%% faster when "
                          "undisturbed, but a perturbation such as a profiler attached can push "
                          "the chains into lockstep for good)")
+    ap.add_argument("--attn-plan", choices=["auto", "beside-fetch", "own-gpu"], default="auto",
+                    help="latent attention's plan hint: 'beside-fetch' (HISPARSE_ATTN_BESIDE_FETCH: "
+                         "another micro-batch's host-link fetch runs beside each attention call) "
+                         "or 'own-gpu'; auto = beside-fetch when several micro-batches move "
+                         "records over the link")
     ap.add_argument("--fetch-workgroups", type=int, default=0,
                     help="workgroups of one fetch launch (0 = the library default)")
     ap.add_argument("--schedule", choices=["overlap", "serial", "side", "batched"],
@@ -597,8 +602,11 @@ def main() -> int:
     # every attention call defers its merge to a separate hisparse_attention_merge call, so
     # that the attention kernel (and the replay it may carry) and the merge kernel are timed
     # apart; the work is that of the fused call
+    beside = (args.attn_plan == "beside-fetch" or
+              (args.attn_plan == "auto" and n_mb > 1 and fetch != hs.HISPARSE_FETCH_NONE))
     ad = hs.AttnDesc(w.q_heads, w.d_qk, w.d_v, w.v_offset, w.tokens_per_record, args.splits,
-                     w.scale, hs.HISPARSE_ATTN_DEFER_MERGE)
+                     w.scale, hs.HISPARSE_ATTN_DEFER_MERGE |
+                     (hs.HISPARSE_ATTN_BESIDE_FETCH if beside else 0))
     ad_ref = ctypes.byref(ad)
     groups = [(a, list(range(a + 1, min(a + G, w.num_layers)))) for a in w.anchors]
 
@@ -1214,6 +1222,7 @@ def main() -> int:
                    "share_group": G, "q_heads": w.q_heads, "fetch": args.fetch,
                    "speculate": args.speculate, "xlayer_overlap": args.xlayer_overlap,
                    "host_memory": args.host_memory, "mode": mode,
+                   "attn_plan": "beside-fetch" if beside else "own-gpu",
                    "steps_per_graph": graph["steps_per_graph"] if graph else None},
         "decode_tokens_per_s": w.num_requests * K / wall,
         "miss_fetch_GBps": miss_gbps,

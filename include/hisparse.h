@@ -125,7 +125,7 @@ typedef struct {
   int32_t num_splits;            /* partitions of the token sequence reduced in a fixed order;
                                     0 = chosen from the shape alone */
   float scale;                   /* softmax scale applied to q.k */
-  int32_t flags;                 /* 0 or HISPARSE_ATTN_DEFER_MERGE */
+  int32_t flags;                 /* 0 or HISPARSE_ATTN_DEFER_MERGE | HISPARSE_ATTN_BESIDE_FETCH */
 } hisparse_attn_desc_t;
 
 /* hisparse_attn_desc_t.flags: the attention call runs only its per-split workgroups (and any
@@ -133,6 +133,14 @@ typedef struct {
  * d_out; hisparse_attention_merge then writes d_out from them. For callers that schedule,
  * overlap or time the two kernels apart. */
 #define HISPARSE_ATTN_DEFER_MERGE 1
+/* hisparse_attn_desc_t.flags, a scheduling hint for latent attention: the call runs beside
+ * another stream's host-link fetch (e.g. two micro-batches taking turns on the link), whose slow
+ * host reads occupy the CUs' memory pipelines. The plan then keeps more loads in flight per
+ * workgroup (one token group, up to four head waves) at the cost of twice the split partial
+ * results; without it, large enough calls use two token groups per workgroup, which halves the
+ * partials and is faster on a GPU of its own. Results differ only within rounding (other split
+ * boundaries); each plan is deterministic. */
+#define HISPARSE_ATTN_BESIDE_FETCH 2
 
 /* Human-readable name of a status code (static storage). */
 const char* hisparse_status_string(hisparse_status_t status);
@@ -339,7 +347,8 @@ hisparse_status_t hisparse_sparse_decode(hisparse_cache_t cache, int32_t layer, 
 /* [async] The merge of an attention call made with HISPARSE_ATTN_DEFER_MERGE: combines the
  * per-split partial results in d_workspace into d_out (float32 [units][q_heads][d_v]), in
  * the fixed split order, so deferred call + merge == the same call without the flag, bit for
- * bit. units, top_k, record_bytes and attn (flags aside) must be those of the deferred call,
+ * bit. units, top_k, record_bytes and attn (HISPARSE_ATTN_DEFER_MERGE aside) must be those of
+ * the deferred call,
  * whose `units` is the cache's units times the layer count for hisparse_sparse_decode_layers;
  * the workspace must not be reused in between. */
 hisparse_status_t hisparse_attention_merge(int32_t units, int32_t top_k, int32_t record_bytes,

@@ -489,29 +489,36 @@ __device__ __forceinline__ void mla_split_exact(const AttnArgs& a, const int32_t
 }
 
 // Latent attention (d_qk 576, d_v 512 = the first 512 key dims). One workgroup per
-// (unit, token split, head block of 32 * NW heads); wave w owns 32 heads and the workgroup's
-// 32-token chunks are staged once in LDS for all of them.
+// (unit, token split, head block of 32 * HW heads); wave w owns 32 heads (w % HW) of token
+// group w / HW. Each token group has its own ring of NST chunk tiles in LDS, staged once for its
+// HW head waves; with TG = 2 groups the split's 32-token chunks alternate between the groups and
+// the two groups' results are merged in LDS at the end, so a workgroup writes one partial result
+// for twice the tokens of one group (half the partial traffic of two workgroups).
 //   S^T[token][head] = K[token][:] . Q^T[:][head]   v_mfma_f32_32x32x16_bf16, 36 k-steps, K rows
 //                                                   from LDS, Q resident in VGPRs
 //   O[head][dim]    += P[head][token] . V[token][dim]  v_mfma_f32_32x32x16_bf16, 2 k-steps x 16
 //                                                   output tiles, V by LDS transpose reads
 // A lane holds 16 of a head's 32 scores (the other 16 are in lane ^ 32), which are exactly its
 // P operands of the two PV k-steps; O (16 tiles x 16 fp32 per lane) lives in accumulators.
-template <int NW, int NST>
-__global__ __launch_bounds__(64 * NW, 1)
+template <int HW, int TG, int NST>
+__global__ __launch_bounds__(64 * HW * TG, 1)
 void attn_mla_kernel(AttnArgs a) {
   constexpr int DQK = 576, DV = 512;
+  constexpr int NW = HW * TG;
   constexpr int P = DQK / 8;                              // 16-byte pieces per token
   constexpr int PP = TileRow<P>::PP;                      // pieces per LDS row
   constexpr int NL = ((kChunk - 1) * PP + P + 63) / 64;   // 64-lane loads per chunk
   constexpr int TILE = NL * 64 * 8;                       // bf16 per chunk tile
-  constexpr int LPW_MAX = (NL + NW - 1) / NW;
-  constexpr int LPW_MIN = NL / NW;
-  constexpr int NL_REM = NL % NW;
+  constexpr int LPW_MAX = (NL + HW - 1) / HW;             // a group's loads per head wave
+  constexpr int LPW_MIN = NL / HW;
+  constexpr int NL_REM = NL % HW;
   constexpr int NKK = DQK / 16;  // QK k-steps
   constexpr int NDV = DV / 32;   // PV output tiles
   static_assert(NST >= 2 && NST <= 4 && (NST - 2) * LPW_MAX < 64, "pipeline depth");
-  __shared__ __align__(16) uint16_t s_kv[NST * TILE];
+  static_assert(TG == 1 || TG == 2, "token groups");
+  static_assert(TG == 1 || TG * NST * TILE * 2 >= HW * (64 * 64 * 16 + 32 * 8),
+                "the tiles hold one group's results for the merge");
+  __shared__ __align__(16) uint16_t s_kv[TG * NST * TILE];
   __shared__ int32_t s_idx[kMaxSplitRecords];         // the split's record indices, -1 = skip
   __shared__ uint32_t s_valid[kMaxSplitTokens / 32];  // bit t of word c: token 32c+t attends
   __shared__ int s_fallback;                           // some score outgrew its reference
@@ -530,6 +537,8 @@ void attn_mla_kernel(AttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
+  const int hg = wave % HW, tg = wave / HW;  // head wave within the token group, token group
+  uint16_t* s_tiles = s_kv + tg * NST * TILE;
 
   const int tok_begin = split * a.split_tokens;
   const int tok_end = min(a.n_tok, tok_begin + a.split_tokens);
@@ -546,26 +555,30 @@ void attn_mla_kernel(AttnArgs a) {
 
   if (tid == 0) s_fallback = 0;
   __syncthreads();  // s_idx is ready
-  const int n_it = (tok_end - tok_begin + kChunk - 1) / kChunk;
-  for (int base = wave * 64; base < n_it * kChunk; base += 64 * NW) {
+  // iteration `it` of token group g covers the split's chunk it * TG + g
+  const int n_it = (tok_end - tok_begin + kChunk * TG - 1) / (kChunk * TG);
+  // every chunk the groups iterate over gets its word, including a last one wholly past the
+  // split end (all zero)
+  const int span = n_it * TG * kChunk;
+  for (int base = wave * 64; base < span; base += 64 * NW) {
     const int tk = tok_begin + base + lane;
     const bool ok = tk < tok_end && s_idx[(tk >> a.tpr_shift) - rec_begin] >= 0;
     const uint64_t m = __ballot(ok);
     if (lane == 0) {
       s_valid[base >> 5] = (uint32_t)m;
-      if (base + 32 < n_it * kChunk) s_valid[(base >> 5) + 1] = (uint32_t)(m >> 32);
+      if (base + 32 < span) s_valid[(base >> 5) + 1] = (uint32_t)(m >> 32);
     }
   }
 
-  const int w_s = __builtin_amdgcn_readfirstlane(wave);
+  const int w_s = __builtin_amdgcn_readfirstlane(hg);
   const int n_loads = w_s < NL_REM ? LPW_MAX : LPW_MIN;
   const int j0 = w_s * LPW_MIN + min(w_s, NL_REM);
+  auto chunk_base = [&](int it) { return tok_begin + (it * TG + tg) * kChunk; };
   auto issue = [&](int it, int buf) {
-    stage_chunk<P, PP, LPW_MAX>(s_kv + buf * TILE, s_idx, pool_u, tok_begin + it * kChunk,
-                                tok_end, rec_begin, a.tpr_shift, a.R, a.token_bytes, j0,
-                                n_loads);
+    stage_chunk<P, PP, LPW_MAX>(s_tiles + buf * TILE, s_idx, pool_u, chunk_base(it), tok_end,
+                                rec_begin, a.tpr_shift, a.R, a.token_bytes, j0, n_loads);
   };
-  const int head0 = hb * 32 * NW + wave * 32;  // first head of this wave
+  const int head0 = hb * 32 * HW + hg * 32;  // first head of this wave
   const int head = head0 + col;
   const bool head_ok = head < a.H;
   f32x16 o[NDV];
@@ -644,8 +657,8 @@ void attn_mla_kernel(AttnArgs a) {
     // every wave is past its reads of buffer (it-1) % NST: refill it with chunk it+NST-1
     if (it + NST - 1 < n_it) issue(it + NST - 1, (it + NST - 1) % NST);
 
-    const uint16_t* tile = s_kv + (it % NST) * TILE;
-    const int cbase = tok_begin + it * kChunk;
+    const uint16_t* tile = s_tiles + (it % NST) * TILE;
+    const int cbase = chunk_base(it);
 
     // ---- scores: S^T for the chunk's 32 tokens x this wave's 32 heads ----
     // K operand reads run KD k-steps ahead of the MFMAs (a small register ring; the
@@ -699,14 +712,68 @@ void attn_mla_kernel(AttnArgs a) {
   }
   wait_loads_and_barrier<0>();  // no staging in flight; s_fallback is final
   if (s_fallback) {
-    mla_split_exact(a, s_idx, s_valid, unit, split, tok_begin, tok_end, rec_begin, head0);
+    if (tg == 0)  // the whole split, for this wave's heads
+      mla_split_exact(a, s_idx, s_valid, unit, split, tok_begin, tok_end, rec_begin, head0);
     return;
   }
-
   // ---- partial results of this split, in the accumulator layout (see mla_part_offset) ----
-  if (head0 < a.H) {
-    float* po = a.part_o + ((int64_t)unit * a.n_parts + split) * a.Hp * DV +
-                (int64_t)(head0 >> 5) * 32 * DV + lane * 4;
+  float* po = a.part_o + ((int64_t)unit * a.n_parts + split) * a.Hp * DV +
+              (int64_t)(head0 >> 5) * 32 * DV + lane * 4;
+  if constexpr (TG == 2) {
+    // The two token groups' results merged per head on the way out, through LDS (the tiles
+    // are free now): group 1 leaves its accumulators and (reference max, sum) there; group 0
+    // rescales both to the larger reference and adds, in that fixed order, into the stores.
+    f32x4* s_o = reinterpret_cast<f32x4*>(s_kv) + hg * 64 * 64;  // [64 regs / 4][64 lanes]
+    float2* s_ml = reinterpret_cast<float2*>(reinterpret_cast<f32x4*>(s_kv) + HW * 64 * 64);
+    if (tg == 1) {
+#pragma unroll
+      for (int n = 0; n < NDV; ++n) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          s_o[(n * 4 + q) * 64 + lane] =
+              f32x4{o[n][4 * q], o[n][4 * q + 1], o[n][4 * q + 2], o[n][4 * q + 3]};
+      }
+      if (lane < 32) s_ml[hg * 32 + col] = make_float2(m_run, l_run);
+    }
+    __syncthreads();
+    if (tg == 1) return;
+    const float2 other = s_ml[hg * 32 + col];
+    const float m_new = fmaxf(m_run, other.x);
+    // a group without a valid token has m = -inf, O = 0, l = 0 and contributes nothing
+    const float a0 = m_run == -INFINITY ? 0.f : exp2f(m_run - m_new);
+    const float a1 = other.x == -INFINITY ? 0.f : exp2f(other.x - m_new);
+    l_run = l_run * a0 + other.y * a1;
+    m_run = m_new;
+    if (head0 < a.H) {
+      // Accumulators are read with explicit v_accvgpr_read (arithmetic on them would make the
+      // compiler move all of O into VGPRs and spill); the reads are assembly, so the wait states
+      // after the last MFMA that wrote them are given here (the barrier above already separates
+      // them by far more).
+      asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+      // accumulator row 4q + e of a lane is head 8q + 4 half + e of the wave's 32
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float s0[4], s1[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          s0[e] = __shfl(a0, 8 * q + 4 * half + e, 64);
+          s1[e] = __shfl(a1, 8 * q + 4 * half + e, 64);
+        }
+#pragma unroll
+        for (int n = 0; n < NDV; ++n) {
+          const f32x4 v = s_o[(n * 4 + q) * 64 + lane];
+          f32x4 r;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float x;
+            asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(x) : "a"(o[n][4 * q + e]));
+            r[e] = x * s0[e] + v[e] * s1[e];
+          }
+          *reinterpret_cast<f32x4*>(po + (n * 4 + q) * 256) = r;
+        }
+      }
+    }
+  } else if (head0 < a.H) {
 #pragma unroll
     for (int n = 0; n < NDV; ++n) {
 #pragma unroll
@@ -879,11 +946,11 @@ void launch_partial(const AttnArgs& args, hipStream_t stream) {
                      dim3(64 * HW * TW), 0, stream, args);
 }
 
-template <int NW, int NST>
+template <int HW, int TG, int NST>
 void launch_mla(const AttnArgs& args, hipStream_t stream) {
   const int nwg_pad = (args.n_wg + 7) & ~7;
-  hipLaunchKernelGGL((attn_mla_kernel<NW, NST>), dim3(nwg_pad + args.pf_wg), dim3(64 * NW), 0,
-                     stream, args);
+  hipLaunchKernelGGL((attn_mla_kernel<HW, TG, NST>), dim3(nwg_pad + args.pf_wg),
+                     dim3(64 * HW * TG), 0, stream, args);
 }
 
 bool is_mla(const hisparse_attn_desc_t& d) {
@@ -902,22 +969,40 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
   AttnPlan p{};
   p.n_tok = top_k * attn->tokens_per_record;
   if (is_mla(*attn)) {
-    // 32 heads per wave, up to 4 waves (128 heads) per workgroup when that still gives about
-    // a workgroup per CU with at least two chunks per split; otherwise 2 waves, which measured
-    // faster than 1 or 4 for a single 128-head unit (more loads in flight per CU than 1 wave,
-    // twice the workgroups of 4)
-    const int64_t split_cap = std::max(1, p.n_tok / (2 * kChunk));
-    if (H <= 32) p.hw = 1;
-    else if (H > 64 && (int64_t)units * ((H + 127) / 128) * split_cap >= kTargetWorkgroups) p.hw = 4;
-    else p.hw = 2;
+    // 32 heads per wave; above 32 heads, 2 head waves (64 heads) per workgroup. With 16 or more
+    // workgroup columns (units x head blocks) there are enough of them for two token groups per
+    // workgroup: twice the tokens per partial result at the same workgroup count, which halves
+    // the split partials (fp32, 2 KB per head) and the merge. Measured alone, attention + merge
+    // over units of 128 heads (us, best split count): 8 units 27.4 against 28.7, 16 units 34.5
+    // against 45.9 (4 head waves, 16 splits, the previous plan), 32 units 50.8 against 55.5;
+    // below 8 units one token group is faster (2 units 18.7 against 20.7).
+    // With HISPARSE_ATTN_BESIDE_FETCH (another stream's host-link fetch shares the GPU, whose
+    // slow host reads sit in the CUs' memory pipelines) the plan keeps three chunks in flight
+    // per workgroup instead: one token group, 4 head waves when that still gives about a
+    // workgroup per CU with two chunks per split. Inside the two-micro-batch decode step of 16
+    // units of 128 heads, that attention takes 39.7 us against 56.4 with two token groups (the
+    // step 1.754 against 1.777 ms), although alone it is the slower of the two.
+    if (H <= 32) {
+      p.hw = 1;
+      p.tg = 1;
+    } else if (attn->flags & HISPARSE_ATTN_BESIDE_FETCH) {
+      const int64_t split_cap = std::max(1, p.n_tok / (2 * kChunk));
+      p.hw = (H > 64 && (int64_t)units * ((H + 127) / 128) * split_cap >= kTargetWorkgroups) ? 4 : 2;
+      p.tg = 1;
+    } else {
+      p.hw = 2;
+      p.tg = (int64_t)units * ((H + 63) / 64) >= 16 ? 2 : 1;
+    }
     p.tw = 1;
     p.hb = (H + 32 * p.hw - 1) / (32 * p.hw);
   } else {              // up to 64 heads per workgroup, 16 per wave
     p.hw = H > 32 ? 4 : (H > 16 ? 2 : 1);
     p.tw = 4 / p.hw;
+    p.tg = 1;
     p.hb = (H + 16 * p.hw - 1) / (16 * p.hw);
   }
-  const int chunk = kChunk * p.tw;
+  // a split is a whole number of the workgroup's chunk rounds
+  const int chunk = kChunk * (is_mla(*attn) ? p.tg : p.tw);
   const int max_splits = (p.n_tok + chunk - 1) / chunk;
   int splits;
   if (attn->num_splits > 0) {
@@ -925,18 +1010,18 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
   } else {
     // at most one workgroup per CU (a workgroup holds a CU's LDS, so one more would wait for a
     // second round), and enough chunks per split for the load pipeline to reach steady state.
-    // For latent attention the split partials (fp32, 2 KB per head and split) grow with the
-    // splits, and measured over 1..32 units of 128 heads, longer splits win as the grid gets
-    // more workgroup columns: 2 chunks per split up to 4 columns, 4 up to 16, 8 beyond (12
-    // units: 39 against 55 us with 22 two-chunk splits). At 16 columns 8-chunk splits are 7%
-    // faster alone but a third slower beside a concurrent host-link fetch (half the
-    // workgroups, each twice as long), the case of two micro-batches taking turns.
+    // For latent attention with one token group the split partials (fp32, 2 KB per head and
+    // split) grow with the splits, and longer splits win as the grid gets more workgroup
+    // columns: 2 chunks per split up to 4 columns, 4 up to 16, 8 beyond (12 units of 128 heads:
+    // 39 against 55 us with 22 two-chunk splits).
     const int per_split = units * p.hb;
     splits = std::max(1, kTargetWorkgroups / per_split);
     int chunks_per_split = 4;
     if (is_mla(*attn)) chunks_per_split = per_split <= 4 ? 2 : (per_split <= 16 ? 4 : 8);
     // a call too small to give even 64 such workgroups is all latency: one chunk per split
     if (is_mla(*attn) && (int64_t)per_split * (p.n_tok / (2 * chunk)) < 64) chunks_per_split = 1;
+    // two token groups: one workgroup per CU, however few chunks each group gets
+    if (is_mla(*attn) && p.tg == 2) chunks_per_split = 1;
     const int min_work_splits = std::max(1, p.n_tok / (chunks_per_split * chunk));
     splits = std::max(1, std::min({splits, max_splits, min_work_splits}));
   }
@@ -973,7 +1058,7 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
     // workgroups of the attention kernel's size, on the CUs the attention leaves idle
     // (a workgroup of these kernels holds a CU's LDS, so replay and attention never share a
     // CU's memory pipeline)
-    const int bd = 64 * p.hw * (is_mla(attn) ? 1 : p.tw);
+    const int bd = 64 * p.hw * (is_mla(attn) ? p.tg : p.tw);
     const int64_t pairs = (int64_t)prefetch->units * prefetch->n_layers;
     const int64_t n_attn = (int64_t)units * p.n_wg_splits * p.hb;
     const int64_t idle = std::max<int64_t>(0, kTargetWorkgroups - ((n_attn + 7) & ~7LL));
@@ -1013,9 +1098,12 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
 
   if (is_mla(attn)) {
     switch (p.hw) {
-      case 1: launch_mla<1, 3>(a, stream); break;
-      case 2: launch_mla<2, 4>(a, stream); break;
-      default: launch_mla<4, 4>(a, stream); break;
+      case 1: launch_mla<1, 1, 3>(a, stream); break;
+      case 2:
+        if (p.tg == 2) launch_mla<2, 2, 2>(a, stream);
+        else launch_mla<2, 1, 4>(a, stream);
+        break;
+      default: launch_mla<4, 1, 4>(a, stream); break;
     }
   } else {
     switch (p.hw) {

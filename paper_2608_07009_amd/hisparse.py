@@ -29,6 +29,7 @@ HISPARSE_FETCH_SDMA = 1
 HISPARSE_FETCH_NONE = 2
 
 HISPARSE_ATTN_DEFER_MERGE = 1
+HISPARSE_ATTN_BESIDE_FETCH = 2
 HISPARSE_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 HISPARSE_HOST_COHERENT = 0

@@ -18,9 +18,9 @@ def log(msg: str) -> None:
     sys.stdout.flush()
 
 
-def attn_desc(w: W.Workload, num_splits: int = 0) -> hs.AttnDesc:
+def attn_desc(w: W.Workload, num_splits: int = 0, flags: int = 0) -> hs.AttnDesc:
     return hs.AttnDesc(w.q_heads, w.d_qk, w.d_v, w.v_offset, w.tokens_per_record, num_splits,
-                       w.scale, 0)
+                       w.scale, flags)
 
 
 class Run:

@@ -74,7 +74,7 @@ def test_invalid_descriptors(field, value, status):
     (dict(q_heads=0), hs.HISPARSE_ERR_INVALID_ARG),
     (dict(scale=0.0), hs.HISPARSE_ERR_INVALID_ARG),
     (dict(num_splits=-1), hs.HISPARSE_ERR_INVALID_ARG),
-    (dict(flags=2), hs.HISPARSE_ERR_INVALID_ARG),
+    (dict(flags=4), hs.HISPARSE_ERR_INVALID_ARG),          # an undefined flag bit
 ])
 def test_invalid_attention_descriptors(change, status):
     w = W.workload(2)

@@ -28,19 +28,20 @@ def rel_l2(a, b):
     return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30))
 
 
-def decode(run, layer, q_dev, slots, ws):
+def decode(run, layer, q_dev, slots, ws, flags=0):
     w = run.w
     out = torch.empty((w.units, w.q_heads, w.d_v), dtype=torch.float32, device=run.dev)
-    hs.hisparse_sparse_decode(run.cache.handle, layer, q_dev, slots, out, attn_desc(w), ws,
-                              ws.numel(), run.stream)
+    hs.hisparse_sparse_decode(run.cache.handle, layer, q_dev, slots, out,
+                              attn_desc(w, 0, flags), ws, ws.numel(), run.stream)
     return out
 
 
-def decode_pool(pool_dev, rec_per_unit, w, q_dev, idx_dev, ws, num_splits=0, units=None):
+def decode_pool(pool_dev, rec_per_unit, w, q_dev, idx_dev, ws, num_splits=0, units=None,
+                flags=0):
     units = w.units if units is None else units
     out = torch.empty((units, w.q_heads, w.d_v), dtype=torch.float32, device=pool_dev.device)
     hs.hisparse_sparse_decode_pool(pool_dev, rec_per_unit, w.record_bytes, units, w.k, q_dev,
-                                   idx_dev, out, attn_desc(w, num_splits), ws, ws.numel(),
+                                   idx_dev, out, attn_desc(w, num_splits, flags), ws, ws.numel(),
                                    torch.cuda.current_stream())
     return out
 
@@ -55,17 +56,24 @@ SAMPLE_UNITS = {1: [0], 2: [0, 17, 31], 3: [0, 29, 63], 4: [0, 40, 63], 5: [0]}
 STEPS = {1: 12, 2: 3, 3: 6, 4: 4, 5: 3}
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
-def test_attention_cache_vs_resident_vs_oracle(cfg):
+BESIDE = hs.HISPARSE_ATTN_BESIDE_FETCH
+
+
+@pytest.mark.parametrize("cfg,flags", [(1, 0), (2, 0), (2, BESIDE), (3, 0), (4, 0), (5, 0),
+                                       (5, BESIDE)])
+def test_attention_cache_vs_resident_vs_oracle(cfg, flags):
+    """Both latent-attention plans (two token groups per workgroup by default; one token group
+    with deeper load pipelines under HISPARSE_ATTN_BESIDE_FETCH)."""
     steps = STEPS[cfg]
     w = W.fit_pinned(W.workload(cfg))
     layer = w.anchors[-1]
-    log(f"test_attention cfg={cfg} {w.name} layer={layer} steps={steps}")
+    log(f"test_attention cfg={cfg} flags={flags} {w.name} layer={layer} steps={steps}")
     run = Run(w, steps, layers_to_fill=[layer])
     try:
         host = run.cache.host_view(layer)                   # [U][L][R] pinned
         resident = torch.from_numpy(host.reshape(-1)).to(run.dev)  # full KV on the device
-        ws_bytes = hs.hisparse_decode_workspace_bytes(w.units, w.k, w.record_bytes, attn_desc(w))
+        ws_bytes = hs.hisparse_decode_workspace_bytes(w.units, w.k, w.record_bytes,
+                                                      attn_desc(w, 0, flags))
         ws = torch.empty(ws_bytes, dtype=torch.uint8, device=run.dev)
         a = layer // w.share_group
         for t in range(steps):
@@ -73,8 +81,8 @@ def test_attention_cache_vs_resident_vs_oracle(cfg):
             q_host = W.queries(w, t, layer)
             q_dev = torch.from_numpy(q_host.view(np.int16)).to(run.dev)
             sel_dev = run.sel[t, a * w.units:(a + 1) * w.units]
-            out_cache = decode(run, layer, q_dev, run.slots[layer], ws)
-            out_res = decode_pool(resident, w.L, w, q_dev, sel_dev, ws)
+            out_cache = decode(run, layer, q_dev, run.slots[layer], ws, flags)
+            out_res = decode_pool(resident, w.L, w, q_dev, sel_dev, ws, flags=flags)
             torch.cuda.synchronize()
             assert torch.equal(out_cache, out_res), f"placement changed the output at step {t}"
             if t in (0, steps - 1):
@@ -95,11 +103,15 @@ def _bf16(rng, shape):
     return t.view(torch.int16).numpy().view(np.uint16)
 
 
-@pytest.mark.parametrize("kind,H,k,tpr,splits", [
-    ("mla", 16, 37, 1, 0), ("mla", 128, 77, 1, 3), ("mla", 40, 300, 1, 0), ("mla", 1, 5, 1, 0),
-    ("gqa", 4, 9, 16, 0), ("gqa", 16, 3, 64, 2), ("gqa", 24, 50, 1, 0), ("gqa", 64, 13, 4, 1),
+@pytest.mark.parametrize("kind,H,k,tpr,splits,units", [
+    ("mla", 16, 37, 1, 0, 3), ("mla", 128, 77, 1, 3, 3), ("mla", 40, 300, 1, 0, 3),
+    ("mla", 1, 5, 1, 0, 3),
+    # 16 or more workgroup columns: latent attention with two token groups per workgroup
+    ("mla", 128, 301, 1, 0, 8), ("mla", 200, 97, 1, 3, 6), ("mla", 128, 64, 1, 0, 9),
+    ("gqa", 4, 9, 16, 0, 3), ("gqa", 16, 3, 64, 2, 3), ("gqa", 24, 50, 1, 0, 3),
+    ("gqa", 64, 13, 4, 1, 3),
 ])
-def test_attention_ragged_and_padding(kind, H, k, tpr, splits):
+def test_attention_ragged_and_padding(kind, H, k, tpr, splits, units):
     """Ragged token counts (not multiples of the 32-token chunk), padding entries, a unit with
     no valid record, head counts that are not multiples of 16, explicit split counts."""
     rng = np.random.default_rng(zlib.crc32(f"{kind}-{H}-{k}-{tpr}".encode()))
@@ -107,7 +119,7 @@ def test_attention_ragged_and_padding(kind, H, k, tpr, splits):
         d_qk, d_v, voff, te, scale = 576, 512, 0, 576, 1 / np.sqrt(192)
     else:
         d_qk, d_v, voff, te, scale = 128, 128, 128, 256, 1 / np.sqrt(128)
-    units, n_rec = 3, max(97, k + 40)
+    n_rec = max(97, k + 40)
     R = te * tpr * 2
     w = W.workload(1 if kind == "mla" else 3, q_heads=H, k=k, d_qk=d_qk, d_v=d_v, v_offset=voff,
                    tokens_per_record=tpr, record_bytes=R, scale=float(scale))
@@ -140,14 +152,15 @@ def test_attention_ragged_and_padding(kind, H, k, tpr, splits):
     assert out.tobytes() == out_p.tobytes()
 
 
-@pytest.mark.parametrize("kind,H,splits", [("mla", 128, 1), ("mla", 20, 2), ("gqa", 16, 1),
-                                           ("gqa", 64, 0)])
-def test_attention_wide_score_range(kind, H, splits):
+@pytest.mark.parametrize("kind,H,splits,units", [("mla", 128, 1, 2), ("mla", 20, 2, 2),
+                                                 ("mla", 128, 1, 8), ("gqa", 16, 1, 2),
+                                                 ("gqa", 64, 0, 2)])
+def test_attention_wide_score_range(kind, H, splits, units):
     """Scores that keep growing along the selection (by far more than the kernels' reference
-    slack within one split) exercise the rescale / exact-fallback paths: still within the
-    oracle's tolerance, still independent of placement."""
+    slack within one split) exercise the rescale / exact-fallback paths (for latent attention
+    with one and with two token groups per workgroup): still within the oracle's tolerance,
+    still independent of placement."""
     rng = np.random.default_rng(zlib.crc32(f"wide-{kind}-{H}-{splits}".encode()))
-    units = 2
     if kind == "mla":
         d_qk, d_v, voff, te, scale, tpr, k = 576, 512, 0, 576, 1 / np.sqrt(192), 1, 256
         growth = slice(512, 576)      # the rope dims carry the growth; values stay N(0,1)

@@ -66,17 +66,18 @@ def test_noalloc_matches_workspace_decode_on_consecutive_calls():
 
 
 def test_noalloc_refuses_oversize_and_deferred_calls():
-    w = W.workload(2, num_requests=2, num_layers=1)
+    w = W.workload(2, num_requests=8, num_layers=1)
     run = Run(w, steps=1)
     try:
         dev = run.dev
         run.resolve_step(0)
-        # 256 heads in 64 explicit splits: 2 units x 64 x 256 x 2 KiB of partials > 64 MiB
+        # 256 heads in as many splits as the plan allows (at least 16 of 2048 tokens): 8 units x
+        # >= 16 x 256 x 2 KiB of partials > 64 MiB
         big = hs.AttnDesc(256, 576, 512, 0, 1, 64, w.scale, 0)
-        assert hs.hisparse_decode_workspace_bytes(2, w.k, w.record_bytes, big) > \
+        assert hs.hisparse_decode_workspace_bytes(w.units, w.k, w.record_bytes, big) > \
             hs.HISPARSE_NOALLOC_SCRATCH_BYTES
-        q = torch.zeros((2, 256, 576), dtype=torch.int16, device=dev)
-        out = torch.empty((2, 256, 512), dtype=torch.float32, device=dev)
+        q = torch.zeros((w.units, 256, 576), dtype=torch.int16, device=dev)
+        out = torch.empty((w.units, 256, 512), dtype=torch.float32, device=dev)
         with pytest.raises(hs.HisparseError) as e:
             hs.hisparse_sparse_decode_noalloc(run.cache.handle, 0, q, run.slots[0], out, big,
                                               run.stream)
