@@ -90,6 +90,13 @@ def parse():
                          "the end of the resolve on; 'batched' (not realisable in a model: "
                          "later layers' queries depend on earlier layers) decodes the group's "
                          "layers in one attention launch")
+    ap.add_argument("--merge-replay-share", type=int, default=0, metavar="S",
+                    help="overlap schedule: the merge after layer l's attention starts the "
+                         "replay into layer l+2 of the share group (the first S/256 of each "
+                         "unit's plan, hisparse_attention_merge_prefetch) and layer l+1's "
+                         "attention carries the rest; 0 = merges carry nothing (measured "
+                         "faster: each launch that carries part of a replay pays the host "
+                         "reads' ramp again)")
     ap.add_argument("--append", action="store_true",
                     help="decode loop with a growing context: after each share group's "
                          "attention, write the step's generated record of every layer through "
@@ -683,6 +690,9 @@ def main() -> int:
     f_append, f_speculate = L.hisparse_append, L.hisparse_speculate
     f_decode_layers, f_fetch_group = L.hisparse_sparse_decode_layers, L.hisparse_fetch_group
     f_merge = L.hisparse_attention_merge
+    f_decode_prefetch_part = L.hisparse_sparse_decode_prefetch_part
+    f_merge_prefetch = L.hisparse_attention_merge_prefetch
+    share = max(0, min(256, args.merge_replay_share))
     rec = hip.L.hipEventRecord
     wait = hip.L.hipStreamWaitEvent
 
@@ -772,14 +782,22 @@ def main() -> int:
         else:
             # overlap (Section 3.5), on one stream: the anchor's fetch, then each layer's
             # attention launch carries the replay of the plan into the next shared layer, so
-            # layer l+1's misses cross the host link while layer l attends
+            # layer l+1's misses cross the host link while layer l attends; with a merge share,
+            # the merge after layer l's attention already starts the replay into layer l+2 and
+            # layer l+1's attention carries the rest, so the link keeps moving through merges
             transfer("fetch", f_fetch, h, a, ms)
             layers = [a] + shared
             for i, l in enumerate(layers[:-1]):
-                call("sparse_decode_prefetch", ms, ev, spans, f_decode_prefetch, h, l, qv[l],
-                     mb.slot_p[a], mb.out_p[l], ad_ref, mb.ws.data_ptr(), mb.ws_bytes, a,
-                     layers[i + 1], 1, ms)
-                merge(mb.U, mb.out_p[l])
+                lo = share if (share and i >= 1) else 0  # begun by the previous merge
+                call("sparse_decode_prefetch", ms, ev, spans, f_decode_prefetch_part, h, l,
+                     qv[l], mb.slot_p[a], mb.out_p[l], ad_ref, mb.ws.data_ptr(), mb.ws_bytes,
+                     a, layers[i + 1], 1, lo, 256, ms)
+                if share and i + 2 < len(layers):
+                    call("attention_merge_prefetch", ms, ev, spans, f_merge_prefetch, h, ad_ref,
+                         mb.out_p[l], mb.ws.data_ptr(), mb.ws_bytes, a, layers[i + 2], 1, 0,
+                         share, ms)
+                else:
+                    merge(mb.U, mb.out_p[l])
             decode(layers[-1])
 
     def step(t, ev=None, spans=None, sel_override=None, q_override=None, fork=True, join=True,
@@ -890,7 +908,7 @@ def main() -> int:
     # (kernel averages, rates);
     # the timed region above is unaffected and covers every step.
     IO_KINDS = ("fetch", "prefetch_replay", "fetch_group", "sparse_decode_prefetch",
-                "speculate")
+                "speculate", "attention_merge_prefetch")
     step_spans = []
     for si, (r0, _, first) in enumerate(step_refs):
         last = step_refs[si + 1][2] if si + 1 < len(step_refs) else len(spans)
@@ -963,6 +981,16 @@ def main() -> int:
     carried_bytes = replay_bytes if n_pf else 0  # replays inside attention launches
     if n_pf:
         replay_bytes = 0
+    # the share of the replays that merge launches carried: per merge, the first share/256 of
+    # each unit's plan entries (floor), of the replay into layer l+2
+    t_mpf, n_mpf = kernel("attention_merge_prefetch")
+    merge_carried = 0
+    if n_mpf:
+        m_units = c[:, [a for a, sh in groups if len(sh) >= 2], :, 1]  # [steps][groups][units]
+        for gi, (a, sh) in enumerate([g for g in groups if len(g[1]) >= 2]):
+            merge_carried += int(((m_units[:, gi, :] * share) >> 8).sum()) * (len(sh) - 1)
+        merge_carried *= R
+        carried_bytes -= merge_carried
     moves_data = fetch != hs.HISPARSE_FETCH_NONE
     kernels = {}
     # resolve tables: integer metadata work per unit (algorithmic bytes):
@@ -1003,6 +1031,13 @@ def main() -> int:
             "GBps": carried_bytes / t_pf / 1e9,
             "note": "attention of one layer with the replay into the next shared layer in the "
                     "same launch; also counted in sparse_decode"}
+    if n_mpf and moves_data:
+        kernels["attention_merge_prefetch"] = {
+            "launches": n_mpf, "avg_us": t_mpf / n_mpf * 1e6,
+            "replay_bytes_per_launch": merge_carried / n_mpf,
+            "GBps": merge_carried / t_mpf / 1e9,
+            "note": "merge of one layer's attention with the first part of the replay into the "
+                    "layer after next in the same launch"}
     t_spc, n_spc = kernel("speculate")
     spec_bytes = 0
     if n_spc:
@@ -1085,11 +1120,12 @@ def main() -> int:
         roof = {"kernel": dom, "bound": "hbm", "achieved": kd["hbm_GBps"], "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": kd["hbm_GBps"] / HBM_PEAK_GBPS, "traffic": None}
 
-    link_bytes = fetch_bytes + replay_bytes + group_bytes + carried_bytes + spec_bytes
+    link_bytes = (fetch_bytes + replay_bytes + group_bytes + carried_bytes + spec_bytes +
+                  merge_carried)
     miss_gbps = link_bytes / io_busy / 1e9 if (io_busy and moves_data) else None
-    # share of the span pass's step time in which some host-link transfer ran
-    kept_ms = sum(step_ms[si] for si in kept)
-    link_busy = io_busy * 1e3 / kept_ms if (kept_ms and moves_data) else None
+    # time per step in which some host-link transfer ran (span pass), a share of the timed
+    # region's step time below
+    io_busy_ms_per_step = io_busy * 1e3 / max(1, Ks)
 
     # the same steps replayed from a captured HIP graph (cold reset, same warmup)
     graph = None
@@ -1200,6 +1236,8 @@ def main() -> int:
     value = served / wall
     # the host link's rate over the whole step of the timed region (not only inside transfers)
     link_step_gbps = (link_bytes / max(1, Ks)) / (wall / K) / 1e9 if moves_data else None
+    link_busy = (min(1.0, io_busy_ms_per_step / (wall / K * 1e3))
+                 if (moves_data and io_busy) else None)
 
     result = {
         "metric": "resolved selections/s + miss-fetch GB/s (% host-link peak), decode tokens/s",
@@ -1222,6 +1260,7 @@ def main() -> int:
                    "share_group": G, "q_heads": w.q_heads, "fetch": args.fetch,
                    "speculate": args.speculate, "xlayer_overlap": args.xlayer_overlap,
                    "host_memory": args.host_memory, "mode": mode,
+                   "merge_replay_share": share if args.schedule == "overlap" else None,
                    "attn_plan": "beside-fetch" if beside else "own-gpu",
                    "steps_per_graph": graph["steps_per_graph"] if graph else None},
         "decode_tokens_per_s": w.num_requests * K / wall,

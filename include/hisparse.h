@@ -390,6 +390,35 @@ hisparse_status_t hisparse_sparse_decode_prefetch(hisparse_cache_t cache, int32_
                                                   int32_t anchor_layer, int32_t first_shared,
                                                   int32_t num_shared, void* stream);
 
+/* [async] hisparse_sparse_decode_prefetch carrying only part of the replay: entries
+ * [m * part_begin / 256, m * part_end / 256) of each unit's plan of m entries, 0 <= part_begin
+ * <= part_end <= 256 (0, 256: all of it, i.e. hisparse_sparse_decode_prefetch). Calls with
+ * adjacent ranges, e.g. one carried by hisparse_attention_merge_prefetch and the rest by this
+ * call, copy every planned record exactly once. Same ordering rules and errors. */
+hisparse_status_t hisparse_sparse_decode_prefetch_part(
+    hisparse_cache_t cache, int32_t layer, const void* d_q, const int32_t* d_slots,
+    float* d_out, const hisparse_attn_desc_t* attn, void* d_workspace, size_t workspace_bytes,
+    int32_t anchor_layer, int32_t first_shared, int32_t num_shared, int32_t part_begin,
+    int32_t part_end, void* stream);
+
+/* [async] hisparse_attention_merge of a deferred attention call made on `cache` (its units, top
+ * k and record size; attn as in that call) whose launch also carries part of an exact-prefetch
+ * replay (Section 3.5): entries [m * part_begin / 256, m * part_end / 256) of each unit's plan of
+ * `anchor_layer`, into shared layers [first_shared, first_shared + num_shared), in extra
+ * workgroups beside the merge. For a decode loop whose every attention call carries the replay
+ * into a later shared layer, the merges would otherwise leave the host link idle; starting the
+ * next-but-one layer's replay in them keeps it busy, and the attention call that follows carries
+ * the rest (hisparse_sparse_decode_prefetch_part). Ordering rules of hisparse_prefetch_layer
+ * apply to the replay. HISPARSE_ERR_INVALID_ARG for a replay range
+ * hisparse_sparse_decode_prefetch_part would refuse. */
+hisparse_status_t hisparse_attention_merge_prefetch(hisparse_cache_t cache,
+                                                    const hisparse_attn_desc_t* attn,
+                                                    float* d_out, const void* d_workspace,
+                                                    size_t workspace_bytes, int32_t anchor_layer,
+                                                    int32_t first_shared, int32_t num_shared,
+                                                    int32_t part_begin, int32_t part_end,
+                                                    void* stream);
+
 /* [async] Sparse decode attention of layers [first_layer, first_layer + num_layers) of one
  * share group in a single launch (Section 3.5: the shared layers read their records through
  * the anchor's slots; batching them is this library's scheduling choice, the result per layer

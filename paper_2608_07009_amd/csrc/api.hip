@@ -502,20 +502,25 @@ hisparse::FetchArgs fetch_args(hisparse_cache_t c, int32_t anchor, int32_t targe
   f.k = c->desc.top_k;
   f.R = (int32_t)R;
   f.units = nu;
+  f.part_lo = 0;
+  f.part_hi = 256;
   return f;
 }
 
 // Copy the records of `anchor`'s latest miss plan from each target layer's host pool into
 // its GPU cache, for targets [target, target + n_layers) and units [u0, u0 + nu) (target ==
 // anchor: the demand fetch; a shared layer: the prefetch replay).
+// Entries [m * part_lo / 256, m * part_hi / 256) of each unit's plan of m entries only.
 hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t target,
                                 hipStream_t stream, int32_t u0 = 0, int32_t nu = -1,
-                                int32_t n_layers = 1) {
+                                int32_t n_layers = 1, int32_t part_lo = 0,
+                                int32_t part_hi = 256) {
   if (nu < 0) nu = c->units - u0;
-  if (c->desc.fetch == HISPARSE_FETCH_NONE || nu == 0) return HISPARSE_OK;
+  if (c->desc.fetch == HISPARSE_FETCH_NONE || nu == 0 || part_lo >= part_hi) return HISPARSE_OK;
   if (c->desc.fetch == HISPARSE_FETCH_SDMA && n_layers > 1) {
     for (int32_t j = 0; j < n_layers; ++j) {
-      const hisparse_status_t st = enqueue_fetch(c, anchor, target + j, stream, u0, nu, 1);
+      const hisparse_status_t st =
+          enqueue_fetch(c, anchor, target + j, stream, u0, nu, 1, part_lo, part_hi);
       if (st != HISPARSE_OK) return st;
     }
     return HISPARSE_OK;
@@ -540,7 +545,8 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
     size_t n = 0;
     for (size_t u = (size_t)u0; u < u_end; ++u) {
       const int2* pl = c->h_plan + u * K;
-      for (int32_t i = 0; i < c->h_plan_count[u]; ++i) {
+      const int32_t m = c->h_plan_count[u];
+      for (int32_t i = (m * part_lo) >> 8; i < (m * part_hi) >> 8; ++i) {
         uint8_t* src = host + (u * L + (size_t)pl[i].x) * R;
         uint8_t* dst = cache + (u * B + (size_t)pl[i].y) * R;
         if (n && (uint8_t*)c->dma_src[n - 1] + c->dma_size[n - 1] == src &&
@@ -577,8 +583,10 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
     return HISPARSE_OK;
   }
   for (int32_t j0 = 0; j0 < n_layers; j0 += hisparse::kMaxFetchLayers) {
-    const hisparse::FetchArgs f = fetch_args(c, anchor, target + j0, u0, nu,
-                                             std::min(n_layers - j0, hisparse::kMaxFetchLayers));
+    hisparse::FetchArgs f = fetch_args(c, anchor, target + j0, u0, nu,
+                                       std::min(n_layers - j0, hisparse::kMaxFetchLayers));
+    f.part_lo = part_lo;
+    f.part_hi = part_hi;
     if (hisparse::launch_fetch(f, transfer_block(c->desc), fetch_workgroups(c->desc), stream) !=
         hipSuccess)
       return HISPARSE_ERR_HIP;
@@ -722,25 +730,36 @@ hisparse_status_t hisparse_sparse_decode_noalloc(hisparse_cache_t c, int32_t lay
   return HISPARSE_OK;
 }
 
-hisparse_status_t hisparse_sparse_decode_prefetch(hisparse_cache_t c, int32_t layer,
-                                                  const void* d_q, const int32_t* d_slots,
-                                                  float* d_out, const hisparse_attn_desc_t* attn,
-                                                  void* d_workspace, size_t workspace_bytes,
-                                                  int32_t anchor_layer, int32_t first_shared,
-                                                  int32_t num_shared, void* stream) {
-  if (!c || layer < 0 || layer >= c->desc.num_layers) return HISPARSE_ERR_INVALID_ARG;
+namespace {
+// Checks of a replay of `anchor_layer`'s plan into shared layers [first_shared, first_shared +
+// num_shared) over plan-entry range [part_begin, part_end) in 256ths.
+bool valid_replay(hisparse_cache_t c, int32_t anchor_layer, int32_t first_shared,
+                  int32_t num_shared, int32_t part_begin, int32_t part_end) {
   if (!is_anchor(c, anchor_layer) || num_shared < 1 || num_shared > hisparse::kMaxFetchLayers)
-    return HISPARSE_ERR_INVALID_ARG;
+    return false;
   const int64_t end = (int64_t)first_shared + num_shared;
   if (first_shared <= anchor_layer ||
       end > std::min<int64_t>((int64_t)anchor_layer + c->desc.share_group, c->desc.num_layers))
+    return false;
+  return 0 <= part_begin && part_begin <= part_end && part_end <= 256;
+}
+}  // namespace
+
+hisparse_status_t hisparse_sparse_decode_prefetch_part(
+    hisparse_cache_t c, int32_t layer, const void* d_q, const int32_t* d_slots, float* d_out,
+    const hisparse_attn_desc_t* attn, void* d_workspace, size_t workspace_bytes,
+    int32_t anchor_layer, int32_t first_shared, int32_t num_shared, int32_t part_begin,
+    int32_t part_end, void* stream) {
+  if (!c || layer < 0 || layer >= c->desc.num_layers) return HISPARSE_ERR_INVALID_ARG;
+  if (!valid_replay(c, anchor_layer, first_shared, num_shared, part_begin, part_end))
     return HISPARSE_ERR_INVALID_ARG;
-  if (layer >= first_shared && layer < end) return HISPARSE_ERR_INVALID_ARG;  // reads what it writes
+  if (layer >= first_shared && layer < first_shared + num_shared)
+    return HISPARSE_ERR_INVALID_ARG;  // reads what it writes
   if (!d_q || !d_slots || !d_out || !d_workspace) return HISPARSE_ERR_INVALID_ARG;
   if (c->desc.fetch != HISPARSE_FETCH_ZERO_COPY) {
     // no kernel-issued copy to carry: the replay on its own (or nothing), then the attention
-    const hisparse_status_t st =
-        enqueue_fetch(c, anchor_layer, first_shared, as_stream(stream), 0, -1, num_shared);
+    const hisparse_status_t st = enqueue_fetch(c, anchor_layer, first_shared, as_stream(stream),
+                                               0, -1, num_shared, part_begin, part_end);
     if (st != HISPARSE_OK) return st;
     return hisparse_sparse_decode(c, layer, d_q, d_slots, d_out, attn, d_workspace,
                                   workspace_bytes, stream);
@@ -752,13 +771,62 @@ hisparse_status_t hisparse_sparse_decode_prefetch(hisparse_cache_t c, int32_t la
   if (workspace_bytes < p.workspace_bytes) return HISPARSE_ERR_INVALID_ARG;
   if ((int64_t)c->desc.capacity * c->desc.record_bytes > (int64_t)INT32_MAX)
     return HISPARSE_ERR_UNSUPPORTED;
-  const hisparse::FetchArgs f = fetch_args(c, anchor_layer, first_shared, 0, c->units, num_shared);
+  hisparse::FetchArgs f = fetch_args(c, anchor_layer, first_shared, 0, c->units, num_shared);
+  f.part_lo = part_begin;
+  f.part_hi = part_end;
   if (hisparse::launch_attention(p, *attn, c->cache[layer], c->desc.capacity,
                                  c->desc.record_bytes, c->units, c->desc.top_k,
                                  reinterpret_cast<const uint16_t*>(d_q), d_slots, d_out,
-                                 d_workspace, as_stream(stream), 0, &f,
+                                 d_workspace, as_stream(stream), 0,
+                                 part_begin < part_end ? &f : nullptr,
                                  fetch_workgroups(c->desc) * 64 * 2,
                                  transfer_block(c->desc) * 2) != hipSuccess)
+    return HISPARSE_ERR_HIP;
+  return HISPARSE_OK;
+}
+
+hisparse_status_t hisparse_sparse_decode_prefetch(hisparse_cache_t c, int32_t layer,
+                                                  const void* d_q, const int32_t* d_slots,
+                                                  float* d_out, const hisparse_attn_desc_t* attn,
+                                                  void* d_workspace, size_t workspace_bytes,
+                                                  int32_t anchor_layer, int32_t first_shared,
+                                                  int32_t num_shared, void* stream) {
+  return hisparse_sparse_decode_prefetch_part(c, layer, d_q, d_slots, d_out, attn, d_workspace,
+                                              workspace_bytes, anchor_layer, first_shared,
+                                              num_shared, 0, 256, stream);
+}
+
+hisparse_status_t hisparse_attention_merge_prefetch(hisparse_cache_t c,
+                                                    const hisparse_attn_desc_t* attn,
+                                                    float* d_out, const void* d_workspace,
+                                                    size_t workspace_bytes, int32_t anchor_layer,
+                                                    int32_t first_shared, int32_t num_shared,
+                                                    int32_t part_begin, int32_t part_end,
+                                                    void* stream) {
+  if (!c || !d_out || !d_workspace) return HISPARSE_ERR_INVALID_ARG;
+  if (!valid_replay(c, anchor_layer, first_shared, num_shared, part_begin, part_end))
+    return HISPARSE_ERR_INVALID_ARG;
+  hisparse::AttnPlan p{};
+  hisparse_status_t st =
+      hisparse::plan_attention(c->units, c->desc.top_k, c->desc.record_bytes, attn, &p);
+  if (st != HISPARSE_OK) return st;
+  if (workspace_bytes < p.workspace_bytes) return HISPARSE_ERR_INVALID_ARG;
+  if (c->desc.fetch != HISPARSE_FETCH_ZERO_COPY) {
+    st = enqueue_fetch(c, anchor_layer, first_shared, as_stream(stream), 0, -1, num_shared,
+                       part_begin, part_end);
+    if (st != HISPARSE_OK) return st;
+    return hisparse::launch_merge(p, *attn, c->units, d_out, d_workspace, as_stream(stream)) ==
+                   hipSuccess
+               ? HISPARSE_OK
+               : HISPARSE_ERR_HIP;
+  }
+  hisparse::FetchArgs f = fetch_args(c, anchor_layer, first_shared, 0, c->units, num_shared);
+  f.part_lo = part_begin;
+  f.part_hi = part_end;
+  if (hisparse::launch_merge(p, *attn, c->units, d_out, d_workspace, as_stream(stream),
+                             part_begin < part_end ? &f : nullptr,
+                             fetch_workgroups(c->desc) * 64 * 2,
+                             transfer_block(c->desc) * 2) != hipSuccess)
     return HISPARSE_ERR_HIP;
   return HISPARSE_OK;
 }

@@ -51,6 +51,14 @@ constexpr float kRescaleSlack = 8.0f;
 // 16-byte loads of padding tokens and padding slots read zeros from here.
 __device__ __attribute__((aligned(16))) uint8_t g_zero_token[2048];
 
+// A replay carried by a launch (attention or merge): the extra workgroups after the launch's
+// own, per_pair of them for each (unit, target layer) of the plan.
+struct CarriedReplay {
+  FetchArgs pf;
+  FastDiv pf_div;
+  int32_t pf_per_pair, pf_wg, pf_u;  // pf_u: 16-byte loads each replay thread keeps in flight
+};
+
 struct AttnArgs {
   const uint8_t* pool;
   const uint16_t* q;
@@ -63,22 +71,20 @@ struct AttnArgs {
   int32_t Hp;         // latent attention: heads rounded up to 32 (partial-output block layout)
   int32_t idx_units;  // unit u reads index row u % idx_units
   float scale_log2;
-  // A prefetch replay carried by the launch: pf_per_pair extra workgroups per (unit, target
-  // layer) of pf, after the attention workgroups, copy that plan's records (0: none).
-  FetchArgs pf;
-  FastDiv pf_div;
-  int32_t pf_per_pair, pf_wg, pf_u;  // pf_u: 16-byte loads each replay thread keeps in flight
+  // A prefetch replay carried by the launch: extra workgroups after the attention workgroups
+  // copy that plan's records (pf_wg = 0: none).
+  CarriedReplay rp;
 };
 
-// An extra workgroup of an attention launch: its share of the carried replay. It shares no
-// memory with the attention workgroups (other layers' caches), so it needs no synchronisation.
-__device__ __forceinline__ void replay_worker(const AttnArgs& a, int e) {
-  const int pair = e / a.pf_per_pair, x = e - pair * a.pf_per_pair;
-  const int unit = pair % a.pf.units, z = pair / a.pf.units;
-  const uint32_t first = x * blockDim.x + threadIdx.x, stride = a.pf_per_pair * blockDim.x;
-  if (a.pf_u >= 4) fetch_slice<4>(a.pf, a.pf_div, unit, z, first, stride);
-  else if (a.pf_u == 2) fetch_slice<2>(a.pf, a.pf_div, unit, z, first, stride);
-  else fetch_slice<1>(a.pf, a.pf_div, unit, z, first, stride);
+// Extra workgroup e of a launch: its share of the carried replay. It shares no memory with the
+// launch's own workgroups (other layers' caches), so it needs no synchronisation.
+__device__ __forceinline__ void replay_worker(const CarriedReplay& r, int e) {
+  const int pair = e / r.pf_per_pair, x = e - pair * r.pf_per_pair;
+  const int unit = pair % r.pf.units, z = pair / r.pf.units;
+  const uint32_t first = x * blockDim.x + threadIdx.x, stride = r.pf_per_pair * blockDim.x;
+  if (r.pf_u >= 4) fetch_slice<4>(r.pf, r.pf_div, unit, z, first, stride);
+  else if (r.pf_u == 2) fetch_slice<2>(r.pf, r.pf_div, unit, z, first, stride);
+  else fetch_slice<1>(r.pf, r.pf_div, unit, z, first, stride);
 }
 
 // Latent-attention partial outputs are stored in the PV accumulators' own layout, so every
@@ -216,7 +222,7 @@ void attn_partial_kernel(AttnArgs a) {
   // staged records through the same L2.
   const int nwg_pad = (a.n_wg + 7) & ~7;
   if ((int)blockIdx.x >= nwg_pad) {  // wave-uniform: the whole workgroup replays
-    replay_worker(a, (int)blockIdx.x - nwg_pad);
+    replay_worker(a.rp, (int)blockIdx.x - nwg_pad);
     return;
   }
   const int w = (int)(blockIdx.x & 7) * (nwg_pad >> 3) + (int)(blockIdx.x >> 3);
@@ -526,7 +532,7 @@ void attn_mla_kernel(AttnArgs a) {
   // XCD-aware mapping, as in attn_partial_kernel
   const int nwg_pad = (a.n_wg + 7) & ~7;
   if ((int)blockIdx.x >= nwg_pad) {  // wave-uniform: the whole workgroup replays
-    replay_worker(a, (int)blockIdx.x - nwg_pad);
+    replay_worker(a.rp, (int)blockIdx.x - nwg_pad);
     return;
   }
   const int w = (int)(blockIdx.x & 7) * (nwg_pad >> 3) + (int)(blockIdx.x >> 3);
@@ -791,6 +797,8 @@ struct CombineArgs {
   const float2* part_ml;
   float* out;
   int32_t H, n_parts, n_rows;  // n_rows = units * H
+  int32_t n_wg;                // the merge's own workgroups; those after them run rp
+  CarriedReplay rp;
 };
 
 // One wave per (unit, head): the largest partial reference max M, the weights
@@ -801,6 +809,10 @@ template <int DV>
 __global__ __launch_bounds__(256) void attn_combine_kernel(CombineArgs a) {
   constexpr int E = DV / 64;  // output floats per lane
   static_assert(E == 2 || E == 8, "d_v");
+  if ((int)blockIdx.x >= a.n_wg) {  // wave-uniform: the whole workgroup replays
+    replay_worker(a.rp, (int)blockIdx.x - a.n_wg);
+    return;
+  }
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= a.n_rows) return;
@@ -865,6 +877,8 @@ struct CombineMlaArgs {
   const float2* part_ml;  // [units][n_parts][H]
   float* out;             // [units][H][512]
   int32_t H, Hp, n_parts;
+  int32_t n_wg;           // the merge's own workgroups; those after them run rp
+  CarriedReplay rp;
 };
 
 // Merge of latent-attention partials: one workgroup per (unit, 32-head block, 256 / NS of the
@@ -877,6 +891,10 @@ __global__ __launch_bounds__(256) void attn_combine_mla_kernel(CombineMlaArgs a)
   __shared__ __align__(16) float s_w[kMlaMaxParts][32];
   __shared__ float s_inv[32];
   __shared__ __align__(16) f32x4 s_acc[NS][GPW];
+  if ((int)blockIdx.x >= a.n_wg) {  // wave-uniform: the whole workgroup replays
+    replay_worker(a.rp, (int)blockIdx.x - a.n_wg);
+    return;
+  }
   constexpr int chunks = BLK4 / GPW;
   const int nb = a.Hp >> 5;
   const int chunk = blockIdx.x % chunks;
@@ -939,17 +957,34 @@ __global__ __launch_bounds__(256) void attn_combine_mla_kernel(CombineMlaArgs a)
   }
 }
 
+// The extra workgroups of a launch that carries a replay: about `threads` threads spread over
+// the replay's (unit, layer) pairs, in workgroups of the launch's size `bd`, at most `cap`
+// workgroups (at least one per pair). False if the grid would be too large.
+bool carried_replay(const FetchArgs& f, int bd, int64_t cap, int32_t threads, int32_t block_bytes,
+                    CarriedReplay* r) {
+  const int64_t pairs = (int64_t)f.units * f.n_layers;
+  int64_t per_pair = std::max<int64_t>(1, threads / (bd * pairs));
+  per_pair = std::max<int64_t>(1, std::min(per_pair, cap / pairs));
+  if (pairs * per_pair > (1 << 20)) return false;
+  r->pf = f;
+  r->pf_div = make_fastdiv((uint32_t)(f.R / 16));
+  r->pf_per_pair = (int32_t)per_pair;
+  r->pf_wg = (int32_t)(pairs * per_pair);
+  r->pf_u = std::max(1, block_bytes / 16);
+  return true;
+}
+
 template <int DQK, int DV, int VOFF, int HW, int TW, int NST>
 void launch_partial(const AttnArgs& args, hipStream_t stream) {
   const int nwg_pad = (args.n_wg + 7) & ~7;
-  hipLaunchKernelGGL((attn_partial_kernel<DQK, DV, VOFF, HW, TW, NST>), dim3(nwg_pad + args.pf_wg),
+  hipLaunchKernelGGL((attn_partial_kernel<DQK, DV, VOFF, HW, TW, NST>), dim3(nwg_pad + args.rp.pf_wg),
                      dim3(64 * HW * TW), 0, stream, args);
 }
 
 template <int HW, int TG, int NST>
 void launch_mla(const AttnArgs& args, hipStream_t stream) {
   const int nwg_pad = (args.n_wg + 7) & ~7;
-  hipLaunchKernelGGL((attn_mla_kernel<HW, TG, NST>), dim3(nwg_pad + args.pf_wg),
+  hipLaunchKernelGGL((attn_mla_kernel<HW, TG, NST>), dim3(nwg_pad + args.rp.pf_wg),
                      dim3(64 * HW * TG), 0, stream, args);
 }
 
@@ -1054,22 +1089,13 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
                             int32_t prefetch_threads, int32_t prefetch_block_bytes) {
   AttnArgs a{};
   if (prefetch && prefetch->units > 0 && prefetch->n_layers > 0) {
-    // about prefetch_threads threads spread over the replay's (unit, layer) pairs, in
-    // workgroups of the attention kernel's size, on the CUs the attention leaves idle
-    // (a workgroup of these kernels holds a CU's LDS, so replay and attention never share a
-    // CU's memory pipeline)
-    const int bd = 64 * p.hw * (is_mla(attn) ? p.tg : p.tw);
-    const int64_t pairs = (int64_t)prefetch->units * prefetch->n_layers;
+    // on the CUs the attention leaves idle (a workgroup of these kernels holds a CU's LDS, so
+    // replay and attention never share a CU's memory pipeline)
     const int64_t n_attn = (int64_t)units * p.n_wg_splits * p.hb;
     const int64_t idle = std::max<int64_t>(0, kTargetWorkgroups - ((n_attn + 7) & ~7LL));
-    int64_t per_pair = std::max<int64_t>(1, prefetch_threads / (bd * pairs));
-    per_pair = std::max<int64_t>(1, std::min(per_pair, idle / pairs));
-    if (pairs * per_pair > (1 << 20)) return hipErrorInvalidValue;
-    a.pf = *prefetch;
-    a.pf_div = make_fastdiv((uint32_t)(prefetch->R / 16));
-    a.pf_per_pair = (int32_t)per_pair;
-    a.pf_wg = (int32_t)(pairs * per_pair);
-    a.pf_u = std::max(1, prefetch_block_bytes / 16);
+    if (!carried_replay(*prefetch, 64 * p.hw * (is_mla(attn) ? p.tg : p.tw), idle,
+                        prefetch_threads, prefetch_block_bytes, &a.rp))
+      return hipErrorInvalidValue;
   }
   a.idx_units = idx_units > 0 ? idx_units : units;
   a.pool = pool;
@@ -1119,25 +1145,38 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
 }
 
 hipError_t launch_merge(const AttnPlan& p, const hisparse_attn_desc_t& attn, int32_t units,
-                        float* out, const void* workspace, hipStream_t stream) {
+                        float* out, const void* workspace, hipStream_t stream,
+                        const FetchArgs* prefetch, int32_t prefetch_threads,
+                        int32_t prefetch_block_bytes) {
   // the same workspace layout as launch_attention: partial outputs, then (max, sum) pairs
   const int Hp = is_mla(attn) ? (attn.q_heads + 31) / 32 * 32 : attn.q_heads;
   const size_t o_bytes = (size_t)units * p.n_parts * Hp * attn.d_v * sizeof(float);
   const float* part_o = reinterpret_cast<const float*>(workspace);
   const float2* part_ml = reinterpret_cast<const float2*>(
       reinterpret_cast<const uint8_t*>(workspace) + ((o_bytes + 255) & ~(size_t)255));
+  // a carried replay: merge workgroups are small (no CU's whole LDS), so the replay's
+  // workgroups run beside them wherever there is room
+  CarriedReplay rp{};
+  if (prefetch && prefetch->units > 0 && prefetch->n_layers > 0 &&
+      !carried_replay(*prefetch, 256, 1 << 20, prefetch_threads, prefetch_block_bytes, &rp))
+    return hipErrorInvalidValue;
   if (is_mla(attn)) {
     const int nb = Hp / 32;
-    CombineMlaArgs c{part_o, part_ml, out, attn.q_heads, Hp, p.n_parts};
-    if ((int64_t)units * nb * 16 >= 2 * kTargetWorkgroups)
-      hipLaunchKernelGGL(attn_combine_mla_kernel<1>, dim3(units * nb * 16), dim3(256), 0, stream, c);
-    else
-      hipLaunchKernelGGL(attn_combine_mla_kernel<4>, dim3(units * nb * 64), dim3(256), 0, stream, c);
+    CombineMlaArgs c{part_o, part_ml, out, attn.q_heads, Hp, p.n_parts, 0, rp};
+    if ((int64_t)units * nb * 16 >= 2 * kTargetWorkgroups) {
+      c.n_wg = units * nb * 16;
+      hipLaunchKernelGGL(attn_combine_mla_kernel<1>, dim3(c.n_wg + rp.pf_wg), dim3(256), 0,
+                         stream, c);
+    } else {
+      c.n_wg = units * nb * 64;
+      hipLaunchKernelGGL(attn_combine_mla_kernel<4>, dim3(c.n_wg + rp.pf_wg), dim3(256), 0,
+                         stream, c);
+    }
     return hipGetLastError();
   }
-  CombineArgs c{part_o, part_ml, out, attn.q_heads, p.n_parts, units * attn.q_heads};
-  const int n_cwg = (units * attn.q_heads + 3) / 4;
-  hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(n_cwg), dim3(256), 0, stream, c);
+  CombineArgs c{part_o, part_ml, out, attn.q_heads, p.n_parts, units * attn.q_heads, 0, rp};
+  c.n_wg = (units * attn.q_heads + 3) / 4;
+  hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(c.n_wg + rp.pf_wg), dim3(256), 0, stream, c);
   return hipGetLastError();
 }
 

@@ -25,16 +25,18 @@ __device__ inline uint32_t fastdiv(uint32_t n, FastDiv f) {
 }
 
 // One thread's share of copying unit `unit`'s planned records into target layer z: the 16-byte
-// chunks first, first + stride, ... of the plan (chunk c = 16-byte piece c % (R / 16) of plan
-// entry c / (R / 16)), U loads in flight before their stores. Each planned record is read from
-// the layer's host pool at its position and written to the layer's cache at its slot.
+// chunks first, first + stride, ... of the plan's entry range (chunk c = 16-byte piece
+// c % (R / 16) of plan entry c / (R / 16)), U loads in flight before their stores. Each planned
+// record is read from the layer's host pool at its position and written to the layer's cache at
+// its slot.
 template <int U>
 __device__ __forceinline__ void fetch_slice(const FetchArgs& a, FastDiv div_cpr, int unit, int z,
                                             uint32_t first, uint32_t stride) {
   typedef unsigned int v4u __attribute__((ext_vector_type(4)));
   const int m = a.plan_count[unit];
   const uint32_t cpr = (uint32_t)a.R >> 4;  // 16-byte chunks per record
-  const uint32_t total = (uint32_t)m * cpr;
+  const uint32_t total = (uint32_t)((m * a.part_hi) >> 8) * cpr;
+  first += (uint32_t)((m * a.part_lo) >> 8) * cpr;
   const int2* plan = a.plan + (int64_t)unit * a.k;
   const uint8_t* host = a.host[z] + (int64_t)unit * a.L * a.R;
   uint8_t* cache = a.cache + (int64_t)z * a.cache_stride + (int64_t)unit * a.B * a.R;

@@ -48,6 +48,9 @@ struct FetchArgs {
   int64_t cache_stride;     // bytes from one target layer's cache to the next
   int64_t L;
   int32_t B, k, R, units, n_layers;
+  // each unit's plan entries [m * part_lo / 256, m * part_hi / 256) of its m (0, 256: all), so
+  // that launches with adjacent ranges split one copy exactly
+  int32_t part_lo, part_hi;
 };
 
 // Device tables the write-through kernel indexes: per anchor its resolve state, per layer its
@@ -113,7 +116,9 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
 // The merge of the per-split partials in `workspace` into out (skipped by launch_attention
 // when attn.flags has HISPARSE_ATTN_DEFER_MERGE).
 hipError_t launch_merge(const AttnPlan& p, const hisparse_attn_desc_t& attn, int32_t units,
-                        float* out, const void* workspace, hipStream_t stream);
+                        float* out, const void* workspace, hipStream_t stream,
+                        const FetchArgs* prefetch = nullptr, int32_t prefetch_threads = 0,
+                        int32_t prefetch_block_bytes = 16);
 hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
                             const uint8_t* pool, int64_t records_per_unit, int32_t record_bytes,
                             int32_t units, int32_t top_k, const uint16_t* q, const int32_t* idx,

@@ -46,7 +46,8 @@ EXPORTED = (
     "hisparse_request_release", "hisparse_reset_units", "hisparse_stage", "hisparse_speculate",
     "hisparse_decode_workspace_bytes", "hisparse_sparse_decode", "hisparse_sparse_decode_layers",
     "hisparse_attention_merge",
-    "hisparse_sparse_decode_prefetch",
+    "hisparse_sparse_decode_prefetch", "hisparse_sparse_decode_prefetch_part",
+    "hisparse_attention_merge_prefetch",
     "hisparse_sparse_decode_pool", "hisparse_sparse_decode_noalloc",
     "hisparse_read_state", "hisparse_read_plan", "hisparse_check_errors",
 )
@@ -126,6 +127,13 @@ def lib() -> ctypes.CDLL:
                                                        ctypes.c_size_t, _I32, _I32, _I32, _V]),
             "hisparse_sparse_decode_noalloc": (_I32, [_V, _I32, _V, _V, _V,
                                                       ctypes.POINTER(AttnDesc), _V]),
+            "hisparse_sparse_decode_prefetch_part": (_I32, [_V, _I32, _V, _V, _V,
+                                                            ctypes.POINTER(AttnDesc), _V,
+                                                            ctypes.c_size_t, _I32, _I32, _I32,
+                                                            _I32, _I32, _V]),
+            "hisparse_attention_merge_prefetch": (_I32, [_V, ctypes.POINTER(AttnDesc), _V, _V,
+                                                         ctypes.c_size_t, _I32, _I32, _I32,
+                                                         _I32, _I32, _V]),
             "hisparse_sparse_decode_pool": (_I32, [_V, ctypes.c_int64, _I32, _I32, _I32, _V, _V,
                                                    _V, ctypes.POINTER(AttnDesc), _V,
                                                    ctypes.c_size_t, _V]),
@@ -300,6 +308,27 @@ def hisparse_sparse_decode_noalloc(cache: int, layer: int, d_q, d_slots, d_out, 
     _check("hisparse_sparse_decode_noalloc",
            lib().hisparse_sparse_decode_noalloc(cache, layer, _p(d_q), _p(d_slots), _p(d_out),
                                                 ctypes.byref(attn), _s(stream)))
+
+
+def hisparse_sparse_decode_prefetch_part(cache: int, layer: int, d_q, d_slots, d_out,
+                                         attn: AttnDesc, d_workspace, workspace_bytes: int,
+                                         anchor_layer: int, first_shared: int, num_shared: int,
+                                         part_begin: int, part_end: int, stream=None) -> None:
+    _check("hisparse_sparse_decode_prefetch_part",
+           lib().hisparse_sparse_decode_prefetch_part(
+               cache, layer, _p(d_q), _p(d_slots), _p(d_out), ctypes.byref(attn),
+               _p(d_workspace), workspace_bytes, anchor_layer, first_shared, num_shared,
+               part_begin, part_end, _s(stream)))
+
+
+def hisparse_attention_merge_prefetch(cache: int, attn: AttnDesc, d_out, d_workspace,
+                                      workspace_bytes: int, anchor_layer: int, first_shared: int,
+                                      num_shared: int, part_begin: int, part_end: int,
+                                      stream=None) -> None:
+    _check("hisparse_attention_merge_prefetch",
+           lib().hisparse_attention_merge_prefetch(
+               cache, ctypes.byref(attn), _p(d_out), _p(d_workspace), workspace_bytes,
+               anchor_layer, first_shared, num_shared, part_begin, part_end, _s(stream)))
 
 
 def hisparse_attention_merge(units: int, top_k: int, record_bytes: int, attn: AttnDesc, d_out,

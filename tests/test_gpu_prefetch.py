@@ -337,3 +337,70 @@ def test_deferred_merge_equals_fused(cfg):
     finally:
         torch.cuda.synchronize()
         run.close()
+
+
+@pytest.mark.parametrize("cfg,fetch,share", [(2, hs.HISPARSE_FETCH_ZERO_COPY, 64),
+                                             (2, hs.HISPARSE_FETCH_ZERO_COPY, 1),
+                                             (2, hs.HISPARSE_FETCH_ZERO_COPY, 256),
+                                             (3, hs.HISPARSE_FETCH_ZERO_COPY, 200),
+                                             (2, hs.HISPARSE_FETCH_SDMA, 64)])
+def test_merge_carried_replay_equals_separate(cfg, fetch, share):
+    """The overlap schedule with the merges starting the replay into the layer after next
+    (hisparse_attention_merge_prefetch over the first share/256 of each unit's plan) and the
+    following attention carrying the rest (hisparse_sparse_decode_prefetch_part): attention
+    outputs bit-identical and caches byte-identical to the replay and the attention issued apart,
+    every planned record copied once; bad plan ranges are argument errors."""
+    G = 4
+    w = W.workload(cfg, num_layers=G, share_group=G, num_requests=2)
+    steps = 3
+    log(f"test_merge_carried_replay_equals_separate {w.name} fetch={fetch} share={share}")
+    split, apart = Run(w, steps, fetch=fetch), Run(w, steps, fetch=fetch)
+    dev = split.dev
+    ad = attn_desc(w)
+    adf = attn_desc(w)
+    adf.flags = hs.HISPARSE_ATTN_DEFER_MERGE
+    nb = hs.hisparse_decode_workspace_bytes(w.units, w.k, w.record_bytes, ad)
+    ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+    out_s = torch.empty((G, w.units, w.q_heads, w.d_v), dtype=torch.float32, device=dev)
+    out_a = torch.empty_like(out_s)
+    try:
+        for t in range(steps):
+            q = [torch.from_numpy(W.queries(w, t, l).view(np.int16)).to(dev) for l in range(G)]
+            for r in (split, apart):
+                hs.hisparse_resolve(r.cache.handle, 0, r.sel_ptr(t, 0), r.slots[0], r.counts[0],
+                                    r.stream)
+            h, st = split.cache.handle, split.stream
+            for l in range(G - 1):
+                lo = share if l >= 1 else 0
+                hs.hisparse_sparse_decode_prefetch_part(h, l, q[l], split.slots[0], out_s[l], adf,
+                                                        ws, nb, 0, l + 1, 1, lo, 256, st)
+                if l + 2 < G:
+                    hs.hisparse_attention_merge_prefetch(h, adf, out_s[l], ws, nb, 0, l + 2, 1, 0,
+                                                         share, st)
+                else:
+                    hs.hisparse_attention_merge(w.units, w.k, w.record_bytes, adf, out_s[l], ws,
+                                                nb, st)
+            hs.hisparse_sparse_decode(h, G - 1, q[G - 1], split.slots[0], out_s[G - 1], ad, ws,
+                                      nb, st)
+            hs.hisparse_prefetch_layers(apart.cache.handle, 0, 1, G - 1, apart.stream)
+            for l in range(G):
+                hs.hisparse_sparse_decode(apart.cache.handle, l, q[l], apart.slots[0], out_a[l],
+                                          ad, ws, nb, apart.stream)
+            torch.cuda.synchronize()
+            assert torch.equal(out_s, out_a), f"step {t}"
+            for l in range(G):
+                assert (layer_cache_host(split, l) == layer_cache_host(apart, l)).all(), \
+                    f"step {t} layer {l}"
+        h, st = split.cache.handle, split.stream
+        for lo, hi in ((-1, 10), (10, 9), (0, 257)):
+            with pytest.raises(hs.HisparseError):
+                hs.hisparse_attention_merge_prefetch(h, adf, out_s[0], ws, nb, 0, 2, 1, lo, hi, st)
+            with pytest.raises(hs.HisparseError):
+                hs.hisparse_sparse_decode_prefetch_part(h, 0, q[0], split.slots[0], out_s[0], adf,
+                                                        ws, nb, 0, 1, 1, lo, hi, st)
+        with pytest.raises(hs.HisparseError):  # a replay target outside the anchor's group
+            hs.hisparse_attention_merge_prefetch(h, adf, out_s[0], ws, nb, 0, 4, 1, 0, 64, st)
+    finally:
+        torch.cuda.synchronize()
+        split.close()
+        apart.close()
