@@ -37,6 +37,13 @@ constexpr int kMaxChunk = 16;  // order entries per thread: B <= 16 * threads
 constexpr int kMaxPer = 4;     // selections per thread: k <= 4 * threads
 constexpr int kBucketBits = 11;
 constexpr int kBuckets = 1 << kBucketBits;  // miss rank buckets (high position bits)
+// The most misses one rank bucket may hold before the misses are sorted instead of counted
+// (counting mates costs about bucket size x misses per thread steps per thread).
+#ifndef HISPARSE_SCAN_LIMIT
+constexpr int kScanLimit = 256;
+#else
+constexpr int kScanLimit = HISPARSE_SCAN_LIMIT;
+#endif
 // One wave per fetch workgroup: each CU that hosts fetch work gives it one wave and a few
 // outstanding host reads, not a whole workgroup's worth.
 constexpr int kFetchThreads = 64;
@@ -80,6 +87,7 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   extern __shared__ __align__(16) unsigned char s_dyn[];
   __shared__ int s_tmp[NT / kWave + 1];
   __shared__ int s_nmiss, s_bad;
+  __shared__ int s_pmin, s_pmax, s_maxb;  // miss position range, largest bucket
 
   const int unit = blockIdx.x;
   const int tid = threadIdx.x;
@@ -110,6 +118,9 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   if (tid == 0) {
     s_nmiss = 0;
     s_bad = 0;
+    s_pmin = INT32_MAX;
+    s_pmax = -1;
+    s_maxb = 0;
   }
   __syncthreads();
 
@@ -148,32 +159,61 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   __syncthreads();
   const int m = s_nmiss;
 
-  // Phase 2: the misses in ascending position order. Bucket them by their high position bits
-  // (a counting pass), then each miss's rank is its bucket's start plus the number of bucket
-  // mates at lower positions; a mate at the same position is a repeated selection.
-  const int lg = L > 1 ? 64 - __clzll((unsigned long long)(L - 1)) : 1;
-  const int shift = lg > kBucketBits ? lg - kBucketBits : 0;
-  const uint32_t low_mask = (1u << shift) - 1u;
+  // Phase 2: the misses in ascending position order. Bucket them by the high bits of their
+  // offset within the misses' own position range (a counting pass), then each miss's rank is
+  // its bucket's start plus the number of bucket mates at lower positions; a mate at the same
+  // position is a repeated selection. Positions are distinct, so a bucket holds at most its
+  // width in misses: a contiguous run of misses spreads over the buckets. Should some bucket
+  // still hold more than kScanLimit misses (clusters far apart), counting mates would cost more
+  // than sorting, and the keys are sorted instead (bitonic network in LDS).
   uint64_t key[kMaxPer];
   int bkt[kMaxPer], loc[kMaxPer];
+  {
+    int pmin = INT32_MAX, pmax = -1;
+#pragma unroll
+    for (int u = 0; u < kMaxPer; ++u) {
+      const int j = tid + u * NT;
+      key[u] = j < m ? s_keys[j] : 0ull;
+      if (j < m) {
+        pmin = min(pmin, (int)(key[u] >> 32));
+        pmax = max(pmax, (int)(key[u] >> 32));
+      }
+    }
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      pmin = min(pmin, __shfl_xor(pmin, o, kWave));
+      pmax = max(pmax, __shfl_xor(pmax, o, kWave));
+    }
+    if ((tid & (kWave - 1)) == 0 && pmax >= 0) {  // one LDS atomic pair per wave
+      atomicMin(&s_pmin, pmin);
+      atomicMax(&s_pmax, pmax);
+    }
+  }
+  __syncthreads();
+  const int pmin = s_pmin;
+  const uint32_t span = s_pmax > pmin ? (uint32_t)(s_pmax - pmin) : 0u;  // < 2^31
+  const int lg = span ? 32 - __clz(span) : 0;
+  const int shift = lg > kBucketBits ? lg - kBucketBits : 0;
+  const uint32_t low_mask = (1u << shift) - 1u;
 #pragma unroll
   for (int u = 0; u < kMaxPer; ++u) {
     const int j = tid + u * NT;
-    key[u] = j < m ? s_keys[j] : 0ull;
-    bkt[u] = (int)((key[u] >> 32) >> shift);
+    bkt[u] = j < m ? (int)((uint32_t)((int)(key[u] >> 32) - pmin) >> shift) : 0;
     loc[u] = j < m ? atomicAdd(&s_cnt[bkt[u]], 1) : 0;
   }
   __syncthreads();
   {
     // exclusive scan of the bucket counts, kBuckets / NT consecutive buckets per thread
     constexpr int per = (kBuckets + NT - 1) / NT;
-    int c[per], sum = 0;
+    int c[per], sum = 0, big = 0;
 #pragma unroll
     for (int q = 0; q < per; ++q) {
       const int b = tid * per + q;
       c[q] = b < kBuckets ? s_cnt[b] : 0;
       sum += c[q];
+      big = max(big, c[q]);
     }
+    if (big > kScanLimit) atomicMax(&s_maxb, big);
     int total;
     int run = block_excl_scan<NT>(sum, s_tmp, &total);  // all reads of s_cnt precede it
 #pragma unroll
@@ -184,36 +224,84 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
     }
   }
   __syncthreads();
-  // bucketed order in the victim array (free until phase 3): low position bits and input index
-  uint32_t* s_bkt = reinterpret_cast<uint32_t*>(s_victim);
-#pragma unroll
-  for (int u = 0; u < kMaxPer; ++u)
-    if (tid + u * NT < m)
-      s_bkt[s_cnt[bkt[u]] + loc[u]] = (((uint32_t)(key[u] >> 32) & low_mask) << 12) | (uint32_t)key[u];
-  __syncthreads();
-  int rank[kMaxPer];
-#pragma unroll
-  for (int u = 0; u < kMaxPer; ++u) {
-    rank[u] = 0;
-    if (tid + u * NT < m) {
-      const int b0 = s_cnt[bkt[u]];
-      const int b1 = bkt[u] + 1 < kBuckets ? s_cnt[bkt[u] + 1] : m;
-      const uint32_t mine = ((uint32_t)(key[u] >> 32) & low_mask);
-      int lower = 0;
-      for (int q = b0; q < b1; ++q) {
-        const uint32_t e = s_bkt[q];
-        const uint32_t lowp = e >> 12;
-        lower += lowp < mine ? 1 : 0;
-        if (lowp == mine && (e & 0xFFFu) != ((uint32_t)key[u] & 0xFFFu)) s_bad = 1;
+  if (s_maxb > kScanLimit) {  // workgroup-uniform
+    // bitonic sort of the m keys in place, ascending (position, input index); the network's
+    // comparators all put the smaller key at the lower index, so indices >= m act as +inf
+    // padding and are never touched
+    int n2 = 1;
+    while (n2 < m) n2 <<= 1;
+    for (int size = 2; size <= n2; size <<= 1) {
+      for (int stride = size >> 1; stride >= 1; stride >>= 1) {
+        for (int c = tid; c < (n2 >> 1); c += NT) {
+          int i, j;
+          if (stride == (size >> 1)) {  // first step of a merge: mirrored pairs
+            const int blk = c / stride, off = c - blk * stride;
+            i = blk * size + off;
+            j = blk * size + size - 1 - off;
+          } else {
+            i = (c / stride) * 2 * stride + c % stride;
+            j = i + stride;
+          }
+          if (j < m) {
+            const uint64_t x = s_keys[i], y = s_keys[j];
+            if (y < x) {
+              s_keys[i] = y;
+              s_keys[j] = x;
+            }
+          }
+        }
+        __syncthreads();
       }
-      rank[u] = b0 + lower;
     }
-  }
-  __syncthreads();  // all reads of the unsorted keys are done
+    for (int q = tid; q + 1 < m; q += NT)
+      if ((s_keys[q] >> 32) == (s_keys[q + 1] >> 32)) s_bad = 1;  // a repeated miss
+    __syncthreads();
+  } else {
+    // bucketed order in the victim array (free until phase 3): low offset bits and input index
+    uint32_t* s_bkt = reinterpret_cast<uint32_t*>(s_victim);
 #pragma unroll
-  for (int u = 0; u < kMaxPer; ++u)
-    if (tid + u * NT < m) s_keys[rank[u]] = key[u];
-  __syncthreads();
+    for (int u = 0; u < kMaxPer; ++u)
+      if (tid + u * NT < m)
+        s_bkt[s_cnt[bkt[u]] + loc[u]] =
+            ((((uint32_t)((int)(key[u] >> 32) - pmin)) & low_mask) << 12) | (uint32_t)key[u];
+    __syncthreads();
+    int rank[kMaxPer];
+#pragma unroll
+    for (int u = 0; u < kMaxPer; ++u) {
+      rank[u] = 0;
+      if (tid + u * NT < m) {
+        const int b0 = s_cnt[bkt[u]];
+        const int b1 = bkt[u] + 1 < kBuckets ? s_cnt[bkt[u] + 1] : m;
+        const uint32_t mine = ((uint32_t)((int)(key[u] >> 32) - pmin)) & low_mask;
+        const uint32_t me = (uint32_t)key[u] & 0xFFFu;
+        int lower = 0;
+        bool rep = false;
+        int q = b0;
+        for (; q + 4 <= b1; q += 4) {  // four mates' reads in flight
+          uint32_t e[4];
+#pragma unroll
+          for (int x = 0; x < 4; ++x) e[x] = s_bkt[q + x];
+#pragma unroll
+          for (int x = 0; x < 4; ++x) {
+            lower += (e[x] >> 12) < mine ? 1 : 0;
+            rep |= (e[x] >> 12) == mine && (e[x] & 0xFFFu) != me;
+          }
+        }
+        for (; q < b1; ++q) {
+          const uint32_t e = s_bkt[q];
+          lower += (e >> 12) < mine ? 1 : 0;
+          rep |= (e >> 12) == mine && (e & 0xFFFu) != me;
+        }
+        if (rep) s_bad = 1;
+        rank[u] = b0 + lower;
+      }
+    }
+    __syncthreads();  // all reads of the unsorted keys are done
+#pragma unroll
+    for (int u = 0; u < kMaxPer; ++u)
+      if (tid + u * NT < m) s_keys[rank[u]] = key[u];
+    __syncthreads();
+  }
 
   if (s_bad) {  // invalid selection: publish -1 and leave the unit's state untouched
     if (slots_out)

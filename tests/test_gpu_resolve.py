@@ -188,3 +188,86 @@ def test_fetch_units_ranges_equal_whole_fetch():
     finally:
         whole.close()
         parts.close()
+
+
+def clustered_streams(L, k, rng):
+    """Selections whose misses cluster in position: a cold contiguous window, a contiguous run
+    mixed with scattered draws and hits, two runs at opposite ends of the range (some rank
+    bucket over the whole range then holds far more misses than the counting pass takes: the
+    kernel sorts them), uniform draws, and a shorter run among draws. Unit 1 repeats one entry
+    of its far-apart runs at step 2 (a bad selection found by the sort)."""
+    steps = []
+    w0 = np.arange(L - k, L)
+    steps.append([w0, w0.copy()])
+    run = np.arange(L // 2, L // 2 + k // 2)
+    steps.append([np.concatenate([run, rng.choice(w0, k - k // 2, replace=False)])] * 2)
+    far = np.concatenate([np.arange(0, k // 2), np.arange(L - 4096 - k // 2, L - 4096)])
+    bad = far.copy()
+    bad[7] = bad[k // 2 + 9]  # a repeated position, one in each run's place
+    steps.append([far, bad])
+    steps.append([rng.choice(L, k, replace=False)] * 2)
+    short = np.arange(L // 3, L // 3 + 600)
+    rest = rng.choice(np.setdiff1d(rng.choice(L, 4 * k, replace=False), short), k - 600,
+                      replace=False)
+    steps.append([np.concatenate([short, rest])] * 2)
+    out = np.empty((len(steps), 2, k), dtype=np.int32)
+    for t, per_unit in enumerate(steps):
+        for u in range(2):
+            out[t, u] = rng.permutation(np.asarray(per_unit[u], dtype=np.int64))
+    return out
+
+
+def test_resolve_clustered_misses_at_large_context():
+    """2^24 records per unit, k = 2048, B = 4096: misses in contiguous runs (the rank buckets
+    follow the misses' own position range; far-apart runs are sorted instead of counted) give
+    the oracle's slots, counts, plans and tables bit for bit, and a repeated entry is still
+    caught."""
+    L, k, B = 1 << 24, 2048, 4096
+    rng = np.random.default_rng(24)
+    sel = clustered_streams(L, k, rng)
+    log(f"test_resolve_clustered_misses_at_large_context L={L} k={k} B={B}")
+    cache = HiSparseCache(num_requests=2, num_layers=1, units_per_request=1, capacity=B,
+                          num_records=L, top_k=k, record_bytes=16)
+    try:
+        dev = torch.device("cuda:0")
+        stream = torch.cuda.current_stream()
+        host = cache.host_view(0)
+        host[:] = rng.integers(0, 256, host.shape, dtype=np.uint8)
+        orc = oracle.OracleCache(2, L, B, k)
+        slots = torch.empty((2, k), dtype=torch.int32, device=dev)
+        counts = torch.empty((2, 2), dtype=torch.int32, device=dev)
+        for t in range(sel.shape[0]):
+            sel_d = torch.from_numpy(sel[t]).to(dev)
+            hs.hisparse_resolve(cache.handle, 0, sel_d, slots, counts, stream)
+            e_slots, e_counts, pp, ps, n_bad = orc.resolve(sel[t])
+            assert n_bad == (1 if t == 2 else 0)
+            assert (slots.cpu().numpy() == e_slots).all(), f"slots step {t}"
+            assert (counts.cpu().numpy() == e_counts).all(), f"counts step {t}"
+            plan, count = cache.read_plan(0)
+            for u in range(2):
+                m = int(e_counts[u, 1])
+                assert count[u] == m
+                assert (plan[u, :m, 0] == pp[u, :m]).all() and (plan[u, :m, 1] == ps[u, :m]).all()
+            st = cache.read_state(0, page_table=False)
+            assert (st["slot_pos"] == orc.slot_pos).all() and (st["slot_ts"] == orc.slot_ts).all()
+            assert (st["order"] == expected_order(orc.slot_ts)).all()
+            status, info = cache.check_errors()
+            if t == 2:
+                assert status == hs.HISPARSE_ERR_BAD_SELECTION and list(info[:3]) == [0, 1, 1]
+            else:
+                assert status == hs.HISPARSE_OK
+        st = cache.read_state(0)
+        assert (st["page_table"] == orc.pt).all()
+        img = d2h_cache(cache, 0).reshape(2, B, 16)
+        for u in range(2):
+            res = np.nonzero(orc.slot_pos[u] >= 0)[0]
+            assert (img[u, res] == host[u, orc.slot_pos[u, res]]).all()
+    finally:
+        torch.cuda.synchronize()
+        cache.close()
+
+
+def d2h_cache(cache, layer):
+    from hs_harness import d2h
+    ptr, n = cache.layer_cache(layer)
+    return d2h(ptr, n)
