@@ -52,7 +52,8 @@ def parse():
     ap.add_argument("--requests", type=int, default=0, metavar="N",
                     help="run the workload with N requests instead of its own count (a batch "
                          "scan; every other shape is the workload's)")
-    ap.add_argument("--fetch", choices=["zero_copy", "none", "sdma"], default="zero_copy")
+    ap.add_argument("--fetch", choices=["zero_copy", "none", "sdma", "staged"],
+                    default="zero_copy")
     ap.add_argument("--host-memory", choices=["coherent", "noncoherent", "uncached"],
                     default="coherent")
     ap.add_argument("--transfer-block", type=int, default=0)
@@ -573,7 +574,9 @@ def main() -> int:
     torch.cuda.set_stream(root_t)
     root_s = root_t.cuda_stream
     fetch = {"none": hs.HISPARSE_FETCH_NONE, "sdma": hs.HISPARSE_FETCH_SDMA,
-             "zero_copy": hs.HISPARSE_FETCH_ZERO_COPY}[args.fetch]
+             "zero_copy": hs.HISPARSE_FETCH_ZERO_COPY,
+             "staged": hs.HISPARSE_FETCH_STAGED}[args.fetch]
+    host_issued = fetch in (hs.HISPARSE_FETCH_SDMA, hs.HISPARSE_FETCH_STAGED)
     hmem = {"coherent": hs.HISPARSE_HOST_COHERENT, "noncoherent": hs.HISPARSE_HOST_NONCOHERENT,
             "uncached": hs.HISPARSE_HOST_UNCACHED}[args.host_memory]
     n_mb = args.micro_batches or (2 if w.num_requests >= 2 else 1)
@@ -581,8 +584,8 @@ def main() -> int:
         print(json.dumps({"error": f"{w.num_requests} requests do not split into {n_mb} "
                           f"micro-batches"}))
         return 2
-    if n_mb > 1 and fetch == hs.HISPARSE_FETCH_SDMA:
-        n_mb = 1  # the SDMA path synchronises the host on every fetch: nothing to overlap
+    if n_mb > 1 and host_issued:
+        n_mb = 1  # these paths synchronise the host on every fetch: nothing to overlap
 
     U_all, k, G = w.units, w.k, w.share_group
     t0 = time.time()
@@ -1129,7 +1132,7 @@ def main() -> int:
 
     # the same steps replayed from a captured HIP graph (cold reset, same warmup)
     graph = None
-    if not args.no_graph and fetch != hs.HISPARSE_FETCH_SDMA:
+    if not args.no_graph and not host_issued:
         # One graph covers S consecutive steps (S even, so every replay sees the same query
         # parity per position): the steps' selections are staged from a device-side step
         # counter at the start, the queries are read in place, and the micro-batches fork once

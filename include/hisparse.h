@@ -24,8 +24,9 @@
  *     writes them on the given stream and keeps no reference after the call returns.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *   - Calls marked [async] enqueue GPU work on `stream`, never synchronise the host, allocate
- *     nothing and can be captured in a HIP graph (with HISPARSE_FETCH_SDMA, the calls that
- *     fetch synchronise `stream` once to read the miss plan back, and cannot be captured).
+ *     nothing and can be captured in a HIP graph (with HISPARSE_FETCH_SDMA or
+ *     HISPARSE_FETCH_STAGED, the calls that fetch synchronise `stream` once to read the miss
+ *     plan back, and cannot be captured).
  *     Calls marked [sync] block the host.
  *   - Every call returns HISPARSE_OK or a negative hisparse_status_t; an argument error is
  *     reported before any work is enqueued, and leaves all state untouched.
@@ -70,7 +71,13 @@ typedef enum {
   HISPARSE_FETCH_SDMA = 1,
   /* Timing mode (the no-IO oracle of Section 4.6): tables and slot outputs are exact, but no
    * record is copied, so the cache holds stale data and attention outputs are not valid. */
-  HISPARSE_FETCH_NONE = 2
+  HISPARSE_FETCH_NONE = 2,
+  /* Staging DMA (the staging alternative to GPU-assisted IO, Section 3.4 Phase 4): the host reads
+   * the miss plan back (a stream synchronisation), host threads gather the missed records from
+   * the pool into a pinned staging buffer, one copy-engine transfer moves them to the device
+   * and a kernel scatters them into their slots. Not capturable, like HISPARSE_FETCH_SDMA; the
+   * cache also holds top_k * R bytes of pinned and of device staging memory per unit. */
+  HISPARSE_FETCH_STAGED = 3
 } hisparse_fetch_t;
 
 /* Kind of pinned host memory backing the pool. */

@@ -43,6 +43,9 @@ int fetch_workgroups(const hisparse_cache_desc_t& d) {
   return d.fetch_workgroups == 0 ? 256 : d.fetch_workgroups;
 }
 
+// Staged fetch buffer layout: the per-unit prefix of entries, then the packed records.
+size_t stage_rec_offset(size_t units) { return ((units + 1) * sizeof(int32_t) + 255) & ~(size_t)255; }
+
 void free_all(hisparse_cache* c) {
   if (!c) return;
   int prev = 0;
@@ -67,6 +70,9 @@ void free_all(hisparse_cache* c) {
   if (c->d_layers) (void)hipFree(c->d_layers);
   if (c->h_plan_count) (void)hipHostFree(c->h_plan_count);
   if (c->h_plan) (void)hipHostFree(c->h_plan);
+  if (c->stage_host) (void)hipHostFree(c->stage_host);
+  if (c->stage_dev) (void)hipFree(c->stage_dev);
+  delete c->gather;
   (void)hipSetDevice(prev);
   delete c;
 }
@@ -155,6 +161,7 @@ hisparse_status_t hisparse_validate_desc(const hisparse_cache_desc_t* d) {
     return HISPARSE_ERR_INVALID_ARG;
   if (d->share_group < 1) return HISPARSE_ERR_INVALID_ARG;
   if (d->fetch != HISPARSE_FETCH_ZERO_COPY && d->fetch != HISPARSE_FETCH_SDMA &&
+      d->fetch != HISPARSE_FETCH_STAGED &&
       d->fetch != HISPARSE_FETCH_NONE)
     return HISPARSE_ERR_UNSUPPORTED;
   if (d->host_memory < HISPARSE_HOST_COHERENT || d->host_memory > HISPARSE_HOST_UNCACHED)
@@ -289,7 +296,24 @@ hisparse_status_t hisparse_cache_create(const hisparse_cache_desc_t* desc, int32
                   hipMemcpyHostToDevice) != hipSuccess)
       st = HISPARSE_ERR_HIP;
   }
-  if (st == HISPARSE_OK && desc->fetch == HISPARSE_FETCH_SDMA) {
+  if (st == HISPARSE_OK && desc->fetch == HISPARSE_FETCH_STAGED) {
+    // [units + 1] int32 prefix (256-byte aligned), then at most every unit's k records
+    c->stage_bytes = stage_rec_offset(U) + U * K * R;
+    if (hipHostMalloc(reinterpret_cast<void**>(&c->stage_host), c->stage_bytes, 0) !=
+        hipSuccess) {
+      c->stage_host = nullptr;
+      (void)hipGetLastError();
+      st = HISPARSE_ERR_OOM;
+    } else {
+      st = dmalloc(&c->stage_dev, c->stage_bytes);
+    }
+    if (st == HISPARSE_OK) {
+      c->gather = new (std::nothrow) hisparse::GatherPool(hisparse::GatherPool::host_threads(16));
+      if (!c->gather) st = HISPARSE_ERR_OOM;
+    }
+  }
+  if (st == HISPARSE_OK &&
+      (desc->fetch == HISPARSE_FETCH_SDMA || desc->fetch == HISPARSE_FETCH_STAGED)) {
     if (hipHostMalloc(reinterpret_cast<void**>(&c->h_plan_count), U * 4, 0) != hipSuccess ||
         hipHostMalloc(reinterpret_cast<void**>(&c->h_plan), U * K * sizeof(int2), 0) !=
             hipSuccess) {
@@ -517,7 +541,8 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
                                 int32_t part_hi = 256) {
   if (nu < 0) nu = c->units - u0;
   if (c->desc.fetch == HISPARSE_FETCH_NONE || nu == 0 || part_lo >= part_hi) return HISPARSE_OK;
-  if (c->desc.fetch == HISPARSE_FETCH_SDMA && n_layers > 1) {
+  if ((c->desc.fetch == HISPARSE_FETCH_SDMA || c->desc.fetch == HISPARSE_FETCH_STAGED) &&
+      n_layers > 1) {
     for (int32_t j = 0; j < n_layers; ++j) {
       const hisparse_status_t st =
           enqueue_fetch(c, anchor, target + j, stream, u0, nu, 1, part_lo, part_hi);
@@ -526,6 +551,87 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
     return HISPARSE_OK;
   }
   auto& an = c->anchors[anchor / c->desc.share_group];
+  if (c->desc.fetch == HISPARSE_FETCH_STAGED) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &cs) != hipSuccess) return HISPARSE_ERR_HIP;
+    if (cs != hipStreamCaptureStatusNone) return HISPARSE_ERR_UNSUPPORTED;
+    const size_t U = (size_t)c->units, K = (size_t)c->desc.top_k;
+    // the plan, once the resolve that wrote it has run (and the previous staged copy out of
+    // the staging buffer with it: same stream)
+    if (hipMemcpyAsync(c->h_plan_count, an.plan_count, U * 4, hipMemcpyDeviceToHost, stream) !=
+            hipSuccess ||
+        hipMemcpyAsync(c->h_plan, an.plan, U * K * sizeof(int2), hipMemcpyDeviceToHost,
+                       stream) != hipSuccess ||
+        hipStreamSynchronize(stream) != hipSuccess)
+      return HISPARSE_ERR_HIP;
+    const size_t R = (size_t)c->desc.record_bytes, L = (size_t)c->desc.num_records;
+    int32_t* prefix = reinterpret_cast<int32_t*>(c->stage_host);
+    // entries of the range per unit; prefix[u] = first packed entry of unit u
+    std::vector<int32_t> lo(U, 0);
+    int32_t n = 0;
+    for (size_t u = 0; u < U; ++u) {
+      const int32_t m = c->h_plan_count[u];
+      const bool in = u >= (size_t)u0 && u < (size_t)u0 + (size_t)nu;
+      lo[u] = (m * part_lo) >> 8;
+      prefix[u] = n;
+      if (in) n += ((m * part_hi) >> 8) - lo[u];
+    }
+    prefix[U] = n;
+    if (n == 0) return HISPARSE_OK;
+    const size_t off = stage_rec_offset(U);
+    uint8_t* rec = c->stage_host + off;
+    const uint8_t* host = reinterpret_cast<const uint8_t*>(c->host[target]);
+    const int2* plan = c->h_plan;
+    if (hipMemcpyAsync(c->stage_dev, c->stage_host, off, hipMemcpyHostToDevice, stream) !=
+        hipSuccess)
+      return HISPARSE_ERR_HIP;
+    // The worker threads gather the records in increasing order, in pieces of about 1 MiB;
+    // this thread enqueues each piece's copy as soon as the piece is packed, so the copy
+    // engine moves one piece while the workers gather the next (with no worker thread, this
+    // thread gathers everything first).
+    constexpr int64_t kGrain = 16;  // entries per hand-out; a piece is a whole number of them
+    const int64_t piece = std::max<int64_t>(4, (int64_t)((1 << 20) / R) / kGrain) * kGrain;
+    const int64_t n_pieces = (n + piece - 1) / piece;
+    std::vector<std::atomic<int64_t>> packed(n_pieces);
+    for (auto& x : packed) x.store(0);
+    const std::function<void(int64_t, int64_t)> gather = [&](int64_t b, int64_t e) {
+      size_t u = std::upper_bound(prefix, prefix + U + 1, (int32_t)b) - prefix - 1;
+      for (int64_t j = b; j < e; ++j) {
+        while (j >= prefix[u + 1]) ++u;
+        const int2 pe = plan[u * K + lo[u] + (j - prefix[u])];
+        memcpy(rec + (size_t)j * R, host + (u * L + (size_t)pe.x) * R, R);
+      }
+      packed[b / piece].fetch_add(e - b, std::memory_order_release);
+    };
+    const bool async = c->gather->threads() > 1;
+    if (async) c->gather->start(n, kGrain, gather);
+    else c->gather->run(n, kGrain, gather);
+    hisparse_status_t copy_st = HISPARSE_OK;
+    for (int64_t q = 0; q < n_pieces; ++q) {
+      const int64_t p0 = q * piece, p1 = std::min<int64_t>(n, p0 + piece);
+      while (packed[q].load(std::memory_order_acquire) < p1 - p0) std::this_thread::yield();
+      if (copy_st == HISPARSE_OK &&
+          hipMemcpyAsync(c->stage_dev + off + (size_t)p0 * R, rec + (size_t)p0 * R,
+                         (size_t)(p1 - p0) * R, hipMemcpyHostToDevice, stream) != hipSuccess)
+        copy_st = HISPARSE_ERR_HIP;
+    }
+    if (async) c->gather->wait();
+    if (copy_st != HISPARSE_OK) return copy_st;
+    // the scatter reads each unit's range of the plan: the same entries, in plan order
+    hisparse::ScatterArgs sa{};
+    sa.stage = c->stage_dev;
+    sa.plan = an.plan;
+    sa.cache = c->cache[target];
+    sa.rec_offset = (int64_t)stage_rec_offset(U);
+    sa.B = c->desc.capacity;
+    sa.k = c->desc.top_k;
+    sa.R = c->desc.record_bytes;
+    sa.units = c->units;
+    sa.plan_count = an.plan_count;
+    sa.part_lo = part_lo;
+    if (hisparse::launch_scatter(sa, stream) != hipSuccess) return HISPARSE_ERR_HIP;
+    return HISPARSE_OK;
+  }
   if (c->desc.fetch == HISPARSE_FETCH_SDMA) {
     hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
     if (hipStreamIsCapturing(stream, &cs) != hipSuccess) return HISPARSE_ERR_HIP;

@@ -6,6 +6,7 @@
 
 #include <vector>
 
+#include "gather_pool.h"
 #include "hisparse.h"
 
 namespace hisparse {
@@ -93,7 +94,20 @@ struct StateArgs {
   int32_t B, units;
 };
 
+// Staged fetch: records packed per unit in a device staging buffer, each unit's run starting at
+// entry prefix[u] (prefix: [units + 1] int32 at the buffer's start, records from rec_offset).
+struct ScatterArgs {
+  const uint8_t* stage;        // device staging buffer
+  const int2* plan;            // [units][k] (position, slot)
+  const int32_t* plan_count;   // [units]
+  uint8_t* cache;              // [units][B][R]
+  int64_t rec_offset;          // bytes before the first record
+  int32_t B, k, R, units;
+  int32_t part_lo;             // unit u's packed run is its plan entries from m * part_lo / 256
+};
+
 hipError_t launch_resolve(const ResolveArgs& a, hipStream_t stream);
+hipError_t launch_scatter(const ScatterArgs& a, hipStream_t stream);
 hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgroups,
                         hipStream_t stream);
 hipError_t launch_reset_state(const StateArgs& a, hipStream_t stream);
@@ -154,9 +168,15 @@ struct hisparse_cache {
   std::vector<Anchor> anchors;   // per anchor layer (layer / share_group)
   std::vector<uint8_t> request_taken;  // request slots handed out by hisparse_request_acquire
   int32_t* err = nullptr;        // device error word
-  // HISPARSE_FETCH_SDMA: pinned readback of a plan and the host-side copy lists
+  // HISPARSE_FETCH_SDMA / _STAGED: pinned readback of a plan and the host-side copy lists
   int32_t* h_plan_count = nullptr;
   int2* h_plan = nullptr;
   std::vector<void*> dma_dst, dma_src;
   std::vector<size_t> dma_size;
+  // HISPARSE_FETCH_STAGED: pinned and device staging buffers ([units + 1] prefix, then up to
+  // units * top_k records) and the host threads that gather into the pinned one
+  uint8_t* stage_host = nullptr;
+  uint8_t* stage_dev = nullptr;
+  size_t stage_bytes = 0;
+  hisparse::GatherPool* gather = nullptr;
 };

@@ -416,6 +416,27 @@ __global__ __launch_bounds__(kFetchThreads) void fetch_kernel(FetchArgs a, FastD
                  gridDim.x * (uint32_t)kFetchThreads);
 }
 
+// Staged fetch: the records packed per unit in the device staging buffer go to their slots
+// (16-byte pieces; grid y = unit). The staging layout and the plan range come from the host.
+__global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
+  typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+  const int u = blockIdx.y;
+  const int32_t* prefix = reinterpret_cast<const int32_t*>(a.stage);
+  const int32_t first = prefix[u], n = prefix[u + 1] - first;
+  const int32_t lo = (a.plan_count[u] * a.part_lo) >> 8;
+  const uint32_t cpr = (uint32_t)a.R >> 4;
+  const uint32_t total = (uint32_t)n * cpr;
+  const uint8_t* src = a.stage + a.rec_offset + (int64_t)first * a.R;
+  const int2* plan = a.plan + (int64_t)u * a.k + lo;
+  uint8_t* cache = a.cache + (int64_t)u * a.B * a.R;
+  for (uint32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < total;
+       c += gridDim.x * blockDim.x) {
+    const uint32_t r = c / cpr, w = c - r * cpr;
+    const v4u v = *reinterpret_cast<const v4u*>(src + (int64_t)r * a.R + (w << 4));
+    *reinterpret_cast<v4u*>(cache + (int64_t)plan[r].y * a.R + (w << 4)) = v;
+  }
+}
+
 // Write-through (Section 3.3 (4)). One workgroup per (unit, share group). The table side is
 // the canonical LRU applied to the one-position selection {pos}, specialised: the anchor's
 // clock advances; a resident position has its stamp refreshed to 2t and its slot moved to the
@@ -542,6 +563,13 @@ hipError_t launch_resolve(const ResolveArgs& a, hipStream_t stream) {
     case 512: return launch_resolve_nt<512>(a, lds, stream);
     default: return launch_resolve_nt<1024>(a, lds, stream);
   }
+}
+
+hipError_t launch_scatter(const ScatterArgs& a, hipStream_t stream) {
+  // a few workgroups per unit: each unit's run is at most k records (HBM to HBM)
+  const int per_unit = std::max(1, std::min(64, 256 / std::max(1, a.units)));
+  hipLaunchKernelGGL(scatter_kernel, dim3(per_unit, a.units), dim3(256), 0, stream, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgroups,

@@ -27,6 +27,7 @@ HISPARSE_ERR_FULL = -6
 HISPARSE_FETCH_ZERO_COPY = 0
 HISPARSE_FETCH_SDMA = 1
 HISPARSE_FETCH_NONE = 2
+HISPARSE_FETCH_STAGED = 3
 
 HISPARSE_ATTN_DEFER_MERGE = 1
 HISPARSE_ATTN_BESIDE_FETCH = 2

@@ -56,7 +56,7 @@ def test_workload_descriptors_are_valid(cfg):
     ("share_group", 0, hs.HISPARSE_ERR_INVALID_ARG),
     ("num_requests", 0, hs.HISPARSE_ERR_INVALID_ARG),
     ("units_per_request", 70000, hs.HISPARSE_ERR_INVALID_ARG),
-    ("fetch", 3, hs.HISPARSE_ERR_UNSUPPORTED),
+    ("fetch", 4, hs.HISPARSE_ERR_UNSUPPORTED),                # no such fetch path
     ("host_memory", 7, hs.HISPARSE_ERR_INVALID_ARG),
     ("transfer_block_bytes", 48, hs.HISPARSE_ERR_INVALID_ARG),
     ("fetch_workgroups", -1, hs.HISPARSE_ERR_INVALID_ARG),

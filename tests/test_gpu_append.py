@@ -23,7 +23,8 @@ from paper_2608_07009_amd import hisparse as hs
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("fetch", [hs.HISPARSE_FETCH_ZERO_COPY, hs.HISPARSE_FETCH_SDMA])
+@pytest.mark.parametrize("fetch", [hs.HISPARSE_FETCH_ZERO_COPY, hs.HISPARSE_FETCH_SDMA,
+                                   hs.HISPARSE_FETCH_STAGED])
 def test_append_write_through_matches_oracle(fetch):
     steps, NL, G = 60, 4, 2  # two share groups (anchors 0 and 2), one append call for all
     base = W.workload(1, num_layers=NL, share_group=G, num_requests=2)

@@ -231,7 +231,8 @@ def test_fetch_group_equals_fetch_and_replays():
 
 @pytest.mark.parametrize("cfg,fetch", [(2, hs.HISPARSE_FETCH_ZERO_COPY),
                                        (3, hs.HISPARSE_FETCH_ZERO_COPY),
-                                       (2, hs.HISPARSE_FETCH_SDMA)])
+                                       (2, hs.HISPARSE_FETCH_SDMA),
+                                       (3, hs.HISPARSE_FETCH_STAGED)])
 def test_decode_prefetch_equals_separate(cfg, fetch):
     """Attention of one layer carrying the replay into later shared layers in the same launch
     gives bit-identical attention outputs and byte-identical caches to the replay and the
@@ -343,7 +344,8 @@ def test_deferred_merge_equals_fused(cfg):
                                              (2, hs.HISPARSE_FETCH_ZERO_COPY, 1),
                                              (2, hs.HISPARSE_FETCH_ZERO_COPY, 256),
                                              (3, hs.HISPARSE_FETCH_ZERO_COPY, 200),
-                                             (2, hs.HISPARSE_FETCH_SDMA, 64)])
+                                             (2, hs.HISPARSE_FETCH_SDMA, 64),
+                                             (2, hs.HISPARSE_FETCH_STAGED, 100)])
 def test_merge_carried_replay_equals_separate(cfg, fetch, share):
     """The overlap schedule with the merges starting the replay into the layer after next
     (hisparse_attention_merge_prefetch over the first share/256 of each unit's plan) and the

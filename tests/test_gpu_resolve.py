@@ -89,19 +89,29 @@ def test_resolve_fetch_none_same_tables():
         b.close()
 
 
-@pytest.mark.parametrize("cfg,steps", [(1, 24), (3, 24)])
-def test_sdma_fetch_matches_zero_copy(cfg, steps):
-    """The host-issued DMA fetch path moves exactly the bytes the zero-copy kernel moves."""
-    w = W.workload(cfg, num_layers=1)
+@pytest.mark.parametrize("cfg,steps,fetch", [(1, 24, hs.HISPARSE_FETCH_SDMA),
+                                             (3, 24, hs.HISPARSE_FETCH_SDMA),
+                                             (1, 24, hs.HISPARSE_FETCH_STAGED),
+                                             (2, 6, hs.HISPARSE_FETCH_STAGED),
+                                             (3, 24, hs.HISPARSE_FETCH_STAGED),
+                                             (4, 6, hs.HISPARSE_FETCH_STAGED)])
+def test_host_issued_fetch_matches_zero_copy(cfg, steps, fetch):
+    """The host-issued fetch paths (per-run copy-engine copies; host-gathered staging, one
+    copy and a device scatter) move exactly the bytes the zero-copy kernel moves, and the
+    resident bytes equal the oracle's host records."""
+    w = W.workload(cfg, num_layers=1, num_requests=min(W.workload(cfg).num_requests, 4))
     a = Run(w, steps)
-    b = Run(w, steps, fetch=hs.HISPARSE_FETCH_SDMA)
+    b = Run(w, steps, fetch=fetch)
+    orc = oracle.OracleCache(w.units, w.L, w.B, w.k)
     try:
         for t in range(steps):
             a.resolve_step(t)
             b.resolve_step(t)
             assert torch.equal(a.slots, b.slots) and torch.equal(a.counts, b.counts)
+            orc.resolve(b.sel_host[t, :w.units])
             if t in (0, steps // 2, steps - 1):
                 assert (layer_cache_host(a, 0) == layer_cache_host(b, 0)).all(), f"step {t}"
+                check_resident_bytes(b, 0, orc)
     finally:
         a.close()
         b.close()
@@ -271,3 +281,29 @@ def d2h_cache(cache, layer):
     from hs_harness import d2h
     ptr, n = cache.layer_cache(layer)
     return d2h(ptr, n)
+
+
+@pytest.mark.parametrize("fetch", [hs.HISPARSE_FETCH_SDMA, hs.HISPARSE_FETCH_STAGED])
+def test_host_issued_fetch_refused_under_capture(fetch):
+    """The host-issued fetch paths read the plan back with a synchronisation, so a fetch enqueued
+    while the stream is capturing a HIP graph is refused (nothing is enqueued), and the same
+    call works eagerly afterwards."""
+    w = W.workload(1, num_layers=1)
+    run = Run(w, 1, fetch=fetch)
+    try:
+        run.resolve_step(0)
+        torch.cuda.synchronize()
+        s = torch.cuda.Stream()
+        g = torch.cuda.CUDAGraph()
+        err = None
+        with torch.cuda.graph(g, stream=s):
+            try:
+                hs.hisparse_fetch(run.cache.handle, 0, s)
+            except hs.HisparseError as e:
+                err = e
+        assert err is not None and err.status == hs.HISPARSE_ERR_UNSUPPORTED
+        hs.hisparse_fetch(run.cache.handle, 0, run.stream)
+        torch.cuda.synchronize()
+    finally:
+        torch.cuda.synchronize()
+        run.close()

@@ -21,7 +21,8 @@ from paper_2608_07009_amd import hisparse as hs
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("fetch", [hs.HISPARSE_FETCH_ZERO_COPY, hs.HISPARSE_FETCH_SDMA])
+@pytest.mark.parametrize("fetch", [hs.HISPARSE_FETCH_ZERO_COPY, hs.HISPARSE_FETCH_SDMA,
+                                   hs.HISPARSE_FETCH_STAGED])
 def test_speculate_matches_oracle(fetch):
     steps, NL = 12, 3
     w = W.workload(2, num_requests=4, num_layers=NL, share_group=1)
