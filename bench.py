@@ -516,6 +516,169 @@ def run_all(args) -> int:
     return 0
 
 
+class DecodeSchedule:
+    """The call sequence of one decode step of every micro-batch (library calls, event records
+    and stream waits), independent of how the calls reach the GPU: the benchmark passes the
+    library and HIP's event calls, the CPU tests pass recorders. Layers run in model order per
+    micro-batch: a layer's attention follows the previous layer's (its query depends on it).
+    Per share group: resolve of the anchor, the transfers of its misses, then attention of each
+    layer of the group. Micro-batches (mbs) carry integer device addresses and streams."""
+
+    def __init__(self, *, w, k, groups, mbs, n_mb, n_qv, ad_ref, lib, rec, wait, root_s, fork_ev,
+                 join_evs, schedule, turns, speculate, append, share, status_string):
+        self.w, self.k, self.groups, self.mbs, self.n_mb, self.n_qv = w, k, groups, mbs, n_mb, n_qv
+        self.ad_ref, self.L, self.rec, self.wait, self.root_s = ad_ref, lib, rec, wait, root_s
+        self.fork_ev, self.join_evs = fork_ev, join_evs
+        self.schedule, self.turns, self.speculate, self.append = schedule, turns, speculate, append
+        self.share, self.status_string = share, status_string
+
+    def events_per_step(self) -> int:
+        """Timing events one step may consume (two per library call)."""
+        return self.n_mb * (2 + sum(2 * (4 + 3 * len(sh) + int(self.speculate))
+                                    for _, sh in self.groups))
+
+    def call(self, name, stream, ev, spans, fn, *fargs):
+        """One library call; with ev (timing events, consumed in order) bracketed by events."""
+        if ev is not None:
+            e0, e1 = ev.pop(), ev.pop()
+            self.rec(e0, stream)
+        rc = fn(*fargs)
+        if rc != 0:
+            raise RuntimeError(f"{name} -> {self.status_string(rc)}")
+        if ev is not None:
+            self.rec(e1, stream)
+            spans.append((name, e0, e1))
+
+    def group_step(self, mb, gi, t, ev, spans, sel_override, q_override, link):
+        """Share group gi of decode step t for one micro-batch. `link`: (event to wait for
+        before this group's host-link transfer, event to record after it), or None."""
+        L, call, rec, wait, k, w = self.L, self.call, self.rec, self.wait, self.k, self.w
+        a, shared = self.groups[gi]
+        qv = q_override[mb.u0] if q_override else mb.q_p[t % self.n_qv]
+        h, ms, ss = mb.h, mb.main, mb.side
+        sp = sel_override[mb.u0][a] if sel_override else mb.sel_p[t][a]
+        cp = None if sel_override else mb.cnt_p[t][a]
+        call("resolve_tables", ms, ev, spans, L.hisparse_resolve_tables, h, a, sp, mb.slot_p[a],
+             cp, ms)
+
+        def merge(units, out_p):
+            call("attention_merge", ms, ev, spans, L.hisparse_attention_merge, units, k,
+                 w.record_bytes, self.ad_ref, out_p, mb.ws_ptr, mb.ws_bytes, ms)
+
+        def decode(l):
+            call("sparse_decode", ms, ev, spans, L.hisparse_sparse_decode, h, l, qv[l],
+                 mb.slot_p[a], mb.out_p[l], self.ad_ref, mb.ws_ptr, mb.ws_bytes, ms)
+            merge(mb.U, mb.out_p[l])
+
+        def transfer(name, fn, *fargs):
+            if link and link[0] is not None:
+                wait(ms, link[0], 0)
+            call(name, ms, ev, spans, fn, *fargs)
+            if link:
+                rec(link[1], ms)
+
+        if not shared:
+            transfer("fetch", L.hisparse_fetch, h, a, ms)
+            nxt = a + 1
+            if self.speculate and nxt < w.num_layers:
+                # this layer's selection as a hint for the next layer, on the side stream
+                # under this layer's attention; the next layer's resolve waits for it
+                rec(mb.sync[0], ms)
+                wait(ss, mb.sync[0], 0)
+                scp = None if sel_override else mb.spec_p[t][nxt]
+                call("speculate", ss, ev, spans, L.hisparse_speculate, h, nxt, sp, scp, ss)
+                rec(mb.sync[1], ss)
+            decode(a)
+            if self.speculate and nxt < w.num_layers:
+                wait(ms, mb.sync[1], 0)
+        elif self.schedule == "serial":
+            # the anchor's fetch and its shared layers' replays in one launch, then the
+            # layers' attention in order
+            transfer("fetch_group", L.hisparse_fetch_group, h, a, 1 + len(shared), ms)
+            for l in [a] + shared:
+                decode(l)
+        elif self.schedule == "batched":
+            # NOT realisable inside a model (the queries of a group's later layers depend on
+            # the earlier layers' outputs): one attention launch for the whole group
+            transfer("fetch_group", L.hisparse_fetch_group, h, a, 1 + len(shared), ms)
+            call("sparse_decode_layers", ms, ev, spans, L.hisparse_sparse_decode_layers, h, a,
+                 1 + len(shared), qv[a], mb.slot_p[a], mb.out_p[a], self.ad_ref, mb.ws_ptr,
+                 mb.ws_bytes, ms)
+            merge(mb.U * (1 + len(shared)), mb.out_p[a])
+        elif self.schedule == "side":
+            # as soon as the resolve has recorded the plan, a side stream replays it into all
+            # shared layers in one launch, sharing the host link with the anchor's own fetch
+            # and running under the anchor's attention; the shared layers' attention waits
+            rec(mb.sync[0], ms)
+            wait(ss, mb.sync[0], 0)
+            call("prefetch_replay", ss, ev, spans, L.hisparse_prefetch_layers, h, a, shared[0],
+                 len(shared), ss)
+            rec(mb.sync[1], ss)
+            transfer("fetch", L.hisparse_fetch, h, a, ms)
+            decode(a)
+            wait(ms, mb.sync[1], 0)
+            for l in shared:
+                decode(l)
+        else:
+            # overlap (Section 3.5), on one stream: the anchor's fetch, then each layer's
+            # attention launch carries the replay of the plan into the next shared layer, so
+            # layer l+1's misses cross the host link while layer l attends; with a merge share,
+            # the merge after layer l's attention already starts the replay into layer l+2 and
+            # layer l+1's attention carries the rest
+            share = self.share
+            transfer("fetch", L.hisparse_fetch, h, a, ms)
+            layers = [a] + shared
+            for i, l in enumerate(layers[:-1]):
+                lo = share if (share and i >= 1) else 0  # begun by the previous merge
+                call("sparse_decode_prefetch", ms, ev, spans,
+                     L.hisparse_sparse_decode_prefetch_part, h, l, qv[l], mb.slot_p[a],
+                     mb.out_p[l], self.ad_ref, mb.ws_ptr, mb.ws_bytes, a, layers[i + 1], 1, lo,
+                     256, ms)
+                if share and i + 2 < len(layers):
+                    call("attention_merge_prefetch", ms, ev, spans,
+                         L.hisparse_attention_merge_prefetch, h, self.ad_ref, mb.out_p[l],
+                         mb.ws_ptr, mb.ws_bytes, a, layers[i + 2], 1, 0, share, ms)
+                else:
+                    merge(mb.U, mb.out_p[l])
+            decode(layers[-1])
+
+    def step(self, t, ev=None, spans=None, sel_override=None, q_override=None, fork=True,
+             join=True, app_override=None):
+        """Enqueue decode step t of every micro-batch: forked from the root stream, joined back
+        into it. Micro-batches take turns on the host link: the transfer of group g of
+        micro-batch i waits for that of micro-batch i-1 (and micro-batch 0's for the last
+        micro-batch's transfer of group g-1), so while one micro-batch moves its misses the
+        others resolve and attend instead of splitting the link and falling into lockstep.
+        With turns "first" only the first group is ordered this way; from that offset the
+        chains run free, with no cross-stream wait per layer."""
+        mbs, n_mb, rec, wait = self.mbs, self.n_mb, self.rec, self.wait
+        if n_mb > 1 and fork:
+            rec(self.fork_ev, self.root_s)
+            for mb in mbs[1:]:
+                wait(mb.main, self.fork_ev, 0)
+        for gi in range(len(self.groups)):
+            for i, mb in enumerate(mbs):
+                link = None
+                if n_mb > 1 and (self.turns == "all" or gi == 0):
+                    prev = (mbs[i - 1].link[gi] if i > 0 else
+                            (mbs[-1].link[gi - 1] if gi > 0 else None))
+                    link = (prev, mb.link[gi])
+                self.group_step(mb, gi, t, ev, spans, sel_override, q_override, link)
+        if self.append:
+            # write-through of the step's generated record of every layer, one launch per
+            # micro-batch after its last attention (an admission may evict a slot the step
+            # read; the next step's resolves come after it on the same stream)
+            for mb in mbs:
+                pos_p, rec_p = app_override[mb.u0] if app_override else (mb.pos_p[t],
+                                                                          mb.new_p[t])
+                self.call("append", mb.main, ev, spans, self.L.hisparse_append, mb.h, 0,
+                          self.w.num_layers, pos_p, rec_p, mb.adm_ptr, mb.main)
+        if n_mb > 1 and join:
+            for mb, je in zip(mbs[1:], self.join_evs[1:]):
+                rec(je, mb.main)
+                wait(self.root_s, je, 0)
+
+
 def main() -> int:
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -653,6 +816,7 @@ def main() -> int:
             self.ws_bytes = max(hs.hisparse_decode_workspace_bytes(m * U, k, w.record_bytes, ad)
                                 for m in range(1, G + 1))
             self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
+            self.ws_ptr = self.ws.data_ptr()
             sl = slice(self.u0, self.u0 + U)
             self.sel_p = [[sel[t, (a // G) * U_all + self.u0:(a // G) * U_all + self.u0 + U]
                            .data_ptr() for a in range(w.num_layers)] for t in range(steps_needed)]
@@ -674,10 +838,15 @@ def main() -> int:
                 self.pos = (torch.arange(steps_needed, dtype=torch.int32, device=dev)
                             .add_(w.L).unsqueeze(1).repeat(1, U).contiguous())
                 self.adm = torch.empty((len(groups), U), dtype=torch.int32, device=dev)
+                self.pos_p = [self.pos[t].data_ptr() for t in range(steps_needed)]
+                self.new_p = [self.new[t].data_ptr() for t in range(steps_needed)]
+                self.adm_ptr = self.adm.data_ptr()
             self.link = [hip.event(timing=False) for _ in groups]
             if args.speculate:  # {already resident, fetched} of every hint event
                 self.spec_counts = torch.zeros((steps_needed, w.num_layers, U, 2),
                                                dtype=torch.int32, device=dev)
+                self.spec_p = [[self.spec_counts[t, l].data_ptr() for l in range(w.num_layers)]
+                               for t in range(steps_needed)]
 
     mbs = [MicroBatch(i) for i in range(n_mb)]
     cache = mbs[0].cache
@@ -687,156 +856,15 @@ def main() -> int:
         f"{w.host_pool_bytes() / 2**30:.1f} GiB, {n_mb} micro-batch(es), schedule "
         f"{args.schedule}, set up in {time.time() - t0:.1f}s")
 
-    f_tables, f_fetch = L.hisparse_resolve_tables, L.hisparse_fetch
-    f_prefetch_layers, f_decode = L.hisparse_prefetch_layers, L.hisparse_sparse_decode
-    f_decode_prefetch = L.hisparse_sparse_decode_prefetch
-    f_append, f_speculate = L.hisparse_append, L.hisparse_speculate
-    f_decode_layers, f_fetch_group = L.hisparse_sparse_decode_layers, L.hisparse_fetch_group
-    f_merge = L.hisparse_attention_merge
-    f_decode_prefetch_part = L.hisparse_sparse_decode_prefetch_part
-    f_merge_prefetch = L.hisparse_attention_merge_prefetch
     share = max(0, min(256, args.merge_replay_share))
     rec = hip.L.hipEventRecord
     wait = hip.L.hipStreamWaitEvent
-
-    def check(rc, what):
-        if rc != 0:
-            raise RuntimeError(f"{what} -> {hs.hisparse_status_string(rc)}")
-
-    def call(name, stream, ev, spans, fn, *fargs):
-        """One library call; with ev (timing events, consumed in order) bracketed by events."""
-        if ev is not None:
-            e0, e1 = ev.pop(), ev.pop()
-            rec(e0, stream)
-        check(fn(*fargs), name)
-        if ev is not None:
-            rec(e1, stream)
-            spans.append((name, e0, e1))
-
-    def group_step(mb, gi, t, ev, spans, sel_override, q_override, link):
-        """Share group gi of decode step t for one micro-batch, layers in model order: every
-        layer's attention follows the previous layer's (its query depends on it). `link`:
-        (event to wait for before this group's host-link transfer, event to record after it),
-        or None."""
-        a, shared = groups[gi]
-        qv = q_override[mb.u0] if q_override else mb.q_p[t % n_qv]
-        h, ms, ss = mb.h, mb.main, mb.side
-        sp = sel_override[mb.u0][a] if sel_override else mb.sel_p[t][a]
-        cp = None if sel_override else mb.cnt_p[t][a]
-        call("resolve_tables", ms, ev, spans, f_tables, h, a, sp, mb.slot_p[a], cp, ms)
-
-        def merge(units, out_p):
-            call("attention_merge", ms, ev, spans, f_merge, units, k, w.record_bytes, ad_ref,
-                 out_p, mb.ws.data_ptr(), mb.ws_bytes, ms)
-
-        def decode(l):
-            call("sparse_decode", ms, ev, spans, f_decode, h, l, qv[l], mb.slot_p[a],
-                 mb.out_p[l], ad_ref, mb.ws.data_ptr(), mb.ws_bytes, ms)
-            merge(mb.U, mb.out_p[l])
-
-        def transfer(name, fn, *fargs):
-            if link and link[0] is not None:
-                wait(ms, link[0], 0)
-            call(name, ms, ev, spans, fn, *fargs)
-            if link:
-                rec(link[1], ms)
-
-        if not shared:
-            transfer("fetch", f_fetch, h, a, ms)
-            nxt = a + 1
-            if args.speculate and nxt < w.num_layers:
-                # this layer's selection as a hint for the next layer, on the side stream
-                # under this layer's attention; the next layer's resolve waits for it
-                rec(mb.sync[0], ms)
-                wait(ss, mb.sync[0], 0)
-                scp = None if sel_override else mb.spec_counts[t, nxt].data_ptr()
-                call("speculate", ss, ev, spans, f_speculate, h, nxt, sp, scp, ss)
-                rec(mb.sync[1], ss)
-            decode(a)
-            if args.speculate and nxt < w.num_layers:
-                wait(ms, mb.sync[1], 0)
-        elif args.schedule == "serial":
-            # the anchor's fetch and its shared layers' replays in one launch, then the
-            # layers' attention in order
-            transfer("fetch_group", f_fetch_group, h, a, 1 + len(shared), ms)
-            for l in [a] + shared:
-                decode(l)
-        elif args.schedule == "batched":
-            # NOT realisable inside a model (the queries of a group's later layers depend on
-            # the earlier layers' outputs): one attention launch for the whole group
-            transfer("fetch_group", f_fetch_group, h, a, 1 + len(shared), ms)
-            call("sparse_decode_layers", ms, ev, spans, f_decode_layers, h, a, 1 + len(shared),
-                 qv[a], mb.slot_p[a], mb.out_p[a], ad_ref, mb.ws.data_ptr(), mb.ws_bytes, ms)
-            merge(mb.U * (1 + len(shared)), mb.out_p[a])
-        elif args.schedule == "side":
-            # as soon as the resolve has recorded the plan, a side stream replays it into all
-            # shared layers in one launch, sharing the host link with the anchor's own fetch
-            # and running under the anchor's attention; the shared layers' attention waits
-            rec(mb.sync[0], ms)
-            wait(ss, mb.sync[0], 0)
-            call("prefetch_replay", ss, ev, spans, f_prefetch_layers, h, a, shared[0],
-                 len(shared), ss)
-            rec(mb.sync[1], ss)
-            transfer("fetch", f_fetch, h, a, ms)
-            decode(a)
-            wait(ms, mb.sync[1], 0)
-            for l in shared:
-                decode(l)
-        else:
-            # overlap (Section 3.5), on one stream: the anchor's fetch, then each layer's
-            # attention launch carries the replay of the plan into the next shared layer, so
-            # layer l+1's misses cross the host link while layer l attends; with a merge share,
-            # the merge after layer l's attention already starts the replay into layer l+2 and
-            # layer l+1's attention carries the rest, so the link keeps moving through merges
-            transfer("fetch", f_fetch, h, a, ms)
-            layers = [a] + shared
-            for i, l in enumerate(layers[:-1]):
-                lo = share if (share and i >= 1) else 0  # begun by the previous merge
-                call("sparse_decode_prefetch", ms, ev, spans, f_decode_prefetch_part, h, l,
-                     qv[l], mb.slot_p[a], mb.out_p[l], ad_ref, mb.ws.data_ptr(), mb.ws_bytes,
-                     a, layers[i + 1], 1, lo, 256, ms)
-                if share and i + 2 < len(layers):
-                    call("attention_merge_prefetch", ms, ev, spans, f_merge_prefetch, h, ad_ref,
-                         mb.out_p[l], mb.ws.data_ptr(), mb.ws_bytes, a, layers[i + 2], 1, 0,
-                         share, ms)
-                else:
-                    merge(mb.U, mb.out_p[l])
-            decode(layers[-1])
-
-    def step(t, ev=None, spans=None, sel_override=None, q_override=None, fork=True, join=True,
-             app_override=None):
-        """Enqueue decode step t of every micro-batch: forked from the root stream, joined back
-        into it. Micro-batches take turns on the host link: the transfer of group g of
-        micro-batch i waits for that of micro-batch i-1 (and micro-batch 0's for the last
-        micro-batch's transfer of group g-1), so while one micro-batch moves its misses the
-        others resolve and attend instead of splitting the link and falling into lockstep.
-        With --turns first only the first group is ordered this way; from that offset the
-        chains run free, with no cross-stream wait per layer."""
-        if n_mb > 1 and fork:
-            rec(fork_ev, root_s)
-            for mb in mbs[1:]:
-                wait(mb.main, fork_ev, 0)
-        for gi in range(len(groups)):
-            for i, mb in enumerate(mbs):
-                link = None
-                if n_mb > 1 and (args.turns == "all" or gi == 0):
-                    prev = (mbs[i - 1].link[gi] if i > 0 else
-                            (mbs[-1].link[gi - 1] if gi > 0 else None))
-                    link = (prev, mb.link[gi])
-                group_step(mb, gi, t, ev, spans, sel_override, q_override, link)
-        if args.append:
-            # write-through of the step's generated record of every layer, one launch per
-            # micro-batch after its last attention (an admission may evict a slot the step
-            # read; the next step's resolves come after it on the same stream)
-            for mb in mbs:
-                pos_p, rec_p = app_override[mb.u0] if app_override else (
-                    mb.pos[t].data_ptr(), mb.new[t].data_ptr())
-                call("append", mb.main, ev, spans, f_append, mb.h, 0, w.num_layers, pos_p,
-                     rec_p, mb.adm.data_ptr(), mb.main)
-        if n_mb > 1 and join:
-            for mb, je in zip(mbs[1:], join_evs[1:]):
-                rec(je, mb.main)
-                wait(root_s, je, 0)
+    sched = DecodeSchedule(w=w, k=k, groups=groups, mbs=mbs, n_mb=n_mb, n_qv=n_qv, ad_ref=ad_ref,
+                           lib=L, rec=rec, wait=wait, root_s=root_s, fork_ev=fork_ev,
+                           join_evs=join_evs, schedule=args.schedule, turns=args.turns,
+                           speculate=args.speculate, append=args.append, share=share,
+                           status_string=hs.hisparse_status_string)
+    step = sched.step
 
     # pinned H2D sweep over the same pool (hipMemcpyAsync), before the timed region
     sweep = {}
@@ -851,8 +879,7 @@ def main() -> int:
     step(0)
     torch.cuda.synchronize()
     cold_ms = (time.perf_counter() - tc) * 1e3
-    per_step_events = n_mb * (2 + sum(2 * (4 + 3 * len(sh) + int(args.speculate))
-                                      for _, sh in groups))
+    per_step_events = sched.events_per_step()
     host_ms = 0.0
     for t in range(1, args.warmup):
         # the last warm-up step is enqueued as the span pass enqueues (with its event pairs),
@@ -989,7 +1016,9 @@ def main() -> int:
     t_mpf, n_mpf = kernel("attention_merge_prefetch")
     merge_carried = 0
     if n_mpf:
-        m_units = c[:, [a for a, sh in groups if len(sh) >= 2], :, 1]  # [steps][groups][units]
+        # misses per [step][group][unit] (index the layer axis alone: a list and a scalar index
+        # around a slice would move the indexed axis first)
+        m_units = c[..., 1][:, [a for a, sh in groups if len(sh) >= 2], :]
         for gi, (a, sh) in enumerate([g for g in groups if len(g[1]) >= 2]):
             merge_carried += int(((m_units[:, gi, :] * share) >> 8).sum()) * (len(sh) - 1)
         merge_carried *= R

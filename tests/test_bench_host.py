@@ -99,3 +99,131 @@ def test_compact_keeps_the_per_workload_figures():
     c = bench.compact(d)
     assert c["layers"] == 56 and c["layers_in_workload"] == 61 and "extra" not in c
     assert c["roofline"] == {"frac": 0.7} and c["kernels_avg_us"] == {"fetch": 27.12}
+
+
+class _FakeHip:
+    """Events and streams as integers; every record and wait is logged and checked: no use of
+    a destroyed event, no wait on an event that was never recorded."""
+
+    def __init__(self):
+        self.next, self.live, self.recorded, self.log = 1000, set(), set(), []
+
+    def event(self):
+        self.next += 1
+        self.live.add(self.next)
+        return self.next
+
+    def destroy(self, e):
+        assert e in self.live, "event destroyed twice"
+        self.live.discard(e)
+        self.recorded.discard(e)
+
+    def rec(self, e, stream):
+        assert e in self.live, "record of a destroyed event"
+        self.recorded.add(e)
+        self.log.append(("rec", e, stream))
+        return 0
+
+    def wait(self, stream, e, flags):
+        assert e in self.live, "wait on a destroyed event"
+        assert e in self.recorded, "wait on an event never recorded"
+        self.log.append(("wait", stream, e))
+        return 0
+
+
+class _FakeLib:
+    def __init__(self, log):
+        self._log = log
+
+    def __getattr__(self, name):
+        if not name.startswith("hisparse_"):
+            raise AttributeError(name)
+
+        def call(*args):
+            self._log.append(("call", name, args[-1]))  # the stream is the last argument
+            return 0
+        return call
+
+
+def _schedule(hip, *, layers, G, n_mb, schedule, speculate, append, turns, share, steps):
+    from types import SimpleNamespace
+    w = SimpleNamespace(num_layers=layers, record_bytes=1152)
+    groups = [(a, list(range(a + 1, min(a + G, layers)))) for a in range(0, layers, G)]
+    mbs = []
+    for i in range(n_mb):
+        base = 10_000 * (i + 1)
+        mbs.append(SimpleNamespace(
+            u0=4 * i, U=4, h=7 + i, main=100 + 2 * i, side=101 + 2 * i,
+            q_p=[[base + 10 * v + l for l in range(layers)] for v in range(2)],
+            sel_p=[[base + 1000 + 100 * t + l for l in range(layers)] for t in range(steps)],
+            cnt_p=[[base + 5000 + 100 * t + l for l in range(layers)] for t in range(steps)],
+            spec_p=[[base + 7000 + 100 * t + l for l in range(layers)] for t in range(steps)],
+            pos_p=[base + 9000 + t for t in range(steps)],
+            new_p=[base + 9500 + t for t in range(steps)],
+            slot_p=[base + 200 + l for l in range(layers)],
+            out_p=[base + 300 + l for l in range(layers)], ws_ptr=base + 400, ws_bytes=1 << 20,
+            adm_ptr=base + 500, sync=[hip.event(), hip.event()],
+            link=[hip.event() for _ in groups]))
+    return bench.DecodeSchedule(
+        w=w, k=2048, groups=groups, mbs=mbs, n_mb=n_mb, n_qv=2, ad_ref=None,
+        lib=_FakeLib(hip.log), rec=hip.rec, wait=hip.wait, root_s=1, fork_ev=hip.event(),
+        join_evs=[hip.event() for _ in mbs], schedule=schedule, turns=turns,
+        speculate=speculate, append=append, share=share, status_string=str)
+
+
+TRANSFERS = ("hisparse_fetch", "hisparse_fetch_group")
+
+
+def test_decode_schedule_events_and_turns():
+    """Every option of the benchmark's decode step, run through recorders: the timing events a
+    step consumes stay within its budget and are distinct, no stream waits on an event that was
+    destroyed or never recorded (warm-up steps without timing events, then timed steps whose
+    events are destroyed after each step), and with turns taken at every layer each micro-batch's
+    transfer waits for the previous transfer's event, in the order of groups and micro-batches."""
+    cases = []
+    for schedule in ("overlap", "serial", "side", "batched"):
+        for n_mb in (1, 2, 3):
+            cases.append(dict(layers=8, G=4, n_mb=n_mb, schedule=schedule, speculate=False,
+                              append=False, turns="all", share=0))
+    cases += [dict(layers=8, G=4, n_mb=2, schedule="overlap", speculate=False, append=True,
+                   turns="first", share=64),
+              dict(layers=6, G=1, n_mb=2, schedule="overlap", speculate=True, append=True,
+                   turns="all", share=0),
+              dict(layers=6, G=1, n_mb=1, schedule="overlap", speculate=True, append=False,
+                   turns="all", share=0),
+              dict(layers=61, G=4, n_mb=1, schedule="overlap", speculate=False, append=False,
+                   turns="all", share=64)]
+    steps = 6
+    for case in cases:
+        hip = _FakeHip()
+        sched = _schedule(hip, steps=steps, **case)
+        budget = sched.events_per_step()
+        timing = set()
+        for t in range(2):  # warm-up: no timing events
+            sched.step(t)
+        for t in range(2, steps):
+            ev = [hip.event() for _ in range(budget)]
+            given = list(ev)
+            timing.update(given)
+            spans = []
+            sched.step(t, ev, spans)
+            used = [e for _, e0, e1 in spans for e in (e0, e1)]
+            assert len(used) == len(set(used)) <= budget, case
+            assert set(used) <= set(given), case
+            for e in given:  # the span pass keeps them longer; destroying early is stricter
+                hip.destroy(e)
+        # turns: each transfer after the first of a step waits for the previous transfer's
+        # link event
+        if case["n_mb"] > 1 and case["turns"] == "all":
+            mbs = sched.mbs
+            log = [x for x in hip.log if not (x[0] == "rec" and x[1] in timing)]
+            calls = [i for i, x in enumerate(log) if x[0] == "call" and x[1] in TRANSFERS]
+            n_groups = len(sched.groups)
+            per_step = n_groups * case["n_mb"]
+            assert len(calls) == steps * per_step, case
+            for j, i in enumerate(calls):
+                g, m = divmod(j % per_step, case["n_mb"])
+                assert log[i + 1] == ("rec", mbs[m].link[g], mbs[m].main), case
+                if j % per_step:
+                    pg, pm = divmod(j % per_step - 1, case["n_mb"])
+                    assert log[i - 1] == ("wait", mbs[m].main, mbs[pm].link[pg]), case
