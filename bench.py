@@ -98,6 +98,11 @@ def parse():
                          "attention carries the rest; 0 = merges carry nothing (measured "
                          "faster: each launch that carries part of a replay pays the host "
                          "reads' ramp again)")
+    ap.add_argument("--handover-share", type=int, default=0, metavar="S",
+                    help="micro-batches taking turns on the link: each fetch is issued as two "
+                         "launches (hisparse_fetch_part), the first S/256 of each unit's plan and "
+                         "the rest, and the next micro-batch's transfer may start after the "
+                         "first, so its start latency overlaps this one's tail; 0 = one launch")
     ap.add_argument("--append", action="store_true",
                     help="decode loop with a growing context: after each share group's "
                          "attention, write the step's generated record of every layer through "
@@ -525,17 +530,19 @@ class DecodeSchedule:
     layer of the group. Micro-batches (mbs) carry integer device addresses and streams."""
 
     def __init__(self, *, w, k, groups, mbs, n_mb, n_qv, ad_ref, lib, rec, wait, root_s, fork_ev,
-                 join_evs, schedule, turns, speculate, append, share, status_string):
+                 join_evs, schedule, turns, speculate, append, share, status_string,
+                 handover=0):
         self.w, self.k, self.groups, self.mbs, self.n_mb, self.n_qv = w, k, groups, mbs, n_mb, n_qv
         self.ad_ref, self.L, self.rec, self.wait, self.root_s = ad_ref, lib, rec, wait, root_s
         self.fork_ev, self.join_evs = fork_ev, join_evs
         self.schedule, self.turns, self.speculate, self.append = schedule, turns, speculate, append
         self.share, self.status_string = share, status_string
+        self.handover = handover  # 256ths of a fetch after which the link turn passes on
 
     def events_per_step(self) -> int:
         """Timing events one step may consume (two per library call)."""
-        return self.n_mb * (2 + sum(2 * (4 + 3 * len(sh) + int(self.speculate))
-                                    for _, sh in self.groups))
+        return self.n_mb * (2 + sum(2 * (4 + 3 * len(sh) + int(self.speculate) +
+                                         int(self.handover > 0)) for _, sh in self.groups))
 
     def call(self, name, stream, ev, spans, fn, *fargs):
         """One library call; with ev (timing events, consumed in order) bracketed by events."""
@@ -577,8 +584,17 @@ class DecodeSchedule:
             if link:
                 rec(link[1], ms)
 
+        def fetch():
+            """The anchor's own fetch; with a hand-over share and a link turn, in two launches
+            with the turn passed on between them."""
+            if link and 0 < self.handover < 256:
+                transfer("fetch", L.hisparse_fetch_part, h, a, 0, self.handover, ms)
+                call("fetch", ms, ev, spans, L.hisparse_fetch_part, h, a, self.handover, 256, ms)
+            else:
+                transfer("fetch", L.hisparse_fetch, h, a, ms)
+
         if not shared:
-            transfer("fetch", L.hisparse_fetch, h, a, ms)
+            fetch()
             nxt = a + 1
             if self.speculate and nxt < w.num_layers:
                 # this layer's selection as a hint for the next layer, on the side stream
@@ -614,7 +630,7 @@ class DecodeSchedule:
             call("prefetch_replay", ss, ev, spans, L.hisparse_prefetch_layers, h, a, shared[0],
                  len(shared), ss)
             rec(mb.sync[1], ss)
-            transfer("fetch", L.hisparse_fetch, h, a, ms)
+            fetch()
             decode(a)
             wait(ms, mb.sync[1], 0)
             for l in shared:
@@ -626,7 +642,7 @@ class DecodeSchedule:
             # the merge after layer l's attention already starts the replay into layer l+2 and
             # layer l+1's attention carries the rest
             share = self.share
-            transfer("fetch", L.hisparse_fetch, h, a, ms)
+            fetch()
             layers = [a] + shared
             for i, l in enumerate(layers[:-1]):
                 lo = share if (share and i >= 1) else 0  # begun by the previous merge
@@ -863,7 +879,8 @@ def main() -> int:
                            lib=L, rec=rec, wait=wait, root_s=root_s, fork_ev=fork_ev,
                            join_evs=join_evs, schedule=args.schedule, turns=args.turns,
                            speculate=args.speculate, append=args.append, share=share,
-                           status_string=hs.hisparse_status_string)
+                           status_string=hs.hisparse_status_string,
+                           handover=max(0, min(256, args.handover_share)))
     step = sched.step
 
     # pinned H2D sweep over the same pool (hipMemcpyAsync), before the timed region
@@ -1293,6 +1310,7 @@ def main() -> int:
                    "speculate": args.speculate, "xlayer_overlap": args.xlayer_overlap,
                    "host_memory": args.host_memory, "mode": mode,
                    "merge_replay_share": share if args.schedule == "overlap" else None,
+                   "handover_share": args.handover_share if n_mb > 1 else None,
                    "attn_plan": "beside-fetch" if beside else "own-gpu",
                    "steps_per_graph": graph["steps_per_graph"] if graph else None},
         "decode_tokens_per_s": w.num_requests * K / wall,

@@ -255,6 +255,14 @@ hisparse_status_t hisparse_resolve_tables(hisparse_cache_t cache, int32_t layer,
                                           int32_t* d_counts, void* stream);
 hisparse_status_t hisparse_fetch(hisparse_cache_t cache, int32_t layer, void* stream);
 
+/* [async] Phase 4 for entries [m * part_begin / 256, m * part_end / 256) of each unit's plan
+ * of m entries only, 0 <= part_begin <= part_end <= 256: calls over adjacent ranges together
+ * equal hisparse_fetch. A caller that hands the host link from one stream to another can let
+ * the next stream's transfer start after the first part (an event recorded between the calls)
+ * while the rest of this one still runs. */
+hisparse_status_t hisparse_fetch_part(hisparse_cache_t cache, int32_t layer, int32_t part_begin,
+                                      int32_t part_end, void* stream);
+
 /* [async] Phase 4 for units [unit_begin, unit_begin + unit_count) of an anchor layer only
  * (Section 3.4; units are independent caches). Calls over disjoint ranges together equal
  * hisparse_fetch, so a caller can pipeline a layer's fetch with the attention of the units

@@ -706,6 +706,13 @@ hisparse_status_t hisparse_fetch(hisparse_cache_t c, int32_t layer, void* stream
   return enqueue_fetch(c, layer, layer, as_stream(stream));
 }
 
+hisparse_status_t hisparse_fetch_part(hisparse_cache_t c, int32_t layer, int32_t part_begin,
+                                      int32_t part_end, void* stream) {
+  if (!c || !is_anchor(c, layer) || part_begin < 0 || part_begin > part_end || part_end > 256)
+    return HISPARSE_ERR_INVALID_ARG;
+  return enqueue_fetch(c, layer, layer, as_stream(stream), 0, -1, 1, part_begin, part_end);
+}
+
 hisparse_status_t hisparse_fetch_units(hisparse_cache_t c, int32_t layer, int32_t unit_begin,
                                        int32_t unit_count, void* stream) {
   if (!c || !is_anchor(c, layer) || unit_begin < 0 || unit_count < 0 ||

@@ -42,7 +42,8 @@ EXPORTED = (
     "hisparse_status_string", "hisparse_validate_desc", "hisparse_validate_attn",
     "hisparse_cache_create", "hisparse_cache_destroy", "hisparse_host_pool",
     "hisparse_layer_cache", "hisparse_reset", "hisparse_resolve", "hisparse_resolve_tables",
-    "hisparse_fetch", "hisparse_fetch_units", "hisparse_fetch_group", "hisparse_prefetch_layer",
+    "hisparse_fetch", "hisparse_fetch_part", "hisparse_fetch_units", "hisparse_fetch_group",
+    "hisparse_prefetch_layer",
     "hisparse_prefetch_layers", "hisparse_append", "hisparse_request_acquire",
     "hisparse_request_release", "hisparse_reset_units", "hisparse_stage", "hisparse_speculate",
     "hisparse_decode_workspace_bytes", "hisparse_sparse_decode", "hisparse_sparse_decode_layers",
@@ -109,6 +110,7 @@ def lib() -> ctypes.CDLL:
             "hisparse_resolve": (_I32, [_V, _I32, _V, _V, _V, _V]),
             "hisparse_resolve_tables": (_I32, [_V, _I32, _V, _V, _V, _V]),
             "hisparse_fetch": (_I32, [_V, _I32, _V]),
+            "hisparse_fetch_part": (_I32, [_V, _I32, _I32, _I32, _V]),
             "hisparse_fetch_units": (_I32, [_V, _I32, _I32, _I32, _V]),
             "hisparse_fetch_group": (_I32, [_V, _I32, _I32, _V]),
             "hisparse_prefetch_layer": (_I32, [_V, _I32, _I32, _V]),
@@ -258,6 +260,12 @@ def hisparse_resolve_tables(cache: int, layer: int, d_sel, d_slots, d_counts=Non
 
 def hisparse_fetch(cache: int, layer: int, stream=None) -> None:
     _check("hisparse_fetch", lib().hisparse_fetch(cache, layer, _s(stream)))
+
+
+def hisparse_fetch_part(cache: int, layer: int, part_begin: int, part_end: int,
+                        stream=None) -> None:
+    _check("hisparse_fetch_part",
+           lib().hisparse_fetch_part(cache, layer, part_begin, part_end, _s(stream)))
 
 
 def hisparse_fetch_units(cache: int, layer: int, unit_begin: int, unit_count: int,

@@ -145,7 +145,8 @@ class _FakeLib:
         return call
 
 
-def _schedule(hip, *, layers, G, n_mb, schedule, speculate, append, turns, share, steps):
+def _schedule(hip, *, layers, G, n_mb, schedule, speculate, append, turns, share, steps,
+              handover=0):
     from types import SimpleNamespace
     w = SimpleNamespace(num_layers=layers, record_bytes=1152)
     groups = [(a, list(range(a + 1, min(a + G, layers)))) for a in range(0, layers, G)]
@@ -168,10 +169,10 @@ def _schedule(hip, *, layers, G, n_mb, schedule, speculate, append, turns, share
         w=w, k=2048, groups=groups, mbs=mbs, n_mb=n_mb, n_qv=2, ad_ref=None,
         lib=_FakeLib(hip.log), rec=hip.rec, wait=hip.wait, root_s=1, fork_ev=hip.event(),
         join_evs=[hip.event() for _ in mbs], schedule=schedule, turns=turns,
-        speculate=speculate, append=append, share=share, status_string=str)
+        speculate=speculate, append=append, share=share, status_string=str, handover=handover)
 
 
-TRANSFERS = ("hisparse_fetch", "hisparse_fetch_group")
+TRANSFERS = ("hisparse_fetch", "hisparse_fetch_group", "hisparse_fetch_part")
 
 
 def test_decode_schedule_events_and_turns():
@@ -192,7 +193,13 @@ def test_decode_schedule_events_and_turns():
               dict(layers=6, G=1, n_mb=1, schedule="overlap", speculate=True, append=False,
                    turns="all", share=0),
               dict(layers=61, G=4, n_mb=1, schedule="overlap", speculate=False, append=False,
-                   turns="all", share=64)]
+                   turns="all", share=64),
+              dict(layers=8, G=1, n_mb=2, schedule="overlap", speculate=False, append=True,
+                   turns="all", share=0, handover=200),
+              dict(layers=8, G=4, n_mb=3, schedule="side", speculate=False, append=False,
+                   turns="all", share=0, handover=128),
+              dict(layers=6, G=1, n_mb=2, schedule="overlap", speculate=True, append=False,
+                   turns="all", share=0, handover=100)]
     steps = 6
     for case in cases:
         hip = _FakeHip()
@@ -216,8 +223,11 @@ def test_decode_schedule_events_and_turns():
         # link event
         if case["n_mb"] > 1 and case["turns"] == "all":
             mbs = sched.mbs
+            links = {e for mb in mbs for e in mb.link}
             log = [x for x in hip.log if not (x[0] == "rec" and x[1] in timing)]
-            calls = [i for i, x in enumerate(log) if x[0] == "call" and x[1] in TRANSFERS]
+            # a transfer that holds the link turn: followed by the record of a link event
+            calls = [i for i, x in enumerate(log) if x[0] == "call" and x[1] in TRANSFERS and
+                     log[i + 1][0] == "rec" and log[i + 1][1] in links]
             n_groups = len(sched.groups)
             per_step = n_groups * case["n_mb"]
             assert len(calls) == steps * per_step, case
@@ -227,3 +237,6 @@ def test_decode_schedule_events_and_turns():
                 if j % per_step:
                     pg, pm = divmod(j % per_step - 1, case["n_mb"])
                     assert log[i - 1] == ("wait", mbs[m].main, mbs[pm].link[pg]), case
+                if case.get("handover"):  # the rest of the fetch after the turn passed on
+                    assert log[i][1] == "hisparse_fetch_part", case
+                    assert log[i + 2] == ("call", "hisparse_fetch_part", mbs[m].main), case

@@ -307,3 +307,30 @@ def test_host_issued_fetch_refused_under_capture(fetch):
     finally:
         torch.cuda.synchronize()
         run.close()
+
+
+@pytest.mark.parametrize("fetch", [hs.HISPARSE_FETCH_ZERO_COPY, hs.HISPARSE_FETCH_STAGED])
+def test_fetch_parts_equal_fetch(fetch):
+    """hisparse_fetch_part over adjacent plan ranges moves exactly what hisparse_fetch moves
+    (every resident slot holds its host record); bad ranges are argument errors."""
+    w = W.workload(2, num_requests=3, num_layers=1)
+    steps = 4
+    a, b = Run(w, steps), Run(w, steps, fetch=fetch)
+    try:
+        for t in range(steps):
+            a.resolve_step(t)
+            hs.hisparse_resolve_tables(b.cache.handle, 0, b.sel_ptr(t, 0), b.slots[0],
+                                       b.counts[0], b.stream)
+            cuts = [0, 37 + 40 * t, 200, 256]
+            for lo, hi in zip(cuts[:-1], cuts[1:]):
+                hs.hisparse_fetch_part(b.cache.handle, 0, lo, hi, b.stream)
+            torch.cuda.synchronize()
+            assert torch.equal(a.slots, b.slots) and torch.equal(a.counts, b.counts)
+            assert (layer_cache_host(a, 0) == layer_cache_host(b, 0)).all(), f"step {t}"
+        for lo, hi in ((-1, 10), (20, 10), (0, 300)):
+            with pytest.raises(hs.HisparseError):
+                hs.hisparse_fetch_part(b.cache.handle, 0, lo, hi, b.stream)
+    finally:
+        torch.cuda.synchronize()
+        a.close()
+        b.close()
