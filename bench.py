@@ -188,10 +188,11 @@ def pinned_sweep(torch, hip: Hip, host_ptr: int, host_bytes: int, dev, stream: i
     return res
 
 
-def traffic_record(workload: str, kernel: str):
+def traffic_record(workload: str, kernel: str, plan: str | None = None):
     """HBM bytes per launch of `kernel` on `workload`, from the rocprofv3 FETCH_SIZE and
     WRITE_SIZE runs summarised under profiles/ (counter values already scaled by a plain copy
-    of known size), or None when no summary matches the current source of that kernel."""
+    of known size), or None when no summary matches the current source of that kernel. A
+    record that names an attention plan applies to runs with that plan only."""
     import glob
     import hashlib
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
@@ -200,6 +201,8 @@ def traffic_record(workload: str, kernel: str):
                 continue
             kv = dict(f.split("=", 1) for f in line.split()[1:])
             if kv.get("workload") != workload or kv.get("kernel") != kernel:
+                continue
+            if "plan" in kv and kv["plan"] != plan:
                 continue
             # source=a[,b...]: the kernel's source files; sha256 over their bytes in that order
             srcs = [os.path.join(ROOT, x) for x in kv["source"].split(",")]
@@ -1162,7 +1165,12 @@ def main() -> int:
         else:
             roof = {"kernel": dom, "bound": "mfma", "achieved": kd["mfma_TFLOPs"],
                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": kd["mfma_frac"]}
-        roof.update({"traffic": None, "algorithmic_bytes_per_launch": att_bytes_call,
+        tr = traffic_record(w.name, "sparse_decode", "beside-fetch" if beside else "own-gpu")
+        if tr:
+            tr["algorithmic_bytes_per_launch"] = att_bytes_call
+            tr["vs_algorithmic"] = (tr["fetch_bytes"] + tr["write_bytes"]) / att_bytes_call
+        roof.update({"traffic": (tr["fetch_bytes"] + tr["write_bytes"]) if tr else None,
+                     "traffic_detail": tr, "algorithmic_bytes_per_launch": att_bytes_call,
                      "flops_per_launch": att_flops_call})
     else:
         kd = kernels["resolve_tables"]

@@ -58,6 +58,14 @@ def test_traffic_record_follows_the_kernel_sources(tmp_path, monkeypatch):
     assert bench.traffic_record("w1", "fetch") is None
     b.unlink()  # a missing source: no record either
     assert bench.traffic_record("w1", "fetch") is None
+    # a record that names an attention plan applies to that plan only
+    b.write_bytes(b"#pragma once\n")
+    with open(tmp_path / "profiles" / "k.md", "a") as f:
+        f.write(f"traffic-record workload=w1 kernel=sparse_decode plan=own-gpu source=src/k.hip,src/k.h "
+                f"sha256={sha} fetch_bytes=7 write_bytes=8\n")
+    assert bench.traffic_record("w1", "sparse_decode", "own-gpu")["write_bytes"] == 8
+    assert bench.traffic_record("w1", "sparse_decode", "beside-fetch") is None
+    assert bench.traffic_record("w1", "sparse_decode") is None
 
 
 def test_cpu_baseline_runs_every_unit_on_threads():
