@@ -256,7 +256,9 @@ def cpu_baseline(w, host_unit, budget_s: float) -> dict:
     units (every (anchor layer, unit) stream of the workload) runs the canonical-LRU resolve of
     every step, with each step's misses gathered from the host pool into the unit's cache image,
     until the time budget is used; then float64 attention, timed separately, over a sample of
-    units of the last resolved step. host_unit(layer, unit) -> uint8 [L][R] host records."""
+    units of the last resolved step. `value` is the resolve's rate; whole_step_selections_per_s
+    combines both rates into the decode step's (one resolve and G attentions per anchor stream
+    and step). host_unit(layer, unit) -> uint8 [L][R] host records."""
     import threading
 
     import numpy as np
@@ -333,6 +335,10 @@ def cpu_baseline(w, host_unit, budget_s: float) -> dict:
         th.join()
     dta = time.perf_counter() - ta
     n_units_att = sum(n_att[i] for i in range(T) if last[i])
+    att_rate = n_units_att / dta if dta > 0 else None
+    # the whole decode step from the two measured rates: per (anchor layer, unit) step, one
+    # resolve of k selections and one attention per layer of the share group, G k served
+    whole = (G * k / (k / (sels / dt) + G / att_rate)) if (att_rate and sels > 0) else None
     return {"value": sels / dt, "unit": "selections/s", "cores": T, "kind": "oracle",
             "cpu_model": cpu_model(),
             "sample": f"canonical-LRU resolve of steps 0..{steps_done - 1} (at least; "
@@ -341,7 +347,8 @@ def cpu_baseline(w, host_unit, budget_s: float) -> dict:
                       f"the unit's cache image, {T} threads over disjoint units, {dt:.1f} s",
             "resolve_steps_done": steps_done, "resolve_steps_in_workload": int(sel_all.shape[0]),
             "attention_us_per_unit": 1e6 * sum(att_t) / max(1, n_units_att),
-            "attention_units_per_s": n_units_att / dta if dta > 0 else None,
+            "attention_units_per_s": att_rate,
+            "whole_step_selections_per_s": whole,
             "attention_sample": f"float64 attention of {n_units_att} units ({w.q_heads} heads "
                                 f"over {k} records) of the last resolved step through their "
                                 f"slots, {T} threads, {dta:.1f} s"}

@@ -82,6 +82,7 @@ def test_cpu_baseline_runs_every_unit_on_threads():
     assert 1 <= r["cores"] <= w.units * w.num_layers
     assert 1 <= r["resolve_steps_done"] <= r["resolve_steps_in_workload"] == w.steps
     assert r["attention_us_per_unit"] > 0 and r["cpu_model"]
+    assert 0 < r["whole_step_selections_per_s"] < r["value"]
 
 
 def test_default_run_tries_every_workload_in_a_child(tmp_path):
