@@ -119,6 +119,9 @@ def parse():
                     help="also measure prefill staging (hisparse_stage): one request's records "
                          "of every layer copied device-to-host into the host pools, alone against "
                          "a pinned device-to-host hipMemcpy sweep, and while the decode steps run")
+    ap.add_argument("--resolve-phases", action="store_true",
+                    help="time the resolve kernel's phases with the phase-timing build "
+                         "(every workload, or --config N)")
     ap.add_argument("--resolve-sweep", action="store_true",
                     help="only time resolve (no IO) across cache sizes B/k = 1..8 and 1..64 "
                          "units on the 32K-context DSA/MLA streams, one JSON line per point")
@@ -469,6 +472,58 @@ def resolve_sweep(args, torch, hs, W, HiSparseCache) -> int:
     return 0
 
 
+PHASE_NAMES = ("stage_probe", "bucket_count", "bucket_scan", "order_misses", "victims",
+               "recency_tail", "tables_plan_slots", "end")
+
+
+def resolve_phases(args, torch, hs, W, HiSparseCache) -> int:
+    """The resolve kernel's phases (Section 4.4's breakdown) on each workload's first anchor
+    layer, from the phase-timing build: the workload's selection stream resolved against its
+    cache with the tables exact (no IO), 8 warm-up steps, then per step the launch bracketed by
+    HIP events and the wall-clock stamps of up to 64 units read back. One JSON line per workload:
+    µs per phase (mean over steps and units), the stamped kernel span and the event span."""
+    import numpy as np
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    warm, steps = 8, 32
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for c in ([args.config] if args.config_given else [1, 2, 3, 4, 5]):
+        w0 = W.workload(c)
+        # one anchor layer; a micro-batch's share of the requests where the step runs two
+        n_req = w0.num_requests // 2 if w0.num_requests >= 2 else w0.num_requests
+        w = dataclasses.replace(w0, num_requests=n_req, num_layers=1, share_group=1)
+        sel = torch.from_numpy(W.selection_streams(w, steps=warm + steps)).to(dev)
+        cache = HiSparseCache.for_workload(w, fetch=hs.HISPARSE_FETCH_NONE)
+        slots = torch.empty((w.units, w.k), dtype=torch.int32, device=dev)
+        counts = torch.empty((w.units, 2), dtype=torch.int32, device=dev)
+        for t in range(warm):
+            hs.hisparse_resolve_tables(cache.handle, 0, sel[t], slots, counts, stream)
+        torch.cuda.synchronize()
+        n = min(w.units, hs.HISPARSE_RESOLVE_PHASE_UNITS)
+        durs, spans, ev_us, misses = [], [], [], []
+        for t in range(steps):
+            e0.record(stream)
+            hs.hisparse_resolve_tables(cache.handle, 0, sel[warm + t], slots, counts, stream)
+            e1.record(stream)
+            st, rate = hs.hisparse_debug_resolve_phases(n)
+            ev_us.append(e0.elapsed_time(e1) * 1e3)
+            st = st[:, :9].astype(np.float64) * 1e6 / rate
+            durs.append(np.diff(st, axis=1))            # [units][8]
+            spans.append(st[:, 8] - st[:, 0])
+            misses.append(counts[:, 1].float().mean().item())
+        cache.close()
+        d = np.concatenate(durs, axis=0)
+        print(json.dumps({"sweep": "resolve_phases", "workload": w0.name, "units": w.units,
+                          "k": w.k, "B": w.B, "L": w.L, "misses_per_unit_step": float(np.mean(misses)),
+                          "phase_us": {name: float(v) for name, v in zip(PHASE_NAMES, d.mean(axis=0))},
+                          "stamped_span_us": float(np.mean(np.concatenate(spans))),
+                          "stamped_span_max_unit_us": float(np.mean([x.max() for x in spans])),
+                          "event_span_us": float(np.mean(ev_us)),
+                          "clock_ticks_per_s": int(rate)}), flush=True)
+    return 0
+
+
 # Workloads of the default run: the headline first, then the others; seconds each child may take.
 ALL_CONFIGS = ((2, 240), (1, 90), (3, 120), (4, 150), (5, 240))
 
@@ -713,8 +768,9 @@ def main() -> int:
                           "are independent caches, so more GPUs shard requests without any "
                           "exchange; run one process per GPU", "n_gpus": args.gpus}))
         return 2
-    if args.config is None and not (args.copy_probe or args.resolve_sweep):
+    if args.config is None and not (args.copy_probe or args.resolve_sweep or args.resolve_phases):
         return run_all(args)
+    args.config_given = args.config is not None
     if args.config is None:
         args.config = 2
 
@@ -736,12 +792,21 @@ def main() -> int:
     import workload as W
     from paper_2608_07009_amd import HiSparseCache, hisparse as hs
 
+    if args.resolve_phases:  # the phase-timing build, loaded in place of the normal library
+        from paper_2608_07009_amd import build as hip_build
+        if not os.path.exists(hip_build.PHASE_STAMPS_LIB_PATH):
+            print(json.dumps({"error": "the phase-timing library is not built (python -m "
+                              "paper_2608_07009_amd.build --phase-stamps)"}))
+            return 1
+        hs.LIB_PATH = hip_build.PHASE_STAMPS_LIB_PATH
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}))
         return 1
     L = hs.lib()  # fails loudly if the HIP library is missing
     if args.resolve_sweep:
         return resolve_sweep(args, torch, hs, W, HiSparseCache)
+    if args.resolve_phases:
+        return resolve_phases(args, torch, hs, W, HiSparseCache)
     hip = Hip()
     w0 = W.workload(args.config)
     if args.requests > 0:  # a different workload: its own name (no profile record applies)

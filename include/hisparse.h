@@ -108,7 +108,8 @@ typedef struct {
                                     or 256 (the paper's swap-in transfer block size); 0 = 16 */
   int32_t fetch_workgroups;      /* one-wave (64-thread) workgroups of one fetch launch,
                                     0 .. 4096, shared by its units and target layers (at least
-                                    one per unit and layer); 0 = 256. A few hundred KB of host
+                                    one per unit and layer); 0 = 192 for records under 4 KiB,
+                                    256 for larger ones (measured best). A few hundred KB of host
                                     reads in flight saturate the link, so a thin grid moves
                                     misses as fast as a wide one while keeping few slow host
                                     reads outstanding per CU, which leaves kernels of other
@@ -480,6 +481,27 @@ hisparse_status_t hisparse_read_plan(hisparse_cache_t cache, int32_t layer, int3
  * the last check (info, if not NULL, receives {layer, unit, number of failing unit-steps}),
  * clearing the latch; otherwise HISPARSE_OK. */
 hisparse_status_t hisparse_check_errors(hisparse_cache_t cache, int32_t* info);
+
+/* Stamps per unit of the resolve kernel's phase timing (see hisparse_debug_resolve_phases). */
+#define HISPARSE_RESOLVE_PHASE_SLOTS 16
+/* The first units whose resolve workgroups record phase stamps. */
+#define HISPARSE_RESOLVE_PHASE_UNITS 64
+
+/* [sync] Diagnostic, Section 4.4's breakdown of the resolve into its phases: in a library built
+ * with HISPARSE_PHASE_STAMPS (`python -m paper_2608_07009_amd.build --phase-stamps`, which
+ * writes lib/libhisparse_phase_stamps.so), the resolve kernel stores the device's constant-rate
+ * wall clock at its phase boundaries, for units below HISPARSE_RESOLVE_PHASE_UNITS, overwriting
+ * the previous launch's stamps. This call waits for the current device and copies the stamps of
+ * the first min(max_units, HISPARSE_RESOLVE_PHASE_UNITS) units into host_stamps (uint64
+ * [units][HISPARSE_RESOLVE_PHASE_SLOTS], caller-owned): slot 0 kernel start, 1 selection staged
+ * and probed (phase 1), 2 misses bucketed, 3 bucket starts scanned, 4 misses in position order
+ * (phase 2), 5 victims chosen (phase 3a), 6 recency index and hit stamps written (phase 3b),
+ * 7 tables, plan and slots updated (phase 5), 8 kernel end; slots 9.. are unused. A unit whose
+ * selection was invalid stops after slot 4. ticks_per_s (if not NULL) receives the clock's rate.
+ * Launches on several streams at once overwrite each other's stamps. In a normal build it
+ * returns HISPARSE_ERR_UNSUPPORTED and touches nothing. */
+hisparse_status_t hisparse_debug_resolve_phases(uint64_t* host_stamps, int32_t max_units,
+                                                int64_t* ticks_per_s);
 
 #ifdef __cplusplus
 }

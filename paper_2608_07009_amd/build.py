@@ -32,13 +32,22 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(os.path.join(LIB_DIR, "obj"), exist_ok=True)
+PHASE_STAMPS_LIB_PATH = os.path.join(LIB_DIR, "libhisparse_phase_stamps.so")
+
+
+def build(verbose: bool = False, phase_stamps: bool = False) -> str:
+    """Compile and link the library. phase_stamps: the phase-timing variant (the resolve kernel
+    records its phase boundaries; hisparse_debug_resolve_phases reads them), written beside the
+    normal library as libhisparse_phase_stamps.so."""
+    tag = "obj_phase_stamps" if phase_stamps else "obj"
+    out = PHASE_STAMPS_LIB_PATH if phase_stamps else LIB_PATH
+    extra = ["-DHISPARSE_PHASE_STAMPS"] if phase_stamps else []
+    os.makedirs(os.path.join(LIB_DIR, tag), exist_ok=True)
     cc = hipcc()
 
     def compile_one(src: str) -> str:
-        obj = os.path.join(LIB_DIR, "obj", src.replace(".hip", ".o"))
-        cmd = [cc, *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        obj = os.path.join(LIB_DIR, tag, src.replace(".hip", ".o"))
+        cmd = [cc, *HIPCC_FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
@@ -48,14 +57,14 @@ def build(verbose: bool = False) -> str:
 
     with cf.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
         objs = list(ex.map(compile_one, SOURCES))
-    tmp = LIB_PATH + ".tmp%d" % os.getpid()
+    tmp = out + ".tmp%d" % os.getpid()
     cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp, "-ldl"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB_PATH)
-    return LIB_PATH
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build(verbose=True, phase_stamps="--phase-stamps" in sys.argv[1:]))

@@ -107,6 +107,10 @@ struct ScatterArgs {
 };
 
 hipError_t launch_resolve(const ResolveArgs& a, hipStream_t stream);
+// Phase stamps of the last resolve launch (phase-timing builds only; else hipErrorNotSupported).
+constexpr int kPhaseStamps = HISPARSE_RESOLVE_PHASE_SLOTS;
+constexpr int kPhaseStampUnits = HISPARSE_RESOLVE_PHASE_UNITS;
+hipError_t read_resolve_phase_stamps(uint64_t* host, int32_t units);
 hipError_t launch_scatter(const ScatterArgs& a, hipStream_t stream);
 hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgroups,
                         hipStream_t stream);

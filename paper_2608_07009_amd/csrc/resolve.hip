@@ -82,6 +82,26 @@ __device__ inline int block_excl_scan(int v, int* s_tmp, int* total) {
 
 __device__ inline bool bit_test(const uint32_t* bm, int s) { return (bm[s >> 5] >> (s & 31)) & 1u; }
 
+#ifdef HISPARSE_PHASE_STAMPS
+__device__ unsigned long long g_phase_stamps[kPhaseStampUnits * kPhaseStamps];
+// Phase-timing build: thread 0 of the workgroups of the first kPhaseStampUnits units stores the
+// constant-rate wall clock at each phase boundary (plain vector stores); the host reads the
+// last launch's stamps with hisparse_debug_resolve_phases. Normal builds compile none of it.
+#define RESOLVE_STAMP(i)                                                                   \
+  do {                                                                                     \
+    if (tid == 0 && unit < kPhaseStampUnits)                                               \
+      g_phase_stamps[unit * kPhaseStamps + (i)] = (unsigned long long)wall_clock64();      \
+  } while (0)
+#define RESOLVE_STAMP_BARRIER() __syncthreads()
+#else
+#define RESOLVE_STAMP(i) \
+  do {                   \
+  } while (0)
+#define RESOLVE_STAMP_BARRIER() \
+  do {                          \
+  } while (0)
+#endif
+
 template <int NT>
 __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   extern __shared__ __align__(16) unsigned char s_dyn[];
@@ -91,6 +111,7 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
 
   const int unit = blockIdx.x;
   const int tid = threadIdx.x;
+  RESOLVE_STAMP(0);
   const int k = a.k, B = a.B;
   const int64_t L = a.L;
   const int k4 = (k + 3) & ~3;
@@ -158,6 +179,7 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   }
   __syncthreads();
   const int m = s_nmiss;
+  RESOLVE_STAMP(1);
 
   // Phase 2: the misses in ascending position order. Bucket them by the high bits of their
   // offset within the misses' own position range (a counting pass), then each miss's rank is
@@ -202,6 +224,7 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
     loc[u] = j < m ? atomicAdd(&s_cnt[bkt[u]], 1) : 0;
   }
   __syncthreads();
+  RESOLVE_STAMP(2);
   {
     // exclusive scan of the bucket counts, kBuckets / NT consecutive buckets per thread
     constexpr int per = (kBuckets + NT - 1) / NT;
@@ -224,6 +247,7 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
     }
   }
   __syncthreads();
+  RESOLVE_STAMP(3);
   if (s_maxb > kScanLimit) {  // workgroup-uniform
     // bitonic sort of the m keys in place, ascending (position, input index); the network's
     // comparators all put the smaller key at the lower index, so indices >= m act as +inf
@@ -303,6 +327,7 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
     __syncthreads();
   }
 
+  RESOLVE_STAMP(4);
   if (s_bad) {  // invalid selection: publish -1 and leave the unit's state untouched
     if (slots_out)
       for (int i = tid; i < k; i += NT) slots_out[i] = -1;
@@ -352,6 +377,7 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
     }
   }
   __syncthreads();
+  RESOLVE_STAMP(5);
 
   // Phase 3b: recency index tail (victims, then hits, each by slot) and hit stamps.
   int nv = 0, nh = 0;
@@ -380,6 +406,8 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
       }
     }
   }
+  RESOLVE_STAMP_BARRIER();
+  RESOLVE_STAMP(6);
 
   // Phase 5: the i-th miss (ascending position) takes the i-th victim.
   for (int q = tid; q < m; q += NT) {
@@ -396,6 +424,7 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
     s_out[i] = v;
   }
   __syncthreads();
+  RESOLVE_STAMP(7);
   if (slots_out)
     for (int i = tid; i < k; i += NT) slots_out[i] = s_out[i];
   if (tid == 0) {
@@ -406,10 +435,14 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
     a.plan_count[unit] = m;
     a.clock[unit] = t;
   }
+  RESOLVE_STAMP(8);
 }
 
 template <int U>
 __global__ __launch_bounds__(kFetchThreads) void fetch_kernel(FetchArgs a, FastDiv div_cpr) {
+  // The fetch shares its CUs with other streams' kernels (the other micro-batch's attention and
+  // merge); its waves issue little but each issue keeps the host link fed, so they go first.
+  __builtin_amdgcn_s_setprio(3);
   // grid z: the target layers (one plan, each layer's own host records and cache)
   fetch_slice<U>(a, div_cpr, blockIdx.y, blockIdx.z,
                  blockIdx.x * (uint32_t)kFetchThreads + threadIdx.x,
@@ -563,6 +596,18 @@ hipError_t launch_resolve(const ResolveArgs& a, hipStream_t stream) {
     case 512: return launch_resolve_nt<512>(a, lds, stream);
     default: return launch_resolve_nt<1024>(a, lds, stream);
   }
+}
+
+hipError_t read_resolve_phase_stamps(uint64_t* host, int32_t units) {
+#ifdef HISPARSE_PHASE_STAMPS
+  return hipMemcpyFromSymbol(host, HIP_SYMBOL(g_phase_stamps),
+                             (size_t)units * kPhaseStamps * sizeof(uint64_t), 0,
+                             hipMemcpyDeviceToHost);
+#else
+  (void)host;
+  (void)units;
+  return hipErrorNotSupported;
+#endif
 }
 
 hipError_t launch_scatter(const ScatterArgs& a, hipStream_t stream) {

@@ -33,6 +33,9 @@ HISPARSE_ATTN_DEFER_MERGE = 1
 HISPARSE_ATTN_BESIDE_FETCH = 2
 HISPARSE_NOALLOC_SCRATCH_BYTES = 64 << 20
 
+HISPARSE_RESOLVE_PHASE_SLOTS = 16
+HISPARSE_RESOLVE_PHASE_UNITS = 64
+
 HISPARSE_HOST_COHERENT = 0
 HISPARSE_HOST_NONCOHERENT = 1
 HISPARSE_HOST_UNCACHED = 2
@@ -52,6 +55,7 @@ EXPORTED = (
     "hisparse_attention_merge_prefetch",
     "hisparse_sparse_decode_pool", "hisparse_sparse_decode_noalloc",
     "hisparse_read_state", "hisparse_read_plan", "hisparse_check_errors",
+    "hisparse_debug_resolve_phases",
 )
 
 
@@ -143,6 +147,7 @@ def lib() -> ctypes.CDLL:
             "hisparse_read_state": (_I32, [_V, _I32, _V, _V, _V, _V, _V]),
             "hisparse_read_plan": (_I32, [_V, _I32, _V, _V]),
             "hisparse_check_errors": (_I32, [_V, _V]),
+            "hisparse_debug_resolve_phases": (_I32, [_V, _I32, ctypes.POINTER(ctypes.c_int64)]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -394,6 +399,18 @@ def hisparse_check_errors(cache: int) -> tuple[int, tuple[int, int, int]]:
     if st not in (HISPARSE_OK, HISPARSE_ERR_BAD_SELECTION):
         raise HisparseError("hisparse_check_errors", st)
     return st, (info[0], info[1], info[2])
+
+
+def hisparse_debug_resolve_phases(max_units: int) -> tuple[np.ndarray, int]:
+    """(uint64 [units][HISPARSE_RESOLVE_PHASE_SLOTS] stamps of the last resolve launch, clock
+    ticks per second); raises HisparseError (UNSUPPORTED) unless the library is a phase-timing
+    build."""
+    n = max(1, min(max_units, HISPARSE_RESOLVE_PHASE_UNITS))
+    out = np.zeros((n, HISPARSE_RESOLVE_PHASE_SLOTS), dtype=np.uint64)
+    rate = ctypes.c_int64(0)
+    _check("hisparse_debug_resolve_phases",
+           lib().hisparse_debug_resolve_phases(out.ctypes.data, n, ctypes.byref(rate)))
+    return out, rate.value
 
 
 def host_view(ptr: int, nbytes: int, dtype=np.uint8) -> np.ndarray:

@@ -172,3 +172,21 @@ def test_largest_topk_and_capacity_are_valid():
         hs.HISPARSE_ERR_INVALID_ARG
     assert hs.hisparse_validate_desc(desc_for(w, top_k=4096, capacity=16385)) == \
         hs.HISPARSE_ERR_INVALID_ARG
+
+
+def test_phase_timing_build_is_a_separate_library():
+    """The phase-timing variant exports the same ABI; the normal library compiles none of the
+    stamps and refuses to read them (no device is touched)."""
+    from paper_2608_07009_amd import build as hip_build
+    assert hs.lib().hisparse_debug_resolve_phases(None, 1, None) == hs.HISPARSE_ERR_UNSUPPORTED
+    with pytest.raises(hs.HisparseError) as e:
+        hs.hisparse_debug_resolve_phases(4)
+    assert e.value.status == hs.HISPARSE_ERR_UNSUPPORTED
+    assert os.path.exists(hip_build.PHASE_STAMPS_LIB_PATH), "build() makes both libraries"
+    lib = ctypes.CDLL(hip_build.PHASE_STAMPS_LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    lib.hisparse_debug_resolve_phases.restype = ctypes.c_int32
+    lib.hisparse_debug_resolve_phases.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]
+    # argument checks come before any device call
+    assert lib.hisparse_debug_resolve_phases(None, 4, None) == hs.HISPARSE_ERR_INVALID_ARG
