@@ -7,10 +7,11 @@
 //            bitmap (a second mark on the same slot is a repeated entry), and append the
 //            misses as (position, input index) keys to LDS.
 //   Phase 2  put the miss keys in ascending position order (what the canonical victim
-//            pairing needs): a counting pass over 2048 buckets of high position bits gives
-//            each bucket's start, and a miss's rank is its bucket start plus the number of
-//            bucket mates at lower positions; a mate at the same position exposes a repeated
-//            miss. A few barriers in all, where a sorting network needs dozens.
+//            pairing needs): a counting pass over up to 2048 buckets of high position bits
+//            (twice the misses, at least 64, when there are at most 256) gives each bucket's
+//            start, and a miss's rank is its bucket start plus the number of bucket mates at
+//            lower positions; a mate at the same position exposes a repeated miss. A few
+//            barriers in all, where a sorting network needs dozens.
 //   Phase 3  victims and recency: the unit keeps a recency index `order` = its slots sorted
 //            by (timestamp, slot). Victims are the first m entries of `order` that were not
 //            hit (one workgroup prefix scan); the new index is
@@ -155,7 +156,6 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   }
 #pragma unroll
   for (int u = 0; u < kMaxPer; ++u) sv[u] = (pv[u] >= 0 && (int64_t)pv[u] < L) ? pt[pv[u]] : -1;
-  for (int b = tid; b < kBuckets; b += NT) s_cnt[b] = 0;
 #pragma unroll
   for (int u = 0; u < kMaxPer; ++u) {
     const int i = tid + u * NT;
@@ -180,6 +180,11 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   __syncthreads();
   const int m = s_nmiss;
   RESOLVE_STAMP(1);
+  // rank buckets: twice the misses (at least 64) for up to 256 misses, so that a few misses
+  // do not pay for a scan over all kBuckets; kBuckets beyond
+  const int nbb = m <= 32 ? 6 : (m <= 256 ? 33 - __clz(m - 1) : kBucketBits);
+  const int nb = 1 << nbb;
+  for (int b = tid; b < nb; b += NT) s_cnt[b] = 0;
 
   // Phase 2: the misses in ascending position order. Bucket them by the high bits of their
   // offset within the misses' own position range (a counting pass), then each miss's rank is
@@ -215,7 +220,7 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   const int pmin = s_pmin;
   const uint32_t span = s_pmax > pmin ? (uint32_t)(s_pmax - pmin) : 0u;  // < 2^31
   const int lg = span ? 32 - __clz(span) : 0;
-  const int shift = lg > kBucketBits ? lg - kBucketBits : 0;
+  const int shift = lg > nbb ? lg - nbb : 0;
   const uint32_t low_mask = (1u << shift) - 1u;
 #pragma unroll
   for (int u = 0; u < kMaxPer; ++u) {
@@ -226,13 +231,15 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   __syncthreads();
   RESOLVE_STAMP(2);
   {
-    // exclusive scan of the bucket counts, kBuckets / NT consecutive buckets per thread
-    constexpr int per = (kBuckets + NT - 1) / NT;
-    int c[per], sum = 0, big = 0;
+    // exclusive scan of the bucket counts, nb / NT consecutive buckets per thread (one for
+    // threads below nb when nb <= NT)
+    constexpr int kPer = (kBuckets + NT - 1) / NT;
+    const int per = nb > NT ? nb / NT : 1;
+    int c[kPer], sum = 0, big = 0;
 #pragma unroll
-    for (int q = 0; q < per; ++q) {
+    for (int q = 0; q < kPer; ++q) {
       const int b = tid * per + q;
-      c[q] = b < kBuckets ? s_cnt[b] : 0;
+      c[q] = (q < per && b < nb) ? s_cnt[b] : 0;
       sum += c[q];
       big = max(big, c[q]);
     }
@@ -240,9 +247,9 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
     int total;
     int run = block_excl_scan<NT>(sum, s_tmp, &total);  // all reads of s_cnt precede it
 #pragma unroll
-    for (int q = 0; q < per; ++q) {
+    for (int q = 0; q < kPer; ++q) {
       const int b = tid * per + q;
-      if (b < kBuckets) s_cnt[b] = run;
+      if (q < per && b < nb) s_cnt[b] = run;
       run += c[q];
     }
   }
@@ -295,7 +302,7 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
       rank[u] = 0;
       if (tid + u * NT < m) {
         const int b0 = s_cnt[bkt[u]];
-        const int b1 = bkt[u] + 1 < kBuckets ? s_cnt[bkt[u] + 1] : m;
+        const int b1 = bkt[u] + 1 < nb ? s_cnt[bkt[u] + 1] : m;
         const uint32_t mine = ((uint32_t)((int)(key[u] >> 32) - pmin)) & low_mask;
         const uint32_t me = (uint32_t)key[u] & 0xFFFu;
         int lower = 0;
@@ -566,8 +573,9 @@ __global__ void reset_state_kernel(StateArgs a) {
 }
 
 template <int NT>
-hipError_t launch_resolve_nt(const ResolveArgs& a, size_t lds, hipStream_t stream) {
-  hipLaunchKernelGGL(resolve_kernel<NT>, dim3(a.units), dim3(NT), lds, stream, a);
+hipError_t launch_resolve_nt(const ResolveArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(resolve_kernel<NT>, dim3(a.units), dim3(NT), resolve_lds_bytes(a.k, a.B),
+                     stream, a);
   return hipGetLastError();
 }
 
@@ -586,15 +594,14 @@ int resolve_threads(int32_t B) {
 }
 
 hipError_t launch_resolve(const ResolveArgs& a, hipStream_t stream) {
-  const size_t lds = resolve_lds_bytes(a.k, a.B);
   const int nt = resolve_threads(a.B);
   if (a.k > kMaxPer * nt) return hipErrorInvalidValue;  // excluded by descriptor validation
   switch (nt) {
-    case 64: return launch_resolve_nt<64>(a, lds, stream);
-    case 128: return launch_resolve_nt<128>(a, lds, stream);
-    case 256: return launch_resolve_nt<256>(a, lds, stream);
-    case 512: return launch_resolve_nt<512>(a, lds, stream);
-    default: return launch_resolve_nt<1024>(a, lds, stream);
+    case 64: return launch_resolve_nt<64>(a, stream);
+    case 128: return launch_resolve_nt<128>(a, stream);
+    case 256: return launch_resolve_nt<256>(a, stream);
+    case 512: return launch_resolve_nt<512>(a, stream);
+    default: return launch_resolve_nt<1024>(a, stream);
   }
 }
 
