@@ -143,11 +143,11 @@ typedef struct {
 #define HISPARSE_ATTN_DEFER_MERGE 1
 /* hisparse_attn_desc_t.flags, a scheduling hint for latent attention: the call runs beside
  * another stream's host-link fetch (e.g. two micro-batches taking turns on the link), whose slow
- * host reads occupy the CUs' memory pipelines. The plan then keeps more loads in flight per
- * workgroup (one token group, up to four head waves) at the cost of twice the split partial
- * results; without it, large enough calls use two token groups per workgroup, which halves the
- * partials and is faster on a GPU of its own. Results differ only within rounding (other split
- * boundaries); each plan is deterministic. */
+ * host reads occupy the memory pipelines of the CUs they run on. The plan then aims at half a
+ * workgroup per CU instead of one (fewer, longer splits): the fetch's waves find CUs without an
+ * attention workgroup, and the split partial results shrink; on a GPU of its own the call is
+ * slower that way. Results differ only within rounding (other split boundaries); each plan is
+ * deterministic. */
 #define HISPARSE_ATTN_BESIDE_FETCH 2
 
 /* Human-readable name of a status code (static storage). */

@@ -1011,18 +1011,11 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
     // over units of 128 heads (us, best split count): 8 units 27.4 against 28.7, 16 units 34.5
     // against 45.9 (4 head waves, 16 splits, the previous plan), 32 units 50.8 against 55.5;
     // below 8 units one token group is faster (2 units 18.7 against 20.7).
-    // With HISPARSE_ATTN_BESIDE_FETCH (another stream's host-link fetch shares the GPU, whose
-    // slow host reads sit in the CUs' memory pipelines) the plan keeps three chunks in flight
-    // per workgroup instead: one token group, 4 head waves when that still gives about a
-    // workgroup per CU with two chunks per split. Inside the two-micro-batch decode step of 16
-    // units of 128 heads, that attention takes 39.7 us against 56.4 with two token groups (the
-    // step 1.754 against 1.777 ms), although alone it is the slower of the two.
+    // With HISPARSE_ATTN_BESIDE_FETCH (another stream's host-link fetch shares the GPU) the
+    // same shapes take half as many workgroups (below): the other half of the CUs is left to
+    // the fetch's waves.
     if (H <= 32) {
       p.hw = 1;
-      p.tg = 1;
-    } else if (attn->flags & HISPARSE_ATTN_BESIDE_FETCH) {
-      const int64_t split_cap = std::max(1, p.n_tok / (2 * kChunk));
-      p.hw = (H > 64 && (int64_t)units * ((H + 127) / 128) * split_cap >= kTargetWorkgroups) ? 4 : 2;
       p.tg = 1;
     } else {
       p.hw = 2;
@@ -1039,6 +1032,14 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
   // a split is a whole number of the workgroup's chunk rounds
   const int chunk = kChunk * (is_mla(*attn) ? p.tg : p.tw);
   const int max_splits = (p.n_tok + chunk - 1) / chunk;
+  // Beside another stream's host-link fetch, latent attention aims at half a workgroup per CU:
+  // the fetch's waves, whose slow host reads occupy the memory pipelines of the CUs they run
+  // on, then find CUs without an attention workgroup. Inside the two-micro-batch decode step
+  // (16 units of 128 heads, 2 token groups, 4 splits) that fetch moves 51.9 GB/s against 50.6
+  // with a workgroup per CU, the step 1.692 against 1.735 ms, and the split partials halve;
+  // the attention itself takes 58 against 40 us, hidden behind the other micro-batch's fetch.
+  const int target = (is_mla(*attn) && (attn->flags & HISPARSE_ATTN_BESIDE_FETCH))
+                         ? kTargetWorkgroups / 2 : kTargetWorkgroups;
   int splits;
   if (attn->num_splits > 0) {
     splits = std::min(attn->num_splits, max_splits);
@@ -1050,7 +1051,7 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
     // columns: 2 chunks per split up to 4 columns, 4 up to 16, 8 beyond (12 units of 128 heads:
     // 39 against 55 us with 22 two-chunk splits).
     const int per_split = units * p.hb;
-    splits = std::max(1, kTargetWorkgroups / per_split);
+    splits = std::max(1, target / per_split);
     int chunks_per_split = 4;
     if (is_mla(*attn)) chunks_per_split = per_split <= 4 ? 2 : (per_split <= 16 ? 4 : 8);
     // a call too small to give even 64 such workgroups is all latency: one chunk per split
@@ -1123,14 +1124,9 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
   a.scale_log2 = attn.scale * 1.4426950408889634f;
 
   if (is_mla(attn)) {
-    switch (p.hw) {
-      case 1: launch_mla<1, 1, 3>(a, stream); break;
-      case 2:
-        if (p.tg == 2) launch_mla<2, 2, 2>(a, stream);
-        else launch_mla<2, 1, 4>(a, stream);
-        break;
-      default: launch_mla<4, 1, 4>(a, stream); break;
-    }
+    if (p.hw == 1) launch_mla<1, 1, 3>(a, stream);
+    else if (p.tg == 2) launch_mla<2, 2, 2>(a, stream);
+    else launch_mla<2, 1, 4>(a, stream);
   } else {
     switch (p.hw) {
       case 1: launch_partial<128, 128, 128, 1, 4, 2>(a, stream); break;
