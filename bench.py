@@ -472,6 +472,50 @@ def resolve_sweep(args, torch, hs, W, HiSparseCache) -> int:
     return 0
 
 
+def attention_alone(torch, hs, hip, mb, w, k, splits, att_bytes, att_flops, stream,
+                    reps: int = 20) -> dict:
+    """Layer 0's attention of one micro-batch (its last step's slots and a query), alone on
+    the GPU: `reps` attention launches back to back between two HIP events, then as many merge
+    launches, with the plan a call gets without the beside-fetch hint (a workspace of its
+    own)."""
+    ad = hs.AttnDesc(w.q_heads, w.d_qk, w.d_v, w.v_offset, w.tokens_per_record, splits,
+                     w.scale, hs.HISPARSE_ATTN_DEFER_MERGE)
+    nb = hs.hisparse_decode_workspace_bytes(mb.U, k, w.record_bytes, ad)
+    ws = torch.empty(nb, dtype=torch.uint8, device="cuda:0")
+    L = hs.lib()
+    e0, e1 = hip.event(), hip.event()
+
+    def attend():
+        rc = L.hisparse_sparse_decode(mb.h, 0, mb.q_p[0][0], mb.slot_p[0], mb.out_p[0],
+                                      ctypes.byref(ad), ws.data_ptr(), nb, stream)
+        if rc != 0:
+            raise RuntimeError(f"hisparse_sparse_decode -> {hs.hisparse_status_string(rc)}")
+
+    def merge():
+        rc = L.hisparse_attention_merge(mb.U, k, w.record_bytes, ctypes.byref(ad), mb.out_p[0],
+                                        ws.data_ptr(), nb, stream)
+        if rc != 0:
+            raise RuntimeError(f"hisparse_attention_merge -> {hs.hisparse_status_string(rc)}")
+
+    out = {}
+    for name, fn in (("attention_us", attend), ("merge_us", merge)):
+        for _ in range(3):
+            fn()
+        hip.L.hipEventRecord(e0, stream)
+        for _ in range(reps):
+            fn()
+        hip.L.hipEventRecord(e1, stream)
+        torch.cuda.synchronize()
+        out[name] = hip.ms(e0, e1) * 1e3 / reps
+    for e in (e0, e1):
+        hip.L.hipEventDestroy(e)
+    a_s = out["attention_us"] * 1e-6
+    return {"units": mb.U, "plan": "own-gpu", **out,
+            "hbm_frac": att_bytes / a_s / 1e9 / HBM_PEAK_GBPS,
+            "mfma_frac": att_flops / a_s / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+            "note": "layer 0, back-to-back launches on one stream with nothing beside them"}
+
+
 PHASE_NAMES = ("stage_probe", "bucket_count", "bucket_scan", "order_misses", "victims",
                "recency_tail", "tables_plan_slots", "end")
 
@@ -1420,6 +1464,12 @@ def main() -> int:
     }
     if staging is not None:
         result["staging"] = staging
+    if "sparse_decode" in kernels:
+        # the attention of one layer call on a GPU of its own (nothing beside it), with the plan
+        # a call gets without the beside-fetch hint: what the kernel does alone, beside the
+        # in-step figure above (whose plan leaves half the CUs to the other micro-batch's fetch)
+        kernels["sparse_decode"]["alone"] = attention_alone(
+            torch, hs, hip, mbs[0], w, k, args.splits, att_bytes_call, att_flops_call, root_s)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle baseline")
         U_mb = U_all // n_mb
