@@ -190,3 +190,22 @@ def test_phase_timing_build_is_a_separate_library():
     lib.hisparse_debug_resolve_phases.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]
     # argument checks come before any device call
     assert lib.hisparse_debug_resolve_phases(None, 4, None) == hs.HISPARSE_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("units,splits_own,splits_beside", [(16, 8, 4), (32, 4, 2), (8, 16, 8)])
+def test_beside_fetch_plan_takes_half_the_workgroups(units, splits_own, splits_beside):
+    """The beside-fetch hint halves a latent-attention call's split count (so its workgroups and
+    its split partials): the workspace holds [parts][128 heads][512] fp32 partials, 256-byte
+    aligned, then [parts][128] (max, sum) pairs per unit."""
+    w = W.workload(2)
+
+    def parts(flags):
+        d = hs.AttnDesc(w.q_heads, w.d_qk, w.d_v, w.v_offset, w.tokens_per_record, 0, w.scale,
+                        flags)
+        n = hs.hisparse_decode_workspace_bytes(units, w.k, w.record_bytes, d)
+        per_part = units * (w.q_heads * w.d_v * 4 + w.q_heads * 8)
+        assert n > 0 and n % 8 == 0
+        return round(n / per_part)
+
+    assert parts(0) == splits_own
+    assert parts(hs.HISPARSE_ATTN_BESIDE_FETCH) == splits_beside
