@@ -1009,7 +1009,7 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
     // workgroup: twice the tokens per partial result at the same workgroup count, which halves
     // the split partials (fp32, 2 KB per head) and the merge. Measured alone, attention + merge
     // over units of 128 heads (us, best split count): 8 units 27.4 against 28.7, 16 units 34.5
-    // against 45.9 (4 head waves, 16 splits, the previous plan), 32 units 50.8 against 55.5;
+    // against 45.9 (one token group of 4 head waves, 16 splits), 32 units 50.8 against 55.5;
     // below 8 units one token group is faster (2 units 18.7 against 20.7).
     // With HISPARSE_ATTN_BESIDE_FETCH (another stream's host-link fetch shares the GPU) the
     // same shapes take half as many workgroups (below): the other half of the CUs is left to
