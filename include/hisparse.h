@@ -76,7 +76,9 @@ typedef enum {
    * the miss plan back (a stream synchronisation), host threads gather the missed records from
    * the pool into a pinned staging buffer, one copy-engine transfer moves them to the device
    * and a kernel scatters them into their slots. Not capturable, like HISPARSE_FETCH_SDMA; the
-   * cache also holds top_k * R bytes of pinned and of device staging memory per unit. */
+   * cache also holds top_k * R bytes of pinned and of device staging memory per unit, which
+   * its staged fetches share: each one first waits on the host until the previous one, on
+   * whatever stream, has scattered out of them. */
   HISPARSE_FETCH_STAGED = 3
 } hisparse_fetch_t;
 

@@ -76,6 +76,7 @@ void free_all(hisparse_cache* c) {
   if (c->d_layers) (void)hipFree(c->d_layers);
   if (c->h_plan_count) (void)hipHostFree(c->h_plan_count);
   if (c->h_plan) (void)hipHostFree(c->h_plan);
+  if (c->stage_done) (void)hipEventDestroy(c->stage_done);
   if (c->stage_host) (void)hipHostFree(c->stage_host);
   if (c->stage_dev) (void)hipFree(c->stage_dev);
   delete c->gather;
@@ -312,6 +313,11 @@ hisparse_status_t hisparse_cache_create(const hisparse_cache_desc_t* desc, int32
       st = HISPARSE_ERR_OOM;
     } else {
       st = dmalloc(&c->stage_dev, c->stage_bytes);
+    }
+    if (st == HISPARSE_OK &&
+        hipEventCreateWithFlags(&c->stage_done, hipEventDisableTiming) != hipSuccess) {
+      c->stage_done = nullptr;
+      st = HISPARSE_ERR_HIP;
     }
     if (st == HISPARSE_OK) {
       c->gather = new (std::nothrow) hisparse::GatherPool(hisparse::GatherPool::host_threads(16));
@@ -562,8 +568,11 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
     if (hipStreamIsCapturing(stream, &cs) != hipSuccess) return HISPARSE_ERR_HIP;
     if (cs != hipStreamCaptureStatusNone) return HISPARSE_ERR_UNSUPPORTED;
     const size_t U = (size_t)c->units, K = (size_t)c->desc.top_k;
-    // the plan, once the resolve that wrote it has run (and the previous staged copy out of
-    // the staging buffer with it: same stream)
+    // The staging buffers are the handle's: the previous staged fetch, on whatever stream,
+    // must have copied out of the pinned one and scattered out of the device one before this
+    // one refills them (an event never recorded is complete).
+    if (hipEventSynchronize(c->stage_done) != hipSuccess) return HISPARSE_ERR_HIP;
+    // the plan, once the resolve that wrote it has run
     if (hipMemcpyAsync(c->h_plan_count, an.plan_count, U * 4, hipMemcpyDeviceToHost, stream) !=
             hipSuccess ||
         hipMemcpyAsync(c->h_plan, an.plan, U * K * sizeof(int2), hipMemcpyDeviceToHost,
@@ -635,7 +644,9 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
     sa.units = c->units;
     sa.plan_count = an.plan_count;
     sa.part_lo = part_lo;
-    if (hisparse::launch_scatter(sa, stream) != hipSuccess) return HISPARSE_ERR_HIP;
+    if (hisparse::launch_scatter(sa, stream) != hipSuccess ||
+        hipEventRecord(c->stage_done, stream) != hipSuccess)
+      return HISPARSE_ERR_HIP;
     return HISPARSE_OK;
   }
   if (c->desc.fetch == HISPARSE_FETCH_SDMA) {

@@ -182,5 +182,6 @@ struct hisparse_cache {
   uint8_t* stage_host = nullptr;
   uint8_t* stage_dev = nullptr;
   size_t stage_bytes = 0;
+  hipEvent_t stage_done = nullptr;  // recorded after the last staged fetch's scatter
   hisparse::GatherPool* gather = nullptr;
 };

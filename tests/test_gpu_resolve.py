@@ -334,3 +334,36 @@ def test_fetch_parts_equal_fetch(fetch):
         torch.cuda.synchronize()
         a.close()
         b.close()
+
+
+def test_staged_fetches_on_two_streams():
+    """The staged fetch path's buffers belong to the handle: an anchor's demand fetch on one
+    stream and the replay of its plan into the shared layer on another, enqueued back to back
+    with only the resolve ordered before both, each land exactly the planned records (the
+    second call waits on the host for the first one's scatter before refilling the buffers)."""
+    w = W.workload(2, num_requests=4, num_layers=2, share_group=2)
+    steps = 4
+    run = Run(w, steps, fetch=hs.HISPARSE_FETCH_STAGED)
+    orc = oracle.OracleCache(w.units, w.L, w.B, w.k)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    try:
+        for t in range(steps):
+            log(f"staged two streams step {t}")
+            with torch.cuda.stream(s1):
+                hs.hisparse_resolve_tables(run.cache.handle, 0, run.sel_ptr(t, 0), run.slots[0],
+                                           run.counts[0], s1)
+                ev = torch.cuda.Event()
+                ev.record(s1)
+                hs.hisparse_fetch(run.cache.handle, 0, s1)
+            s2.wait_event(ev)
+            hs.hisparse_prefetch_layer(run.cache.handle, 0, 1, s2)
+            torch.cuda.synchronize()
+            orc.resolve(run.sel_host[t, :w.units])
+            for layer in (0, 1):
+                img = layer_cache_host(run, layer)
+                host = run.cache.host_view(layer)
+                for u in range(w.units):
+                    res = np.nonzero(orc.slot_pos[u] >= 0)[0]
+                    assert (img[u, res] == host[u, orc.slot_pos[u, res]]).all(), (t, layer, u)
+    finally:
+        run.close()
