@@ -7,7 +7,7 @@
 #include <mutex>
 #include <new>
 
-#include "internal.h"
+#include "handle.h"
 
 using hisparse::kMaxCapacity;
 using hisparse::kMaxRecordBytes;
