@@ -72,8 +72,8 @@ def parse():
                          "2 requests, else 1)")
     ap.add_argument("--turns", choices=["all", "first"], default="all",
                     help="micro-batches take turns on the host link at every layer, or at the "
-                         "first only (then run free from that offset: 1-2%% faster when "
-                         "undisturbed, but a perturbation such as a profiler attached can push "
+                         "first only (then run free from that offset; on the DSA/MLA workload "
+                         "1.5%% slower, and a perturbation such as a profiler attached can push "
                          "the chains into lockstep for good)")
     ap.add_argument("--attn-plan", choices=["auto", "beside-fetch", "own-gpu"], default="auto",
                     help="latent attention's plan hint: 'beside-fetch' (HISPARSE_ATTN_BESIDE_FETCH: "
