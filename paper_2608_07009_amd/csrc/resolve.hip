@@ -156,6 +156,7 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   }
 #pragma unroll
   for (int u = 0; u < kMaxPer; ++u) sv[u] = (pv[u] >= 0 && (int64_t)pv[u] < L) ? pt[pv[u]] : -1;
+  int pmin = INT32_MAX, pmax = -1;  // this thread's miss positions (phase 2 buckets by them)
 #pragma unroll
   for (int u = 0; u < kMaxPer; ++u) {
     const int i = tid + u * NT;
@@ -172,11 +173,26 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
         } else {
           const int r = atomicAdd(&s_nmiss, 1);
           s_keys[r] = ((uint64_t)(uint32_t)p << 32) | (uint32_t)i;
+          pmin = min(pmin, p);
+          pmax = max(pmax, p);
         }
       }
       s_out[i] = out;
     }
   }
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    pmin = min(pmin, __shfl_xor(pmin, o, kWave));
+    pmax = max(pmax, __shfl_xor(pmax, o, kWave));
+  }
+  if ((tid & (kWave - 1)) == 0 && pmax >= 0) {  // one LDS atomic pair per wave
+    atomicMin(&s_pmin, pmin);
+    atomicMax(&s_pmax, pmax);
+  }
+  // rank buckets cleared here for large workgroups (a few stores per thread beside the probes'
+  // latency), after the miss count for small ones (which then need a barrier of their own)
+  if constexpr (NT >= 256)
+    for (int b = tid; b < kBuckets; b += NT) s_cnt[b] = 0;
   __syncthreads();
   const int m = s_nmiss;
   RESOLVE_STAMP(1);
@@ -184,7 +200,10 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   // do not pay for a scan over all kBuckets; kBuckets beyond
   const int nbb = m <= 32 ? 6 : (m <= 256 ? 33 - __clz(m - 1) : kBucketBits);
   const int nb = 1 << nbb;
-  for (int b = tid; b < nb; b += NT) s_cnt[b] = 0;
+  if constexpr (NT < 256) {
+    for (int b = tid; b < nb; b += NT) s_cnt[b] = 0;
+    __syncthreads();
+  }
 
   // Phase 2: the misses in ascending position order. Bucket them by the high bits of their
   // offset within the misses' own position range (a counting pass), then each miss's rank is
@@ -195,29 +214,12 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   // than sorting, and the keys are sorted instead (bitonic network in LDS).
   uint64_t key[kMaxPer];
   int bkt[kMaxPer], loc[kMaxPer];
-  {
-    int pmin = INT32_MAX, pmax = -1;
 #pragma unroll
-    for (int u = 0; u < kMaxPer; ++u) {
-      const int j = tid + u * NT;
-      key[u] = j < m ? s_keys[j] : 0ull;
-      if (j < m) {
-        pmin = min(pmin, (int)(key[u] >> 32));
-        pmax = max(pmax, (int)(key[u] >> 32));
-      }
-    }
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      pmin = min(pmin, __shfl_xor(pmin, o, kWave));
-      pmax = max(pmax, __shfl_xor(pmax, o, kWave));
-    }
-    if ((tid & (kWave - 1)) == 0 && pmax >= 0) {  // one LDS atomic pair per wave
-      atomicMin(&s_pmin, pmin);
-      atomicMax(&s_pmax, pmax);
-    }
+  for (int u = 0; u < kMaxPer; ++u) {
+    const int j = tid + u * NT;
+    key[u] = j < m ? s_keys[j] : 0ull;
   }
-  __syncthreads();
-  const int pmin = s_pmin;
+  pmin = s_pmin;
   const uint32_t span = s_pmax > pmin ? (uint32_t)(s_pmax - pmin) : 0u;  // < 2^31
   const int lg = span ? 32 - __clz(span) : 0;
   const int shift = lg > nbb ? lg - nbb : 0;
