@@ -80,6 +80,10 @@ def parse():
                          "another micro-batch's host-link fetch runs beside each attention call) "
                          "or 'own-gpu'; auto = beside-fetch when several micro-batches move "
                          "records over the link")
+    ap.add_argument("--carry-hint", action=argparse.BooleanOptionalAction, default=True,
+                    help="attention calls that carry a replay into the next shared layer, and "
+                         "their merges, take the HISPARSE_ATTN_CARRIES_REPLAY plan hint (fewer, "
+                         "longer splits for small calls)")
     ap.add_argument("--fetch-workgroups", type=int, default=0,
                     help="workgroups of one fetch launch (0 = the library default)")
     ap.add_argument("--schedule", choices=["overlap", "serial", "side", "batched"],
@@ -640,9 +644,11 @@ class DecodeSchedule:
 
     def __init__(self, *, w, k, groups, mbs, n_mb, n_qv, ad_ref, lib, rec, wait, root_s, fork_ev,
                  join_evs, schedule, turns, speculate, append, share, status_string,
-                 handover=0):
+                 handover=0, ad_carry=None):
         self.w, self.k, self.groups, self.mbs, self.n_mb, self.n_qv = w, k, groups, mbs, n_mb, n_qv
         self.ad_ref, self.L, self.rec, self.wait, self.root_s = ad_ref, lib, rec, wait, root_s
+        # the descriptor of attention calls that carry a replay, and of their merges
+        self.ad_carry = ad_ref if ad_carry is None else ad_carry
         self.fork_ev, self.join_evs = fork_ev, join_evs
         self.schedule, self.turns, self.speculate, self.append = schedule, turns, speculate, append
         self.share, self.status_string = share, status_string
@@ -677,9 +683,10 @@ class DecodeSchedule:
         call("resolve_tables", ms, ev, spans, L.hisparse_resolve_tables, h, a, sp, mb.slot_p[a],
              cp, ms)
 
-        def merge(units, out_p):
+        def merge(units, out_p, ad=None):
             call("attention_merge", ms, ev, spans, L.hisparse_attention_merge, units, k,
-                 w.record_bytes, self.ad_ref, out_p, mb.ws_ptr, mb.ws_bytes, ms)
+                 w.record_bytes, self.ad_ref if ad is None else ad, out_p, mb.ws_ptr,
+                 mb.ws_bytes, ms)
 
         def decode(l):
             call("sparse_decode", ms, ev, spans, L.hisparse_sparse_decode, h, l, qv[l],
@@ -757,14 +764,14 @@ class DecodeSchedule:
                 lo = share if (share and i >= 1) else 0  # begun by the previous merge
                 call("sparse_decode_prefetch", ms, ev, spans,
                      L.hisparse_sparse_decode_prefetch_part, h, l, qv[l], mb.slot_p[a],
-                     mb.out_p[l], self.ad_ref, mb.ws_ptr, mb.ws_bytes, a, layers[i + 1], 1, lo,
+                     mb.out_p[l], self.ad_carry, mb.ws_ptr, mb.ws_bytes, a, layers[i + 1], 1, lo,
                      256, ms)
                 if share and i + 2 < len(layers):
                     call("attention_merge_prefetch", ms, ev, spans,
-                         L.hisparse_attention_merge_prefetch, h, self.ad_ref, mb.out_p[l],
+                         L.hisparse_attention_merge_prefetch, h, self.ad_carry, mb.out_p[l],
                          mb.ws_ptr, mb.ws_bytes, a, layers[i + 2], 1, 0, share, ms)
                 else:
-                    merge(mb.U, mb.out_p[l])
+                    merge(mb.U, mb.out_p[l], self.ad_carry)
             decode(layers[-1])
 
     def step(self, t, ev=None, spans=None, sel_override=None, q_override=None, fork=True,
@@ -916,6 +923,11 @@ def main() -> int:
                      w.scale, hs.HISPARSE_ATTN_DEFER_MERGE |
                      (hs.HISPARSE_ATTN_BESIDE_FETCH if beside else 0))
     ad_ref = ctypes.byref(ad)
+    # the attention calls that carry a replay (overlap schedule) and their merges take the
+    # carries-replay plan hint
+    ad_c = hs.AttnDesc(w.q_heads, w.d_qk, w.d_v, w.v_offset, w.tokens_per_record, args.splits,
+                       w.scale, ad.flags | hs.HISPARSE_ATTN_CARRIES_REPLAY)
+    ad_carry = ctypes.byref(ad_c)
     groups = [(a, list(range(a + 1, min(a + G, w.num_layers)))) for a in w.anchors]
 
     class MicroBatch:
@@ -948,8 +960,8 @@ def main() -> int:
             self.slots = torch.empty((w.num_layers, U, k), dtype=torch.int32, device=dev)
             self.counts = torch.zeros((steps_needed, w.num_layers, U, 2), dtype=torch.int32,
                                       device=dev)
-            self.ws_bytes = max(hs.hisparse_decode_workspace_bytes(m * U, k, w.record_bytes, ad)
-                                for m in range(1, G + 1))
+            self.ws_bytes = max(hs.hisparse_decode_workspace_bytes(m * U, k, w.record_bytes, d)
+                                for m in range(1, G + 1) for d in (ad, ad_c))
             self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
             self.ws_ptr = self.ws.data_ptr()
             sl = slice(self.u0, self.u0 + U)
@@ -999,7 +1011,8 @@ def main() -> int:
                            join_evs=join_evs, schedule=args.schedule, turns=args.turns,
                            speculate=args.speculate, append=args.append, share=share,
                            status_string=hs.hisparse_status_string,
-                           handover=max(0, min(256, args.handover_share)))
+                           handover=max(0, min(256, args.handover_share)),
+                           ad_carry=ad_carry if args.carry_hint else None)
     step = sched.step
 
     # pinned H2D sweep over the same pool (hipMemcpyAsync), before the timed region

@@ -135,7 +135,8 @@ typedef struct {
   int32_t num_splits;            /* partitions of the token sequence reduced in a fixed order;
                                     0 = chosen from the shape alone */
   float scale;                   /* softmax scale applied to q.k */
-  int32_t flags;                 /* 0 or HISPARSE_ATTN_DEFER_MERGE | HISPARSE_ATTN_BESIDE_FETCH */
+  int32_t flags;                 /* 0 or HISPARSE_ATTN_DEFER_MERGE | HISPARSE_ATTN_BESIDE_FETCH |
+                                    HISPARSE_ATTN_CARRIES_REPLAY */
 } hisparse_attn_desc_t;
 
 /* hisparse_attn_desc_t.flags: the attention call runs only its per-split workgroups (and any
@@ -151,6 +152,16 @@ typedef struct {
  * slower that way. Results differ only within rounding (other split boundaries); each plan is
  * deterministic. */
 #define HISPARSE_ATTN_BESIDE_FETCH 2
+/* hisparse_attn_desc_t.flags, a scheduling hint for latent attention: the call carries an
+ * exact-prefetch replay (hisparse_sparse_decode_prefetch, _part) whose host-link transfer takes
+ * longer than the attention itself, so the launch lasts as long as the replay and the merge that
+ * follows it sits on the decode chain (Section 3.5). With one token group per workgroup (few
+ * workgroup columns, e.g. one request of 128 heads) the plan then takes splits of at least 4
+ * chunks instead of 2: half the attention workgroups, which stay hidden behind the replay and
+ * leave it more CUs, and half the split partials for the merge to read. Set it on the carrying
+ * call and on its hisparse_attention_merge (or _merge_prefetch). Results differ only within
+ * rounding (other split boundaries); each plan is deterministic. */
+#define HISPARSE_ATTN_CARRIES_REPLAY 4
 
 /* Human-readable name of a status code (static storage). */
 const char* hisparse_status_string(hisparse_status_t status);

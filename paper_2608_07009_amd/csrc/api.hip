@@ -189,7 +189,8 @@ hisparse_status_t hisparse_validate_desc(const hisparse_cache_desc_t* d) {
 hisparse_status_t hisparse_validate_attn(int32_t record_bytes, int32_t top_k,
                                          const hisparse_attn_desc_t* a) {
   if (!a) return HISPARSE_ERR_INVALID_ARG;
-  if ((a->flags & ~(HISPARSE_ATTN_DEFER_MERGE | HISPARSE_ATTN_BESIDE_FETCH)) != 0 ||
+  if ((a->flags & ~(HISPARSE_ATTN_DEFER_MERGE | HISPARSE_ATTN_BESIDE_FETCH |
+                    HISPARSE_ATTN_CARRIES_REPLAY)) != 0 ||
       a->q_heads < 1 || a->q_heads > 256 ||
       a->num_splits < 0)
     return HISPARSE_ERR_INVALID_ARG;

@@ -1054,6 +1054,14 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
     splits = std::max(1, target / per_split);
     int chunks_per_split = 4;
     if (is_mla(*attn)) chunks_per_split = per_split <= 4 ? 2 : (per_split <= 16 ? 4 : 8);
+    // A call that carries a replay lasts as long as the replay's host reads; its attention only
+    // has to finish within them, and the merge after it is on the decode chain. One request of
+    // 128 heads with a replay of its 2048 selections into the next shared layer: 16 four-chunk
+    // splits instead of 32 two-chunk ones take the launch from 28.0 to 27.4 us and its merge
+    // from 5.8 to 4.6 us (one 1M-token request, 56 layers in groups of 4: decode step 2.299 ->
+    // 2.226 ms), although that attention alone takes 17.7 against 12.5 us.
+    if (is_mla(*attn) && (attn->flags & HISPARSE_ATTN_CARRIES_REPLAY))
+      chunks_per_split = std::max(chunks_per_split, 4);
     // a call too small to give even 64 such workgroups is all latency: one chunk per split
     if (is_mla(*attn) && (int64_t)per_split * (p.n_tok / (2 * chunk)) < 64) chunks_per_split = 1;
     // two token groups: one workgroup per CU, however few chunks each group gets

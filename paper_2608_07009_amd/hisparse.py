@@ -31,6 +31,7 @@ HISPARSE_FETCH_STAGED = 3
 
 HISPARSE_ATTN_DEFER_MERGE = 1
 HISPARSE_ATTN_BESIDE_FETCH = 2
+HISPARSE_ATTN_CARRIES_REPLAY = 4
 HISPARSE_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 HISPARSE_RESOLVE_PHASE_SLOTS = 16

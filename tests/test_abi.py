@@ -74,7 +74,7 @@ def test_invalid_descriptors(field, value, status):
     (dict(q_heads=0), hs.HISPARSE_ERR_INVALID_ARG),
     (dict(scale=0.0), hs.HISPARSE_ERR_INVALID_ARG),
     (dict(num_splits=-1), hs.HISPARSE_ERR_INVALID_ARG),
-    (dict(flags=4), hs.HISPARSE_ERR_INVALID_ARG),          # an undefined flag bit
+    (dict(flags=8), hs.HISPARSE_ERR_INVALID_ARG),          # an undefined flag bit
 ])
 def test_invalid_attention_descriptors(change, status):
     w = W.workload(2)
@@ -209,3 +209,24 @@ def test_beside_fetch_plan_takes_half_the_workgroups(units, splits_own, splits_b
 
     assert parts(0) == splits_own
     assert parts(hs.HISPARSE_ATTN_BESIDE_FETCH) == splits_beside
+
+
+@pytest.mark.parametrize("units,splits_plain,splits_carry", [(1, 32, 16), (2, 32, 16), (4, 16, 16),
+                                                            (16, 8, 8)])
+def test_carries_replay_plan_takes_longer_splits(units, splits_plain, splits_carry):
+    """The carries-replay hint gives latent attention with one token group per workgroup (fewer
+    than 16 workgroup columns) splits of at least 4 chunks of 32 tokens: for one or two units of
+    128 heads at k = 2048 half the splits (and split partials); from 4 units on the plan already
+    takes 4-chunk splits, and with two token groups (16 units) the hint changes nothing."""
+    w = W.workload(2)
+
+    def parts(flags):
+        d = hs.AttnDesc(w.q_heads, w.d_qk, w.d_v, w.v_offset, w.tokens_per_record, 0, w.scale,
+                        flags)
+        n = hs.hisparse_decode_workspace_bytes(units, w.k, w.record_bytes, d)
+        per_part = units * (w.q_heads * w.d_v * 4 + w.q_heads * 8)
+        return round(n / per_part)
+
+    assert parts(0) == splits_plain
+    assert parts(hs.HISPARSE_ATTN_CARRIES_REPLAY) == splits_carry
+    assert parts(hs.HISPARSE_ATTN_CARRIES_REPLAY | hs.HISPARSE_ATTN_DEFER_MERGE) == splits_carry

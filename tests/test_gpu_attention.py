@@ -57,13 +57,14 @@ STEPS = {1: 12, 2: 3, 3: 6, 4: 4, 5: 3}
 
 
 BESIDE = hs.HISPARSE_ATTN_BESIDE_FETCH
+CARRY = hs.HISPARSE_ATTN_CARRIES_REPLAY
 
 
 @pytest.mark.parametrize("cfg,flags", [(1, 0), (2, 0), (2, BESIDE), (3, 0), (4, 0), (5, 0),
-                                       (5, BESIDE)])
+                                       (5, BESIDE), (5, CARRY)])
 def test_attention_cache_vs_resident_vs_oracle(cfg, flags):
-    """Both latent-attention plans (two token groups per workgroup by default; one token group
-    with deeper load pipelines under HISPARSE_ATTN_BESIDE_FETCH)."""
+    """Every latent-attention plan: the default, the beside-fetch hint's (half the workgroups,
+    longer splits) and, for one request, the carries-replay hint's (4-chunk splits)."""
     steps = STEPS[cfg]
     w = W.fit_pinned(W.workload(cfg))
     layer = w.anchors[-1]

@@ -406,3 +406,54 @@ def test_merge_carried_replay_equals_separate(cfg, fetch, share):
         torch.cuda.synchronize()
         split.close()
         apart.close()
+
+
+@pytest.mark.parametrize("requests", [1, 2])
+def test_carries_replay_hint_equals_separate(requests):
+    """The overlap schedule with HISPARSE_ATTN_CARRIES_REPLAY on the replay-carrying attention
+    calls and on their merges, the last layer's attention without it (one or two requests of 128
+    latent heads, k = 2048: one token group per workgroup, where the hint halves the splits):
+    outputs bit-identical to the same plans' attention issued apart from the replay, caches
+    byte-identical."""
+    G = 4
+    w = W.workload(2, num_layers=G, share_group=G, num_requests=requests)
+    steps = 2
+    log(f"test_carries_replay_hint_equals_separate {w.name} units={w.units}")
+    split, apart = Run(w, steps), Run(w, steps)
+    dev = split.dev
+    ad = attn_desc(w)
+    adc = attn_desc(w, 0, hs.HISPARSE_ATTN_CARRIES_REPLAY)
+    adcf = attn_desc(w, 0, hs.HISPARSE_ATTN_CARRIES_REPLAY | hs.HISPARSE_ATTN_DEFER_MERGE)
+    nb = hs.hisparse_decode_workspace_bytes(w.units, w.k, w.record_bytes, ad)
+    nbc = hs.hisparse_decode_workspace_bytes(w.units, w.k, w.record_bytes, adc)
+    assert 0 < nbc < nb  # fewer split partials
+    ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+    out_s = torch.empty((G, w.units, w.q_heads, w.d_v), dtype=torch.float32, device=dev)
+    out_a = torch.empty_like(out_s)
+    try:
+        for t in range(steps):
+            q = [torch.from_numpy(W.queries(w, t, l).view(np.int16)).to(dev) for l in range(G)]
+            for r in (split, apart):
+                hs.hisparse_resolve(r.cache.handle, 0, r.sel_ptr(t, 0), r.slots[0], r.counts[0],
+                                    r.stream)
+            h, st = split.cache.handle, split.stream
+            for l in range(G - 1):
+                hs.hisparse_sparse_decode_prefetch(h, l, q[l], split.slots[0], out_s[l], adcf, ws,
+                                                   nbc, 0, l + 1, 1, st)
+                hs.hisparse_attention_merge(w.units, w.k, w.record_bytes, adcf, out_s[l], ws, nbc,
+                                            st)
+            hs.hisparse_sparse_decode(h, G - 1, q[G - 1], split.slots[0], out_s[G - 1], ad, ws, nb,
+                                      st)
+            hs.hisparse_prefetch_layers(apart.cache.handle, 0, 1, G - 1, apart.stream)
+            for l in range(G):
+                hs.hisparse_sparse_decode(apart.cache.handle, l, q[l], apart.slots[0], out_a[l],
+                                          adc if l < G - 1 else ad, ws, nb, apart.stream)
+            torch.cuda.synchronize()
+            assert torch.equal(out_s, out_a), f"step {t}"
+            for l in range(G):
+                assert (layer_cache_host(split, l) == layer_cache_host(apart, l)).all(), \
+                    f"step {t} layer {l}"
+    finally:
+        torch.cuda.synchronize()
+        split.close()
+        apart.close()
