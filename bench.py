@@ -102,6 +102,10 @@ def parse():
                          "attention carries the rest; 0 = merges carry nothing (measured "
                          "faster: each launch that carries part of a replay pays the host "
                          "reads' ramp again)")
+    ap.add_argument("--link-stream", action="store_true",
+                    help="micro-batches taking turns on the host link: every transfer on one "
+                         "shared stream, in turn order, instead of each micro-batch's own stream "
+                         "waiting for the previous transfer's event")
     ap.add_argument("--handover-share", type=int, default=0, metavar="S",
                     help="micro-batches taking turns on the link: each fetch is issued as two "
                          "launches (hisparse_fetch_part), the first S/256 of each unit's plan and "
@@ -644,7 +648,7 @@ class DecodeSchedule:
 
     def __init__(self, *, w, k, groups, mbs, n_mb, n_qv, ad_ref, lib, rec, wait, root_s, fork_ev,
                  join_evs, schedule, turns, speculate, append, share, status_string,
-                 handover=0, ad_carry=None):
+                 handover=0, ad_carry=None, link_s=None, link_join=None):
         self.w, self.k, self.groups, self.mbs, self.n_mb, self.n_qv = w, k, groups, mbs, n_mb, n_qv
         self.ad_ref, self.L, self.rec, self.wait, self.root_s = ad_ref, lib, rec, wait, root_s
         # the descriptor of attention calls that carry a replay, and of their merges
@@ -653,6 +657,12 @@ class DecodeSchedule:
         self.schedule, self.turns, self.speculate, self.append = schedule, turns, speculate, append
         self.share, self.status_string = share, status_string
         self.handover = handover  # 256ths of a fetch after which the link turn passes on
+        # one stream for every micro-batch's host-link transfers (turns taken by queue order),
+        # with the event recorded after it to join back into the root stream
+        self.link_s, self.link_join = link_s, link_join
+        if link_s is not None and (n_mb < 2 or turns != "all" or handover or link_join is None):
+            raise ValueError("a shared link stream takes turns at every layer, without a "
+                             "hand-over share, between two or more micro-batches")
 
     def events_per_step(self) -> int:
         """Timing events one step may consume (two per library call)."""
@@ -694,6 +704,16 @@ class DecodeSchedule:
             merge(mb.U, mb.out_p[l])
 
         def transfer(name, fn, *fargs):
+            ls = self.link_s
+            if ls is not None:
+                # on the shared link stream (its queue order is the turn order): it waits for
+                # this micro-batch's resolve, and the attention waits for it
+                rec(mb.rdone[gi], ms)
+                wait(ls, mb.rdone[gi], 0)
+                call(name, ls, ev, spans, fn, *fargs[:-1], ls)
+                rec(mb.link[gi], ls)
+                wait(ms, mb.link[gi], 0)
+                return
             if link and link[0] is not None:
                 wait(ms, link[0], 0)
             call(name, ms, ev, spans, fn, *fargs)
@@ -788,6 +808,8 @@ class DecodeSchedule:
             rec(self.fork_ev, self.root_s)
             for mb in mbs[1:]:
                 wait(mb.main, self.fork_ev, 0)
+            if self.link_s is not None:
+                wait(self.link_s, self.fork_ev, 0)
         for gi in range(len(self.groups)):
             for i, mb in enumerate(mbs):
                 link = None
@@ -809,6 +831,9 @@ class DecodeSchedule:
             for mb, je in zip(mbs[1:], self.join_evs[1:]):
                 rec(je, mb.main)
                 wait(self.root_s, je, 0)
+            if self.link_s is not None:
+                rec(self.link_join, self.link_s)
+                wait(self.root_s, self.link_join, 0)
 
 
 def main() -> int:
@@ -999,6 +1024,16 @@ def main() -> int:
     cache = mbs[0].cache
     fork_ev = hip.event(timing=False)
     join_evs = [hip.event(timing=False) for _ in mbs]
+    link_s = link_join = None
+    if args.link_stream:
+        if n_mb < 2 or args.turns != "all" or args.handover_share:
+            print(json.dumps({"error": "--link-stream needs two or more micro-batches taking "
+                              "turns at every layer, without --handover-share"}))
+            return 2
+        link_t = torch.cuda.Stream()
+        link_s, link_join = link_t.cuda_stream, hip.event(timing=False)
+        for mb in mbs:  # resolve done, per group: the link stream's transfer waits for it
+            mb.rdone = [hip.event(timing=False) for _ in groups]
     log(f"{w.name}: layers {w.num_layers} (of {w0.num_layers}), host pool "
         f"{w.host_pool_bytes() / 2**30:.1f} GiB, {n_mb} micro-batch(es), schedule "
         f"{args.schedule}, set up in {time.time() - t0:.1f}s")
@@ -1012,7 +1047,8 @@ def main() -> int:
                            speculate=args.speculate, append=args.append, share=share,
                            status_string=hs.hisparse_status_string,
                            handover=max(0, min(256, args.handover_share)),
-                           ad_carry=ad_carry if args.carry_hint else None)
+                           ad_carry=ad_carry if args.carry_hint else None,
+                           link_s=link_s, link_join=link_join)
     step = sched.step
 
     # pinned H2D sweep over the same pool (hipMemcpyAsync), before the timed region
@@ -1448,6 +1484,7 @@ def main() -> int:
                    "host_memory": args.host_memory, "mode": mode,
                    "merge_replay_share": share if args.schedule == "overlap" else None,
                    "handover_share": args.handover_share if n_mb > 1 else None,
+                   "link_stream": bool(link_s),
                    "attn_plan": "beside-fetch" if beside else "own-gpu",
                    "steps_per_graph": graph["steps_per_graph"] if graph else None},
         "decode_tokens_per_s": w.num_requests * K / wall,

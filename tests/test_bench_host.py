@@ -5,6 +5,7 @@ process per workload."""
 import os
 
 import numpy as np
+import pytest
 
 import bench
 
@@ -154,8 +155,11 @@ class _FakeLib:
         return call
 
 
+LINK_S = 55  # the shared link stream of the link-stream cases
+
+
 def _schedule(hip, *, layers, G, n_mb, schedule, speculate, append, turns, share, steps,
-              handover=0):
+              handover=0, link=False):
     from types import SimpleNamespace
     w = SimpleNamespace(num_layers=layers, record_bytes=1152)
     groups = [(a, list(range(a + 1, min(a + G, layers)))) for a in range(0, layers, G)]
@@ -173,12 +177,13 @@ def _schedule(hip, *, layers, G, n_mb, schedule, speculate, append, turns, share
             slot_p=[base + 200 + l for l in range(layers)],
             out_p=[base + 300 + l for l in range(layers)], ws_ptr=base + 400, ws_bytes=1 << 20,
             adm_ptr=base + 500, sync=[hip.event(), hip.event()],
-            link=[hip.event() for _ in groups]))
+            link=[hip.event() for _ in groups], rdone=[hip.event() for _ in groups]))
     return bench.DecodeSchedule(
         w=w, k=2048, groups=groups, mbs=mbs, n_mb=n_mb, n_qv=2, ad_ref=None,
         lib=_FakeLib(hip.log), rec=hip.rec, wait=hip.wait, root_s=1, fork_ev=hip.event(),
         join_evs=[hip.event() for _ in mbs], schedule=schedule, turns=turns,
-        speculate=speculate, append=append, share=share, status_string=str, handover=handover)
+        speculate=speculate, append=append, share=share, status_string=str, handover=handover,
+        link_s=LINK_S if link else None, link_join=hip.event() if link else None)
 
 
 TRANSFERS = ("hisparse_fetch", "hisparse_fetch_group", "hisparse_fetch_part")
@@ -249,3 +254,72 @@ def test_decode_schedule_events_and_turns():
                 if case.get("handover"):  # the rest of the fetch after the turn passed on
                     assert log[i][1] == "hisparse_fetch_part", case
                     assert log[i + 2] == ("call", "hisparse_fetch_part", mbs[m].main), case
+
+
+def test_decode_schedule_link_stream():
+    """The shared link stream: every micro-batch's transfer goes to one stream in the order of
+    groups and micro-batches, waits there for its own micro-batch's resolve (an event recorded
+    on that micro-batch's stream right after the resolve), and is followed by the record of its
+    link event, which the micro-batch's stream waits for before its attention. The link stream
+    forks from the root stream with the micro-batches and joins back into it; no wait names a
+    destroyed or never-recorded event, over single steps and over steps captured several to a
+    graph (fork at the first, join at the last). Options it cannot combine with are refused."""
+    cases = [dict(layers=8, G=1, n_mb=2, schedule="overlap", speculate=False, append=False),
+             dict(layers=8, G=1, n_mb=3, schedule="overlap", speculate=False, append=True),
+             dict(layers=6, G=1, n_mb=2, schedule="overlap", speculate=True, append=False),
+             dict(layers=8, G=4, n_mb=2, schedule="serial", speculate=False, append=False),
+             dict(layers=8, G=4, n_mb=2, schedule="overlap", speculate=False, append=False)]
+    steps = 8
+    for case in cases:
+        hip = _FakeHip()
+        sched = _schedule(hip, steps=steps, turns="all", share=0, link=True, **case)
+        budget = sched.events_per_step()
+        timing = set()
+        sched.step(0)
+        sched.step(1)
+        for t0 in (2, 5):  # a graph of 3 steps, twice: fork at the first, join at the last
+            for j in range(3):
+                ev = [hip.event() for _ in range(budget)]
+                timing.update(ev)
+                spans = []
+                sched.step(t0 + j, ev, spans, fork=(j == 0), join=(j == 2))
+                used = [e for _, e0, e1 in spans for e in (e0, e1)]
+                assert len(used) == len(set(used)) <= budget, case
+                for e in ev:
+                    hip.destroy(e)
+        mbs, n_mb = sched.mbs, case["n_mb"]
+        log = [x for x in hip.log if not (x[0] == "rec" and x[1] in timing)]
+        calls = [i for i, x in enumerate(log) if x[0] == "call" and x[1] in TRANSFERS]
+        per_step = len(sched.groups) * n_mb
+        assert len(calls) == steps * per_step, case
+        for j, i in enumerate(calls):
+            g, m = divmod(j % per_step, n_mb)
+            mb = mbs[m]
+            assert log[i][2] == LINK_S, case
+            assert log[i - 2:i] == [("rec", mb.rdone[g], mb.main), ("wait", LINK_S, mb.rdone[g])]
+            assert log[i + 1:i + 3] == [("rec", mb.link[g], LINK_S), ("wait", mb.main, mb.link[g])]
+            # the resolve of that group precedes it on the micro-batch's stream
+            prev = [x for x in log[:i - 2] if x[0] == "call" and x[2] == mb.main]
+            assert prev[-1][1] == "hisparse_resolve_tables", case
+        # no attention before its transfer: every attention call of a micro-batch follows the
+        # wait for its latest link event on that stream
+        for mb in mbs:
+            waited = False
+            for x in log:
+                if x[0] == "rec" and x[1] in mb.rdone:  # a new transfer is on its way
+                    waited = False
+                if x[0] == "wait" and x[1] == mb.main and x[2] in mb.link:
+                    waited = True
+                if x[0] == "call" and x[2] == mb.main and "decode" in x[1]:
+                    assert waited, case
+        forks = [x for x in log if x == ("wait", LINK_S, sched.fork_ev)]
+        joins = [i for i, x in enumerate(log) if x == ("rec", sched.link_join, LINK_S)]
+        assert len(forks) == 2 + 2 and len(joins) == 2 + 2, case
+        for i in joins:
+            assert log[i + 1] == ("wait", 1, sched.link_join), case
+    hip = _FakeHip()
+    for bad in (dict(n_mb=1, turns="all", handover=0), dict(n_mb=2, turns="first", handover=0),
+                dict(n_mb=2, turns="all", handover=64)):
+        with pytest.raises(ValueError):
+            _schedule(hip, layers=4, G=1, schedule="overlap", speculate=False, append=False,
+                      share=0, steps=2, link=True, **bad)
