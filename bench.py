@@ -105,7 +105,7 @@ def parse():
     ap.add_argument("--link-stream", action="store_true",
                     help="micro-batches taking turns on the host link: every transfer on one "
                          "shared stream, in turn order, instead of each micro-batch's own stream "
-                         "waiting for the previous transfer's event")
+                         "waiting for the previous transfer's event (switched off: refused)")
     ap.add_argument("--handover-share", type=int, default=0, metavar="S",
                     help="micro-batches taking turns on the link: each fetch is issued as two "
                          "launches (hisparse_fetch_part), the first S/256 of each unit's plan and "
@@ -1026,14 +1026,13 @@ def main() -> int:
     join_evs = [hip.event(timing=False) for _ in mbs]
     link_s = link_join = None
     if args.link_stream:
-        if n_mb < 2 or args.turns != "all" or args.handover_share:
-            print(json.dumps({"error": "--link-stream needs two or more micro-batches taking "
-                              "turns at every layer, without --handover-share"}))
-            return 2
-        link_t = torch.cuda.Stream()
-        link_s, link_join = link_t.cuda_stream, hip.event(timing=False)
-        for mb in mbs:  # resolve done, per group: the link stream's transfer waits for it
-            mb.rdone = [hip.event(timing=False) for _ in groups]
+        # The schedule's shared-link-stream mode (DecodeSchedule, link_s) passes the CPU test of
+        # its event order and lifetimes, but its run on the DSA/MLA workload ended in a
+        # segmentation fault of this process after the eager warm-up steps, with no GPU fault;
+        # no cause has been found, so it is not run.
+        print(json.dumps({"error": "--link-stream is switched off: its run ended in a "
+                          "segmentation fault of the host process whose cause is not known"}))
+        return 2
     log(f"{w.name}: layers {w.num_layers} (of {w0.num_layers}), host pool "
         f"{w.host_pool_bytes() / 2**30:.1f} GiB, {n_mb} micro-batch(es), schedule "
         f"{args.schedule}, set up in {time.time() - t0:.1f}s")
