@@ -116,6 +116,45 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 typedef __attribute__((address_space(3))) void lds_void;
 
+// LDS reads that the compiler does not see as memory accesses. In the latent-attention loop the
+// next chunk's direct-to-LDS loads are in flight while the current chunk is read from another
+// buffer; before a compiler-visible LDS read the compiler would wait for those loads (it cannot
+// tell the buffers apart), which takes the load of chunk it+1 out from under the compute of
+// chunk it. The caller waits for these reads itself, with s_waitcnt lgkmcnt(N), N = the number
+// of its own reads issued after the one it needs: LDS reads complete in order, so any other
+// LGKM operation in flight can only lengthen that wait.
+__device__ inline uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const lds_void*)p;
+}
+__device__ inline u32x4 lds_read_b128(uint32_t addr) {
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
+  return v;
+}
+__device__ inline v4i16 lds_read_tr16_b64(uint32_t addr) {
+  v4i16 v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(addr));
+  return v;
+}
+// Wait until at most N LGKM operations are outstanding; a and b are the registers of the reads
+// waited for (tied, so that their users stay after the wait).
+template <int N>
+__device__ __forceinline__ void lgkm_wait2(v4i16& a, v4i16& b) {
+  asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(a), "+v"(b) : "n"(N));
+}
+// S^T += K . Q^T for one k-step once the K rows' read (with at most N later LDS reads) is in;
+// the first step of a chain (FIRST) starts from zero. The s_nop covers the wait states after a
+// just-written operand that the compiler does not see through the assembly.
+template <int N, bool FIRST>
+__device__ __forceinline__ void mfma_qk(f32x16& acc, const u32x4& k, const bf16x8_t& q) {
+  if constexpr (FIRST)
+    asm volatile("s_waitcnt lgkmcnt(%3)\n\ts_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0"
+                 : "=&v"(acc) : "v"(k), "v"(q), "n"(N));
+  else
+    asm volatile("s_waitcnt lgkmcnt(%3)\n\ts_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0"
+                 : "+v"(acc) : "v"(k), "v"(q), "n"(N));
+}
+
 // Wait until at most N direct-to-LDS loads of this wave are outstanding and its LDS writes are
 // done, then synchronise the workgroup. (A workgroup fence would also drain the younger
 // prefetches, which is exactly what the pipeline must not do.)
@@ -506,7 +545,7 @@ __device__ __forceinline__ void mla_split_exact(const AttnArgs& a, const int32_t
 //                                                   output tiles, V by LDS transpose reads
 // A lane holds 16 of a head's 32 scores (the other 16 are in lane ^ 32), which are exactly its
 // P operands of the two PV k-steps; O (16 tiles x 16 fp32 per lane) lives in accumulators.
-template <int HW, int TG, int NST>
+template <int HW, int TG, int NST, bool PACED>
 __global__ __launch_bounds__(64 * HW * TG, 1)
 void attn_mla_kernel(AttnArgs a) {
   constexpr int DQK = 576, DV = 512;
@@ -561,6 +600,22 @@ void attn_mla_kernel(AttnArgs a) {
 
   if (tid == 0) s_fallback = 0;
   __syncthreads();  // s_idx is ready
+  const int head0 = hb * 32 * HW + hg * 32;  // first head of this wave
+  const int head = head0 + col;
+  const bool head_ok = head < a.H;
+  // Q^T operand: Q[head][16kk + 8 half .. +7], loaded unconditionally (a head past H reads head
+  // 0's row: its scores are never stored and, equal to head 0's, change no split-level
+  // decision). Unpaced, its loads go out first: they are in flight while the validity masks
+  // are written and the first chunks issued. Paced, they follow the first chunks' arrival
+  // (below), which spreads the workgroups' start-up traffic.
+  bf16x8_t qreg[NKK];
+  const uint16_t* qrow = a.q + ((int64_t)unit * a.H + (head_ok ? head : 0)) * DQK + 8 * half;
+  auto load_q = [&]() {
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk)
+      qreg[kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(qrow + kk * 16));
+  };
+  if constexpr (!PACED) load_q();
   // iteration `it` of token group g covers the split's chunk it * TG + g
   const int n_it = (tok_end - tok_begin + kChunk * TG - 1) / (kChunk * TG);
   // every chunk the groups iterate over gets its word, including a last one wholly past the
@@ -584,9 +639,6 @@ void attn_mla_kernel(AttnArgs a) {
     stage_chunk<P, PP, LPW_MAX>(s_tiles + buf * TILE, s_idx, pool_u, chunk_base(it), tok_end,
                                 rec_begin, a.tpr_shift, a.R, a.token_bytes, j0, n_loads);
   };
-  const int head0 = hb * 32 * HW + hg * 32;  // first head of this wave
-  const int head = head0 + col;
-  const bool head_ok = head < a.H;
   f32x16 o[NDV];
 #pragma unroll
   for (int n = 0; n < NDV; ++n) o[n] = f32x16{};
@@ -610,22 +662,28 @@ void attn_mla_kernel(AttnArgs a) {
     // V operand by transpose reads: in each 16-lane group lane 4s+q addresses row
     // 16kb + 4s + half (+2 for the second read), columns 32n + 16 (col >> 4) + 4q .. +3; lane
     // t of the group then holds V[those rows][32n + 16 (col >> 4) + t], the k order of P.
-    const uint16_t* v0 = tile + (4 * ((lane & 15) >> 2) + half) * PP * 8 + 16 * (col >> 4) +
-                         4 * (lane & 3);
+    const uint32_t v0 = lds_addr(tile + (4 * ((lane & 15) >> 2) + half) * PP * 8 +
+                                 16 * (col >> 4) + 4 * (lane & 3));
     // MFMA i = (k-step kb, tile n) = (i / NDV, i % NDV), so consecutive MFMAs update
     // different tiles; its two reads run VD MFMAs ahead
     constexpr int VD = 3;
     constexpr int NM = 2 * NDV;
+    static_assert(VD == 3 && NM > VD, "the waits below count a ring of 3 read pairs");
     v4i16 vlo[VD], vhi[VD];
     auto vread = [&](int i, int slot) {
-      const uint16_t* vp = v0 + (i / NDV) * 16 * PP * 8 + 32 * (i % NDV);
-      vlo[slot] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)vp);
-      vhi[slot] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vp + 2 * PP * 8));
+      const uint32_t vp = v0 + 2 * ((i / NDV) * 16 * PP * 8 + 32 * (i % NDV));
+      vlo[slot] = lds_read_tr16_b64(vp);
+      vhi[slot] = lds_read_tr16_b64(vp + 2 * (2 * PP * 8));
     };
 #pragma unroll
     for (int i = 0; i < VD; ++i) vread(i, i);
 #pragma unroll
     for (int i = 0; i < NM; ++i) {
+      // the reads issued after index i's pair: those of indices i+1 .. min(i+VD-1, NM-1)
+      const int later = NM - 1 - i < VD - 1 ? NM - 1 - i : VD - 1;
+      if (later == 2) lgkm_wait2<4>(vlo[i % VD], vhi[i % VD]);
+      else if (later == 1) lgkm_wait2<2>(vlo[i % VD], vhi[i % VD]);
+      else lgkm_wait2<0>(vlo[i % VD], vhi[i % VD]);
       const bf16x8_t vb = __builtin_bit_cast(
           bf16x8_t, __builtin_shufflevector(vlo[i % VD], vhi[i % VD], 0, 1, 2, 3, 4, 5, 6, 7));
       o[i % NDV] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(i < NDV ? pa0 : pa1, vb, o[i % NDV],
@@ -643,28 +701,21 @@ void attn_mla_kernel(AttnArgs a) {
 #pragma unroll
   for (int st = 0; st < NST - 1; ++st)
     if (st < n_it) issue(st, st);
-
-  // Q^T operand: Q[head][16kk + 8 half .. +7], loaded while the first chunks are in flight
-  bf16x8_t qreg[NKK];
-  {
-    const uint16_t* qrow = a.q + ((int64_t)unit * a.H + (head_ok ? head : 0)) * DQK + 8 * half;
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (head_ok) v = *reinterpret_cast<const u32x4*>(qrow + kk * 16);
-      qreg[kk] = __builtin_bit_cast(bf16x8_t, v);
-    }
+  if constexpr (PACED) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    load_q();
   }
-
 
   for (int it = 0; it < n_it; ++it) {
     // chunks it+1 .. it+NST-2 were issued earlier and may still be in flight
     wait_chunk<NST, LPW_MAX, LPW_MIN>(min(NST - 2, n_it - 1 - it), w_s < NL_REM);
-    // every wave is past its reads of buffer (it-1) % NST: refill it with chunk it+NST-1
-    if (it + NST - 1 < n_it) issue(it + NST - 1, (it + NST - 1) % NST);
-
     const uint16_t* tile = s_tiles + (it % NST) * TILE;
     const int cbase = chunk_base(it);
+    // the chunk's validity word, read before the next chunk's loads are issued
+    const uint32_t vmask = s_valid[(cbase - tok_begin) >> 5];
+    __builtin_amdgcn_sched_barrier(0);
+    // every wave is past its reads of buffer (it-1) % NST: refill it with chunk it+NST-1
+    if (it + NST - 1 < n_it) issue(it + NST - 1, (it + NST - 1) % NST);
 
     // ---- scores: S^T for the chunk's 32 tokens x this wave's 32 heads ----
     // K operand reads run KD k-steps ahead of the MFMAs (a small register ring; the
@@ -674,31 +725,27 @@ void attn_mla_kernel(AttnArgs a) {
     // covered in it: wait states before each MFMA for a just-written operand, and after the
     // last one before the scores are read.
     constexpr int KD = 4;
+    static_assert(KD == 4 && NKK > KD, "the waits below count a ring of 4 reads");
     f32x16 sacc, sacc1;  // even / odd k-steps: two independent MFMA chains
-    const uint16_t* krow = tile + (mla_row(col) * PP + half) * 8;
+    const uint32_t krow = lds_addr(tile + (mla_row(col) * PP + half) * 8);
     u32x4 kbuf[KD];
 #pragma unroll
-    for (int kk = 0; kk < KD; ++kk) kbuf[kk] = lds_load16(krow + kk * 16);
+    for (int kk = 0; kk < KD; ++kk) kbuf[kk] = lds_read_b128(krow + kk * 32);
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
-      if (kk == 0)
-        asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0"
-                     : "=&v"(sacc) : "v"(kbuf[0]), "v"(qreg[0]));
-      else if (kk == 1)
-        asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, 0"
-                     : "=&v"(sacc1) : "v"(kbuf[1]), "v"(qreg[1]));
-      else if (kk & 1)
-        asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0"
-                     : "+v"(sacc1) : "v"(kbuf[kk % KD]), "v"(qreg[kk]));
-      else
-        asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0"
-                     : "+v"(sacc) : "v"(kbuf[kk % KD]), "v"(qreg[kk]));
-      if (kk + KD < NKK) kbuf[kk % KD] = lds_load16(krow + (kk + KD) * 16);
+      // the K reads issued after read kk: those of k-steps kk+1 .. min(kk+KD-1, NKK-1)
+      const int later = NKK - 1 - kk < KD - 1 ? NKK - 1 - kk : KD - 1;
+      f32x16& acc = (kk & 1) ? sacc1 : sacc;
+      if (kk < 2) mfma_qk<KD - 1, true>(acc, kbuf[kk % KD], qreg[kk]);
+      else if (later == 3) mfma_qk<3, false>(acc, kbuf[kk % KD], qreg[kk]);
+      else if (later == 2) mfma_qk<2, false>(acc, kbuf[kk % KD], qreg[kk]);
+      else if (later == 1) mfma_qk<1, false>(acc, kbuf[kk % KD], qreg[kk]);
+      else mfma_qk<0, false>(acc, kbuf[kk % KD], qreg[kk]);
+      if (kk + KD < NKK) kbuf[kk % KD] = lds_read_b128(krow + (kk + KD) * 32);
       __builtin_amdgcn_sched_barrier(0);
     }
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(sacc), "+v"(sacc1));
     sacc += sacc1;
-    const uint32_t vmask = s_valid[(cbase - tok_begin) >> 5];
     int hq = half;
     asm volatile("" : "+v"(hq));
 #pragma unroll
@@ -981,10 +1028,10 @@ void launch_partial(const AttnArgs& args, hipStream_t stream) {
                      dim3(64 * HW * TW), 0, stream, args);
 }
 
-template <int HW, int TG, int NST>
+template <int HW, int TG, int NST, bool PACED = false>
 void launch_mla(const AttnArgs& args, hipStream_t stream) {
   const int nwg_pad = (args.n_wg + 7) & ~7;
-  hipLaunchKernelGGL((attn_mla_kernel<HW, TG, NST>), dim3(nwg_pad + args.rp.pf_wg),
+  hipLaunchKernelGGL((attn_mla_kernel<HW, TG, NST, PACED>), dim3(nwg_pad + args.rp.pf_wg),
                      dim3(64 * HW * TG), 0, stream, args);
 }
 
@@ -1040,6 +1087,16 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
   // the attention itself takes 58 against 40 us, hidden behind the other micro-batch's fetch.
   const int target = (is_mla(*attn) && (attn->flags & HISPARSE_ATTN_BESIDE_FETCH))
                          ? kTargetWorkgroups / 2 : kTargetWorkgroups;
+  // Beside another stream's fetch and with 32 or more workgroup columns (16 units of 128 heads
+  // and up, two token groups) the call hides behind the other micro-batch's longer fetch, whose
+  // host reads then set the step; there every workgroup loading its query together with its
+  // first chunks slows those reads, and the paced kernel loads the query after them: the
+  // two-micro-batch decode step at 32 requests took 1.82 ms unpaced against 1.69 ms paced (64
+  // requests: 3.43 against 3.23). Below 32 columns the chain of attention, merge and resolve is
+  // the longer one and the unpaced start wins (16 requests: 1.005 against 1.052 ms with the
+  // query loaded after the first chunks; 8 requests: 0.711 against 0.724).
+  p.paced = is_mla(*attn) && (attn->flags & HISPARSE_ATTN_BESIDE_FETCH) && p.tg == 2 &&
+            (int64_t)units * p.hb >= 32;
   int splits;
   if (attn->num_splits > 0) {
     splits = std::min(attn->num_splits, max_splits);
@@ -1133,6 +1190,7 @@ hipError_t launch_attention(const AttnPlan& p, const hisparse_attn_desc_t& attn,
 
   if (is_mla(attn)) {
     if (p.hw == 1) launch_mla<1, 1, 3>(a, stream);
+    else if (p.tg == 2 && p.paced) launch_mla<2, 2, 2, true>(a, stream);
     else if (p.tg == 2) launch_mla<2, 2, 2>(a, stream);
     else launch_mla<2, 1, 4>(a, stream);
   } else {

@@ -120,6 +120,7 @@ int resolve_threads(int32_t B);
 struct AttnPlan {
   int32_t hw, tw, hb;        // head waves, token waves, head blocks
   int32_t tg;                // latent attention: token groups merged within a workgroup
+  bool paced;                // latent attention: the query loaded after the first chunks
   int32_t n_tok;             // tokens per unit = k * tokens_per_record
   int32_t split_tokens;      // tokens per workgroup split (multiple of 32 * tw)
   int32_t n_wg_splits;       // workgroup splits per unit
