@@ -110,7 +110,6 @@ __device__ inline uint32_t weights_bf16x2(float s0, float s1, float m, float* ps
 }
 __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
-__device__ inline u32x4 lds_load16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
@@ -141,6 +140,15 @@ __device__ inline v4i16 lds_read_tr16_b64(uint32_t addr) {
 template <int N>
 __device__ __forceinline__ void lgkm_wait2(v4i16& a, v4i16& b) {
   asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(a), "+v"(b) : "n"(N));
+}
+// The same for two 16-byte reads, with n (a constant once the caller's loop is unrolled, at
+// most M) selecting the count.
+template <int M>
+__device__ __forceinline__ void lgkm_wait2_upto(int n, u32x4& a, u32x4& b) {
+  if constexpr (M >= 0) {
+    if (n == M) asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(a), "+v"(b) : "n"(M));
+    else lgkm_wait2_upto<M - 1>(n, a, b);
+  }
 }
 // S^T += K . Q^T for one k-step once the K rows' read (with at most N later LDS reads) is in;
 // the first step of a chain (FIRST) starts from zero. The s_nop covers the wait states after a
@@ -290,16 +298,6 @@ void attn_partial_kernel(AttnArgs a) {
 
   const int head = hb * 16 * HW + hg * 16 + (lane & 15);
   const bool head_ok = head < a.H;
-  bf16x8_t qreg[NKK];
-  {
-    const uint16_t* qrow = a.q + ((int64_t)unit * a.H + (head_ok ? head : 0)) * DQK + 8 * g;
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (head_ok) v = *reinterpret_cast<const u32x4*>(qrow + kk * 32);
-      qreg[kk] = __builtin_bit_cast(bf16x8_t, v);
-    }
-  }
 
   f32x4 o[NOUT];
 #pragma unroll
@@ -307,6 +305,16 @@ void attn_partial_kernel(AttnArgs a) {
   float m_run = -INFINITY, l_run = 0.f;
 
   __syncthreads();  // s_idx is ready
+  // Q^T operand, loaded unconditionally (a head past H reads head 0's row: its scores are never
+  // stored and, being head 0's, move no reference max that head 0 does not) and before the
+  // validity masks are written and the first chunks issued, so that it is in flight meanwhile
+  bf16x8_t qreg[NKK];
+  {
+    const uint16_t* qrow = a.q + ((int64_t)unit * a.H + (head_ok ? head : 0)) * DQK + 8 * g;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk)
+      qreg[kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(qrow + kk * 32));
+  }
   const int n_it = (tok_end - tok_begin + kChunk * TW - 1) / (kChunk * TW);
   {
     // every chunk the token groups iterate over gets its word, including chunks that lie
@@ -364,57 +372,68 @@ void attn_partial_kernel(AttnArgs a) {
     // read); lane t then holds V[those tokens][16n + t], i.e. B[k = 8g .. 8g+7][n = t], in the
     // token order of this lane's P values.
     const int ts = (lane & 15) >> 2, q4 = (lane & 3) * 4;
-    const uint16_t* vrow0 = tile + tile_row(4 * g + ts) * PP * 8 + VOFF + q4;
-    const uint16_t* vrow1 = vrow0 + 16 * PP * 8;
+    const uint32_t vrow0 = lds_addr(tile + tile_row(4 * g + ts) * PP * 8 + VOFF + q4);
+    const uint32_t vrow1 = vrow0 + 2 * (16 * PP * 8);
+    // transpose reads VD output tiles ahead of their MFMAs (opaque LDS reads, see lds_read_b128)
+    constexpr int VD = 3;
+    static_assert(VD == 3 && NOUT > VD, "the waits below count a ring of 3 read pairs");
+    v4i16 vlo[VD], vhi[VD];
+    auto vread = [&](int n, int slot) {
+      vlo[slot] = lds_read_tr16_b64(vrow0 + 2 * 16 * n);
+      vhi[slot] = lds_read_tr16_b64(vrow1 + 2 * 16 * n);
+    };
+#pragma unroll
+    for (int n = 0; n < VD; ++n) vread(n, n);
 #pragma unroll
     for (int n = 0; n < NOUT; ++n) {
-      const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vrow0 + 16 * n));
-      const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vrow1 + 16 * n));
+      // the reads issued after tile n's pair: those of tiles n+1 .. min(n+VD-1, NOUT-1)
+      const int later = NOUT - 1 - n < VD - 1 ? NOUT - 1 - n : VD - 1;
+      if (later == 2) lgkm_wait2<4>(vlo[n % VD], vhi[n % VD]);
+      else if (later == 1) lgkm_wait2<2>(vlo[n % VD], vhi[n % VD]);
+      else lgkm_wait2<0>(vlo[n % VD], vhi[n % VD]);
       const bf16x8_t vb = __builtin_bit_cast(
-          bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+          bf16x8_t, __builtin_shufflevector(vlo[n % VD], vhi[n % VD], 0, 1, 2, 3, 4, 5, 6, 7));
       o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[n], 0, 0, 0);
+      if (n + VD < NOUT) vread(n + VD, n % VD);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    // transpose reads two output tiles ahead of their MFMAs
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-    for (int n = 0; n < NOUT - 2; ++n) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
   };
 
   for (;;) {
     for (; it < n_it; ++it) {
       // chunks it+1 .. it+NST-2 were issued earlier and may still be in flight
       wait(min(NST - 2, n_it - 1 - it));
+      const uint16_t* tile = s_tiles + (it % NST) * TILE;
+      const int cbase = tok_begin + it * kChunk * TW + tg * kChunk;
+      // the chunk's validity word, read before the next chunk's loads are issued
+      const uint32_t vmask = s_valid[(cbase - tok_begin) >> 5];
+      __builtin_amdgcn_sched_barrier(0);
       // every wave is past its reads of buffer (it-1) % NST: refill it with chunk it+NST-1
       if (it + NST - 1 < n_it) issue(it + NST - 1, (it + NST - 1) % NST);
 
-      const uint16_t* tile = s_tiles + (it % NST) * TILE;
-      const int cbase = tok_begin + it * kChunk * TW + tg * kChunk;
-
       // ---- scores: S^T tiles for tokens [0,16) and [16,32) of the chunk ----
+      // all K reads first (opaque LDS reads, see lds_read_b128), then each k-step's MFMAs once
+      // its pair is in
       s0 = f32x4{0.f, 0.f, 0.f, 0.f};
       s1 = f32x4{0.f, 0.f, 0.f, 0.f};
-      const uint16_t* k0 = tile + (tile_row(lane & 15) * PP + g) * 8;
-      const uint16_t* k1 = k0 + 16 * PP * 8;
+      const uint32_t k0 = lds_addr(tile + (tile_row(lane & 15) * PP + g) * 8);
+      const uint32_t k1 = k0 + 2 * (16 * PP * 8);
+      static_assert(NKK <= 8, "lgkmcnt holds at most 15 outstanding reads");
+      u32x4 ka[NKK], kb[NKK];
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) {
-        const bf16x8_t a0 = __builtin_bit_cast(bf16x8_t, lds_load16(k0 + kk * 32));
-        const bf16x8_t a1 = __builtin_bit_cast(bf16x8_t, lds_load16(k1 + kk * 32));
-        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qreg[kk], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, qreg[kk], s1, 0, 0, 0);
+        ka[kk] = lds_read_b128(k0 + 2 * kk * 32);
+        kb[kk] = lds_read_b128(k1 + 2 * kk * 32);
       }
-      // keep operand reads two k-steps ahead of the MFMAs instead of all hoisted up front
-      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-      for (int kk = 0; kk < NKK - 2; ++kk) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      for (int kk = 0; kk < NKK; ++kk) {
+        lgkm_wait2_upto<2 * (NKK - 1)>(2 * (NKK - 1 - kk), ka[kk], kb[kk]);
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka[kk]),
+                                                    qreg[kk], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kb[kk]),
+                                                    qreg[kk], s1, 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-      const uint32_t vmask = s_valid[(cbase - tok_begin) >> 5];
       int gq = g;
       asm volatile("" : "+v"(gq));
 #pragma unroll
