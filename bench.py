@@ -83,7 +83,8 @@ def parse():
     ap.add_argument("--carry-hint", action=argparse.BooleanOptionalAction, default=True,
                     help="attention calls that carry a replay into the next shared layer, and "
                          "their merges, take the HISPARSE_ATTN_CARRIES_REPLAY plan hint (fewer, "
-                         "longer splits for small calls)")
+                         "longer splits for small calls; not with --fetch none, where the replay "
+                         "moves nothing)")
     ap.add_argument("--fetch-workgroups", type=int, default=0,
                     help="workgroups of one fetch launch (0 = the library default)")
     ap.add_argument("--schedule", choices=["overlap", "serial", "side", "batched"],
@@ -1046,7 +1047,8 @@ def main() -> int:
                            speculate=args.speculate, append=args.append, share=share,
                            status_string=hs.hisparse_status_string,
                            handover=max(0, min(256, args.handover_share)),
-                           ad_carry=ad_carry if args.carry_hint else None,
+                           ad_carry=(ad_carry if args.carry_hint and fetch != hs.HISPARSE_FETCH_NONE
+                                     else None),
                            link_s=link_s, link_join=link_join)
     step = sched.step
 
