@@ -1106,16 +1106,16 @@ hisparse_status_t plan_attention(int32_t units, int32_t top_k, int32_t record_by
   // the attention itself takes 58 against 40 us, hidden behind the other micro-batch's fetch.
   const int target = (is_mla(*attn) && (attn->flags & HISPARSE_ATTN_BESIDE_FETCH))
                          ? kTargetWorkgroups / 2 : kTargetWorkgroups;
-  // Beside another stream's fetch and with 32 or more workgroup columns (16 units of 128 heads
-  // and up, two token groups) the call hides behind the other micro-batch's longer fetch, whose
-  // host reads then set the step; there every workgroup loading its query together with its
-  // first chunks slows those reads, and the paced kernel loads the query after them: the
-  // two-micro-batch decode step at 32 requests took 1.82 ms unpaced against 1.69 ms paced (64
-  // requests: 3.43 against 3.23). Below 32 columns the chain of attention, merge and resolve is
-  // the longer one and the unpaced start wins (16 requests: 1.005 against 1.052 ms with the
-  // query loaded after the first chunks; 8 requests: 0.711 against 0.724).
+  // Beside another stream's fetch and with more than 16 workgroup columns (more than 8 units of
+  // 128 heads, two token groups) the call hides behind the other micro-batch's longer fetch,
+  // whose host reads then set the step; there every workgroup loading its query together with
+  // its first chunks slows those reads, and the paced kernel loads the query after them. The
+  // two-micro-batch decode step at 20, 24, 28, 32 and 64 requests took 1.247, 1.450, 1.730,
+  // 1.82 and 3.43 ms unpaced against 1.241, 1.371, 1.519, 1.69 and 3.23 ms paced. At 16 columns
+  // and below the chain of attention, merge and resolve is the longer one and the unpaced start
+  // wins (16 requests: 1.005 against 1.052 ms; 8 requests: 0.711 against 0.724).
   p.paced = is_mla(*attn) && (attn->flags & HISPARSE_ATTN_BESIDE_FETCH) && p.tg == 2 &&
-            (int64_t)units * p.hb >= 32;
+            (int64_t)units * p.hb > 16;
   int splits;
   if (attn->num_splits > 0) {
     splits = std::min(attn->num_splits, max_splits);
