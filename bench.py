@@ -75,6 +75,17 @@ def parse():
                          "first only (then run free from that offset; on the DSA/MLA workload "
                          "1.5%% slower, and a perturbation such as a profiler attached can push "
                          "the chains into lockstep for good)")
+    ap.add_argument("--link-turns", choices=["events", "device"], default="device",
+                    help="how micro-batches pass the host link on: every transfer is launched "
+                         "after its own resolve and waits on the device for the previous one's "
+                         "signal (hisparse_fetch_turn; default), or each transfer's stream waits "
+                         "for an event recorded after the previous transfer (DSA/MLA 1.69 "
+                         "against 1.65 ms per step, NSA blocks 1.62 against 1.54); the "
+                         "kernel-span pass always uses events, so that a fetch's span is its "
+                         "transfer alone")
+    ap.add_argument("--turn-share", type=int, default=256, metavar="S",
+                    help="device link turns: the next transfer starts once S/256 of the "
+                         "previous one's workgroups have finished (128-256 measured equal)")
     ap.add_argument("--attn-plan", choices=["auto", "beside-fetch", "own-gpu"], default="auto",
                     help="latent attention's plan hint: 'beside-fetch' (HISPARSE_ATTN_BESIDE_FETCH: "
                          "another micro-batch's host-link fetch runs beside each attention call) "
@@ -649,7 +660,8 @@ class DecodeSchedule:
 
     def __init__(self, *, w, k, groups, mbs, n_mb, n_qv, ad_ref, lib, rec, wait, root_s, fork_ev,
                  join_evs, schedule, turns, speculate, append, share, status_string,
-                 handover=0, ad_carry=None, link_s=None, link_join=None):
+                 handover=0, ad_carry=None, link_s=None, link_join=None, dturns=None,
+                 turn_slots=1, turn_share=256):
         self.w, self.k, self.groups, self.mbs, self.n_mb, self.n_qv = w, k, groups, mbs, n_mb, n_qv
         self.ad_ref, self.L, self.rec, self.wait, self.root_s = ad_ref, lib, rec, wait, root_s
         # the descriptor of attention calls that carry a replay, and of their merges
@@ -664,6 +676,22 @@ class DecodeSchedule:
         if link_s is not None and (n_mb < 2 or turns != "all" or handover or link_join is None):
             raise ValueError("a shared link stream takes turns at every layer, without a "
                              "hand-over share, between two or more micro-batches")
+        # link turns on the device (hisparse_fetch_turn): a word pair per transfer of each of
+        # turn_slots consecutive steps, reset on the root stream before each fork; every
+        # transfer of a step waits on the device for the previous one's signal instead of its
+        # stream waiting for an event
+        self.dturns, self.turn_slots, self.turn_share = dturns, turn_slots, turn_share
+        if dturns is not None and (n_mb < 2 or handover or link_s is not None or (
+                schedule in ("serial", "batched") and any(sh for _, sh in groups))):
+            raise ValueError("device link turns take the anchors' own fetches of two or more "
+                             "micro-batches, without a hand-over share or a link stream")
+
+    def n_turns(self) -> int:
+        return self.turn_slots * len(self.groups) * self.n_mb
+
+    def turn_index(self, t, gi, i) -> int:
+        """The device turn of the transfer of group gi of micro-batch i in step t."""
+        return ((t % self.turn_slots) * len(self.groups) + gi) * self.n_mb + i
 
     def events_per_step(self) -> int:
         """Timing events one step may consume (two per library call)."""
@@ -684,7 +712,8 @@ class DecodeSchedule:
 
     def group_step(self, mb, gi, t, ev, spans, sel_override, q_override, link):
         """Share group gi of decode step t for one micro-batch. `link`: (event to wait for
-        before this group's host-link transfer, event to record after it), or None."""
+        before this group's host-link transfer, event to record after it), with device turns
+        (turn to wait for or -1, turn to signal), or None."""
         L, call, rec, wait, k, w = self.L, self.call, self.rec, self.wait, self.k, self.w
         a, shared = self.groups[gi]
         qv = q_override[mb.u0] if q_override else mb.q_p[t % self.n_qv]
@@ -714,6 +743,11 @@ class DecodeSchedule:
                 call(name, ls, ev, spans, fn, *fargs[:-1], ls)
                 rec(mb.link[gi], ls)
                 wait(ms, mb.link[gi], 0)
+                return
+            if link and self.dturns is not None:
+                # the link turn on the device: fargs = (handle, layer, stream)
+                call(name, ms, ev, spans, L.hisparse_fetch_turn, fargs[0], fargs[1],
+                     self.dturns, self.n_turns(), link[0], link[1], self.turn_share, ms)
                 return
             if link and link[0] is not None:
                 wait(ms, link[0], 0)
@@ -806,6 +840,10 @@ class DecodeSchedule:
         chains run free, with no cross-stream wait per layer."""
         mbs, n_mb, rec, wait = self.mbs, self.n_mb, self.rec, self.wait
         if n_mb > 1 and fork:
+            if self.dturns is not None:  # ordered before every micro-batch by the fork
+                self.call("link_turns_reset", self.root_s, None, None,
+                          self.L.hisparse_link_turns_reset, self.dturns, self.n_turns(),
+                          self.root_s)
             rec(self.fork_ev, self.root_s)
             for mb in mbs[1:]:
                 wait(mb.main, self.fork_ev, 0)
@@ -814,7 +852,11 @@ class DecodeSchedule:
         for gi in range(len(self.groups)):
             for i, mb in enumerate(mbs):
                 link = None
-                if n_mb > 1 and (self.turns == "all" or gi == 0):
+                if n_mb > 1 and (self.turns == "all" or gi == 0) and self.dturns is not None:
+                    ti = self.turn_index(t, gi, i)
+                    first = i == 0 and (gi == 0 or self.turns != "all")
+                    link = (-1 if first else ti - 1, ti)
+                elif n_mb > 1 and (self.turns == "all" or gi == 0):
                     prev = (mbs[i - 1].link[gi] if i > 0 else
                             (mbs[-1].link[gi - 1] if gi > 0 else None))
                     link = (prev, mb.link[gi])
@@ -1039,6 +1081,11 @@ def main() -> int:
         f"{args.schedule}, set up in {time.time() - t0:.1f}s")
 
     share = max(0, min(256, args.merge_replay_share))
+    dturns = dturns_t = None
+    if args.link_turns == "device" and n_mb > 1 and fetch == hs.HISPARSE_FETCH_ZERO_COPY:
+        n_t = max(1, args.graph_steps) * len(groups) * n_mb
+        dturns_t = torch.zeros(2 * n_t, dtype=torch.int32, device=dev)
+        dturns = dturns_t.data_ptr()
     rec = hip.L.hipEventRecord
     wait = hip.L.hipStreamWaitEvent
     sched = DecodeSchedule(w=w, k=k, groups=groups, mbs=mbs, n_mb=n_mb, n_qv=n_qv, ad_ref=ad_ref,
@@ -1049,7 +1096,9 @@ def main() -> int:
                            handover=max(0, min(256, args.handover_share)),
                            ad_carry=(ad_carry if args.carry_hint and fetch != hs.HISPARSE_FETCH_NONE
                                      else None),
-                           link_s=link_s, link_join=link_join)
+                           link_s=link_s, link_join=link_join, dturns=dturns,
+                           turn_slots=max(1, args.graph_steps),
+                           turn_share=max(1, min(256, args.turn_share)))
     step = sched.step
 
     # pinned H2D sweep over the same pool (hipMemcpyAsync), before the timed region
@@ -1086,6 +1135,7 @@ def main() -> int:
     # duration while sharing the GPU.
     events = [hip.event() for _ in range(per_step_events * args.steps)]
     spans = []
+    sched.dturns = None  # event turns: a transfer's span holds no wait for its turn
     cal0, cal1 = hip.event(), hip.event()
     rec(cal0, root_s)
     torch.cuda._sleep(1_000_000)
@@ -1351,6 +1401,7 @@ def main() -> int:
     io_busy_ms_per_step = io_busy * 1e3 / max(1, Ks)
 
     # the same steps replayed from a captured HIP graph (cold reset, same warmup)
+    sched.dturns = dturns
     graph = None
     if not args.no_graph and not host_issued:
         # One graph covers S consecutive steps (S even, so every replay sees the same query
@@ -1486,6 +1537,8 @@ def main() -> int:
                    "merge_replay_share": share if args.schedule == "overlap" else None,
                    "handover_share": args.handover_share if n_mb > 1 else None,
                    "link_stream": bool(link_s),
+                   "link_turns": "device" if dturns is not None else "events",
+                   "turn_share": sched.turn_share if dturns is not None else None,
                    "attn_plan": "beside-fetch" if beside else "own-gpu",
                    "steps_per_graph": graph["steps_per_graph"] if graph else None},
         "decode_tokens_per_s": w.num_requests * K / wall,

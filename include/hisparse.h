@@ -277,6 +277,35 @@ hisparse_status_t hisparse_fetch(hisparse_cache_t cache, int32_t layer, void* st
 hisparse_status_t hisparse_fetch_part(hisparse_cache_t cache, int32_t layer, int32_t part_begin,
                                       int32_t part_end, void* stream);
 
+/* [async] hisparse_fetch (Section 3.4 Phase 4) taking turns on the host link with fetches
+ * issued on other streams, ordered on the device instead of by stream events. The paper
+ * overlaps the fetch with other work so that IO stays off the critical path (Section 3.5);
+ * with several independent batches of units, each with its own stream, one batch's fetch
+ * overlaps another's attention best when the fetches use the link one after another.
+ *   d_turns int32 [2 * n_turns] (n_turns >= 1), device memory owned by the caller, zeroed with
+ *     hisparse_link_turns_reset before the first launch of a sequence of turns; turn i is
+ *     the pair d_turns[2i], d_turns[2i + 1]. Each turn is signalled by one launch and waited
+ *     for by at most one.
+ *   wait_turn: -1, or the turn whose signal this launch waits for before its first host
+ *     read. The launch's waves are resident while they wait, polling d_turns.
+ *   signal_turn: -1, or the turn this launch signals once signal_share / 256 (1..256) of its
+ *     workgroups have finished their copies (256: all of them, the link free).
+ * The copies and results equal hisparse_fetch's whatever the order of the launches: a turn
+ * orders only the use of the link, never data, and a wait ends by itself after about 4 ms,
+ * so a turn never signalled (reset missing, its launch on a stream that waits for this one)
+ * costs time, not correctness. For a sequence issued on streams that may run concurrently.
+ * HISPARSE_ERR_UNSUPPORTED unless the cache fetches zero-copy (the host-issued paths and
+ * HISPARSE_FETCH_NONE launch no kernel); INVALID_ARG for a shared layer, a null d_turns,
+ * n_turns < 1, indices outside [-1, n_turns), wait_turn == signal_turn, or a share outside
+ * 1..256. */
+hisparse_status_t hisparse_fetch_turn(hisparse_cache_t cache, int32_t layer, int32_t* d_turns,
+                                      int32_t n_turns, int32_t wait_turn, int32_t signal_turn,
+                                      int32_t signal_share, void* stream);
+
+/* [async] Zero n_turns (1..2^24) link turns, d_turns[0 .. 2 * n_turns), with a fill kernel on
+ * `stream` (capturable; no memset node). See hisparse_fetch_turn. */
+hisparse_status_t hisparse_link_turns_reset(int32_t* d_turns, int32_t n_turns, void* stream);
+
 /* [async] Phase 4 for units [unit_begin, unit_begin + unit_count) of an anchor layer only
  * (Section 3.4; units are independent caches). Calls over disjoint ranges together equal
  * hisparse_fetch, so a caller can pipeline a layer's fetch with the attention of the units

@@ -551,7 +551,8 @@ hisparse::FetchArgs fetch_args(hisparse_cache_t c, int32_t anchor, int32_t targe
 hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t target,
                                 hipStream_t stream, int32_t u0 = 0, int32_t nu = -1,
                                 int32_t n_layers = 1, int32_t part_lo = 0,
-                                int32_t part_hi = 256) {
+                                int32_t part_hi = 256,
+                                const hisparse::LinkTurn* turn = nullptr) {
   if (nu < 0) nu = c->units - u0;
   if (c->desc.fetch == HISPARSE_FETCH_NONE || nu == 0 || part_lo >= part_hi) return HISPARSE_OK;
   if ((c->desc.fetch == HISPARSE_FETCH_SDMA || c->desc.fetch == HISPARSE_FETCH_STAGED) &&
@@ -711,8 +712,8 @@ hisparse_status_t enqueue_fetch(hisparse_cache_t c, int32_t anchor, int32_t targ
                                        std::min(n_layers - j0, hisparse::kMaxFetchLayers));
     f.part_lo = part_lo;
     f.part_hi = part_hi;
-    if (hisparse::launch_fetch(f, transfer_block(c->desc), fetch_workgroups(c->desc), stream) !=
-        hipSuccess)
+    if (hisparse::launch_fetch(f, transfer_block(c->desc), fetch_workgroups(c->desc), stream,
+                               turn) != hipSuccess)
       return HISPARSE_ERR_HIP;
   }
   return HISPARSE_OK;
@@ -729,6 +730,27 @@ hisparse_status_t hisparse_fetch_part(hisparse_cache_t c, int32_t layer, int32_t
   if (!c || !is_anchor(c, layer) || part_begin < 0 || part_begin > part_end || part_end > 256)
     return HISPARSE_ERR_INVALID_ARG;
   return enqueue_fetch(c, layer, layer, as_stream(stream), 0, -1, 1, part_begin, part_end);
+}
+
+hisparse_status_t hisparse_fetch_turn(hisparse_cache_t c, int32_t layer, int32_t* d_turns,
+                                      int32_t n_turns, int32_t wait_turn, int32_t signal_turn,
+                                      int32_t signal_share, void* stream) {
+  if (!c || !is_anchor(c, layer) || !d_turns || n_turns < 1 || wait_turn < -1 ||
+      signal_turn < -1 || wait_turn >= n_turns || signal_turn >= n_turns || signal_share < 1 ||
+      signal_share > 256 || (wait_turn >= 0 && wait_turn == signal_turn))
+    return HISPARSE_ERR_INVALID_ARG;
+  // host-issued copies and no-IO caches have no kernel to take a turn (a waiting launch would
+  // run out its bound)
+  if (c->desc.fetch != HISPARSE_FETCH_ZERO_COPY) return HISPARSE_ERR_UNSUPPORTED;
+  const hisparse::LinkTurn t{d_turns, wait_turn, signal_turn, signal_share};
+  return enqueue_fetch(c, layer, layer, as_stream(stream), 0, -1, 1, 0, 256, &t);
+}
+
+hisparse_status_t hisparse_link_turns_reset(int32_t* d_turns, int32_t n_turns, void* stream) {
+  if (!d_turns || n_turns < 1 || n_turns > (1 << 24)) return HISPARSE_ERR_INVALID_ARG;
+  return hisparse::launch_turns_reset(d_turns, n_turns, as_stream(stream)) == hipSuccess
+             ? HISPARSE_OK
+             : HISPARSE_ERR_HIP;
 }
 
 hisparse_status_t hisparse_fetch_units(hisparse_cache_t c, int32_t layer, int32_t unit_begin,

@@ -109,8 +109,18 @@ constexpr int kPhaseStamps = HISPARSE_RESOLVE_PHASE_SLOTS;
 constexpr int kPhaseStampUnits = HISPARSE_RESOLVE_PHASE_UNITS;
 hipError_t read_resolve_phase_stamps(uint64_t* host, int32_t units);
 hipError_t launch_scatter(const ScatterArgs& a, hipStream_t stream);
+// Host-link turns between fetch launches on different streams (hisparse_fetch_turn): turn i
+// is the word pair turns[2i] (finished workgroups of the launch that signals it) and
+// turns[2i + 1] (non-zero once the launch that waits for it may start reading).
+struct LinkTurn {
+  int32_t* turns;  // null: no turn taking
+  int32_t wait;    // turn to wait for before the first host read (-1: none)
+  int32_t signal;  // turn to signal (-1: none)
+  int32_t share;   // 1..256: the 256ths of this launch's workgroups that finish before it does
+};
 hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgroups,
-                        hipStream_t stream);
+                        hipStream_t stream, const LinkTurn* turn = nullptr);
+hipError_t launch_turns_reset(int32_t* turns, int32_t n_turns, hipStream_t stream);
 hipError_t launch_reset_state(const StateArgs& a, hipStream_t stream);
 hipError_t launch_admit(const AdmitArgs& a, int32_t n_groups, hipStream_t stream);
 size_t resolve_lds_bytes(int32_t k, int32_t B);

@@ -447,15 +447,49 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   RESOLVE_STAMP(8);
 }
 
+// Link turns as the fetch kernel sees them: the word to poll before reading (null: none), the
+// pair to count finished workgroups into (null: none), and the count that opens the next turn.
+struct TurnDev {
+  const int32_t* wait_flag;
+  int32_t* signal_pair;
+  int32_t go;
+};
+
+// A turn only orders the launches' use of the host link; no launch reads what another writes,
+// so a wait that outlasts this bound simply proceeds.
+constexpr uint64_t kTurnWaitTicks = 400000;  // 4 ms of the constant 100 MHz clock
+
 template <int U>
-__global__ __launch_bounds__(kFetchThreads) void fetch_kernel(FetchArgs a, FastDiv div_cpr) {
+__global__ __launch_bounds__(kFetchThreads) void fetch_kernel(FetchArgs a, FastDiv div_cpr,
+                                                              TurnDev turn) {
   // The fetch shares its CUs with other streams' kernels (the other micro-batch's attention and
   // merge); its waves issue little but each issue keeps the host link fed, so they go first.
   __builtin_amdgcn_s_setprio(3);
+  if (turn.wait_flag) {
+    // Waves of a launch that waits for its turn are resident already and poll the flag (an
+    // uncached device-scope read every few hundred cycles), so the link passes from one launch
+    // to the next without a dependency through the command processor.
+    const uint64_t t0 = wall_clock64();
+    while (__hip_atomic_load(turn.wait_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0 &&
+           wall_clock64() - t0 < kTurnWaitTicks)
+      __builtin_amdgcn_s_sleep(8);
+  }
   // grid z: the target layers (one plan, each layer's own host records and cache)
   fetch_slice<U>(a, div_cpr, blockIdx.y, blockIdx.z,
                  blockIdx.x * (uint32_t)kFetchThreads + threadIdx.x,
                  gridDim.x * (uint32_t)kFetchThreads);
+  if (turn.signal_pair && threadIdx.x == 0) {
+    // this wave's host reads have all returned (its stores consumed them)
+    const int32_t n = __hip_atomic_fetch_add(turn.signal_pair, 1, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT) + 1;
+    if (n == turn.go)
+      __hip_atomic_store(turn.signal_pair + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+__global__ void turns_reset_kernel(int32_t* turns, int32_t n) {
+  for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+    turns[i] = 0;
 }
 
 // Staged fetch: the records packed per unit in the device staging buffer go to their slots
@@ -627,7 +661,7 @@ hipError_t launch_scatter(const ScatterArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgroups,
-                        hipStream_t stream) {
+                        hipStream_t stream, const LinkTurn* turn) {
   const int U = transfer_block_bytes / 16;
   const int64_t max_chunks = (int64_t)a.k * (a.R / 16);
   int64_t x = (max_chunks + (int64_t)kFetchThreads * U - 1) / ((int64_t)kFetchThreads * U);
@@ -637,13 +671,27 @@ hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgr
   if (x > cap) x = cap;
   const dim3 grid((unsigned)x, (unsigned)a.units, (unsigned)a.n_layers);
   const FastDiv f = make_fastdiv((uint32_t)(a.R / 16));
-  switch (U) {
-    case 1: hipLaunchKernelGGL(fetch_kernel<1>, grid, dim3(kFetchThreads), 0, stream, a, f); break;
-    case 2: hipLaunchKernelGGL(fetch_kernel<2>, grid, dim3(kFetchThreads), 0, stream, a, f); break;
-    case 4: hipLaunchKernelGGL(fetch_kernel<4>, grid, dim3(kFetchThreads), 0, stream, a, f); break;
-    case 8: hipLaunchKernelGGL(fetch_kernel<8>, grid, dim3(kFetchThreads), 0, stream, a, f); break;
-    default: hipLaunchKernelGGL(fetch_kernel<16>, grid, dim3(kFetchThreads), 0, stream, a, f); break;
+  TurnDev t{nullptr, nullptr, 0};
+  if (turn && turn->turns) {
+    const int64_t wgs = x * a.units * a.n_layers;
+    if (turn->wait >= 0) t.wait_flag = turn->turns + 2 * (int64_t)turn->wait + 1;
+    if (turn->signal >= 0) t.signal_pair = turn->turns + 2 * (int64_t)turn->signal;
+    t.go = (int32_t)std::max<int64_t>(1, (wgs * turn->share + 255) / 256);
   }
+  switch (U) {
+    case 1: hipLaunchKernelGGL(fetch_kernel<1>, grid, dim3(kFetchThreads), 0, stream, a, f, t); break;
+    case 2: hipLaunchKernelGGL(fetch_kernel<2>, grid, dim3(kFetchThreads), 0, stream, a, f, t); break;
+    case 4: hipLaunchKernelGGL(fetch_kernel<4>, grid, dim3(kFetchThreads), 0, stream, a, f, t); break;
+    case 8: hipLaunchKernelGGL(fetch_kernel<8>, grid, dim3(kFetchThreads), 0, stream, a, f, t); break;
+    default: hipLaunchKernelGGL(fetch_kernel<16>, grid, dim3(kFetchThreads), 0, stream, a, f, t); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_turns_reset(int32_t* turns, int32_t n_turns, hipStream_t stream) {
+  const int32_t n = 2 * n_turns;
+  const int blocks = std::max(1, std::min(64, (n + 255) / 256));
+  hipLaunchKernelGGL(turns_reset_kernel, dim3(blocks), dim3(256), 0, stream, turns, n);
   return hipGetLastError();
 }
 

@@ -46,8 +46,8 @@ EXPORTED = (
     "hisparse_status_string", "hisparse_validate_desc", "hisparse_validate_attn",
     "hisparse_cache_create", "hisparse_cache_destroy", "hisparse_host_pool",
     "hisparse_layer_cache", "hisparse_reset", "hisparse_resolve", "hisparse_resolve_tables",
-    "hisparse_fetch", "hisparse_fetch_part", "hisparse_fetch_units", "hisparse_fetch_group",
-    "hisparse_prefetch_layer",
+    "hisparse_fetch", "hisparse_fetch_part", "hisparse_fetch_turn", "hisparse_link_turns_reset",
+    "hisparse_fetch_units", "hisparse_fetch_group", "hisparse_prefetch_layer",
     "hisparse_prefetch_layers", "hisparse_append", "hisparse_request_acquire",
     "hisparse_request_release", "hisparse_reset_units", "hisparse_stage", "hisparse_speculate",
     "hisparse_decode_workspace_bytes", "hisparse_sparse_decode", "hisparse_sparse_decode_layers",
@@ -116,6 +116,8 @@ def lib() -> ctypes.CDLL:
             "hisparse_resolve_tables": (_I32, [_V, _I32, _V, _V, _V, _V]),
             "hisparse_fetch": (_I32, [_V, _I32, _V]),
             "hisparse_fetch_part": (_I32, [_V, _I32, _I32, _I32, _V]),
+            "hisparse_fetch_turn": (_I32, [_V, _I32, _V, _I32, _I32, _I32, _I32, _V]),
+            "hisparse_link_turns_reset": (_I32, [_V, _I32, _V]),
             "hisparse_fetch_units": (_I32, [_V, _I32, _I32, _I32, _V]),
             "hisparse_fetch_group": (_I32, [_V, _I32, _I32, _V]),
             "hisparse_prefetch_layer": (_I32, [_V, _I32, _I32, _V]),
@@ -272,6 +274,18 @@ def hisparse_fetch_part(cache: int, layer: int, part_begin: int, part_end: int,
                         stream=None) -> None:
     _check("hisparse_fetch_part",
            lib().hisparse_fetch_part(cache, layer, part_begin, part_end, _s(stream)))
+
+
+def hisparse_fetch_turn(cache: int, layer: int, d_turns, n_turns: int, wait_turn: int,
+                        signal_turn: int, signal_share: int = 256, stream=None) -> None:
+    _check("hisparse_fetch_turn",
+           lib().hisparse_fetch_turn(cache, layer, _p(d_turns), n_turns, wait_turn, signal_turn,
+                                     signal_share, _s(stream)))
+
+
+def hisparse_link_turns_reset(d_turns, n_turns: int, stream=None) -> None:
+    _check("hisparse_link_turns_reset",
+           lib().hisparse_link_turns_reset(_p(d_turns), n_turns, _s(stream)))
 
 
 def hisparse_fetch_units(cache: int, layer: int, unit_begin: int, unit_count: int,

@@ -106,3 +106,26 @@ def expected_order(slot_ts: np.ndarray) -> np.ndarray:
     """Slots of each unit by ascending (timestamp, slot)."""
     B = slot_ts.shape[-1]
     return np.stack([np.lexsort((np.arange(B), ts)) for ts in slot_ts]).astype(np.int32)
+
+
+def turn_step(runs, streams, turns, t, n_layers):
+    """One step of two or more micro-batches taking device link turns: the turns reset on the
+    first stream, the others forked from it, then per layer each micro-batch's resolve and its
+    fetch waiting for the previous micro-batch's turn; joined back into the first stream."""
+    n_mb = len(runs)
+    hs.hisparse_link_turns_reset(turns, n_layers * n_mb, streams[0])
+    fork = torch.cuda.Event()
+    fork.record(streams[0])
+    for s in streams[1:]:
+        s.wait_event(fork)
+    for l in range(n_layers):
+        for i, (r, s) in enumerate(zip(runs, streams)):
+            hs.hisparse_resolve_tables(r.cache.handle, l, r.sel_ptr(t, l), r.slots[l],
+                                       r.counts[l], s)
+            ti = l * n_mb + i
+            hs.hisparse_fetch_turn(r.cache.handle, l, turns, n_layers * n_mb, ti - 1, ti, 192,
+                                   s)
+    for s in streams[1:]:
+        j = torch.cuda.Event()
+        j.record(s)
+        streams[0].wait_event(j)

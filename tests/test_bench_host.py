@@ -142,8 +142,8 @@ class _FakeHip:
 
 
 class _FakeLib:
-    def __init__(self, log):
-        self._log = log
+    def __init__(self, log, args_log=None):
+        self._log, self._args = log, args_log
 
     def __getattr__(self, name):
         if not name.startswith("hisparse_"):
@@ -151,6 +151,8 @@ class _FakeLib:
 
         def call(*args):
             self._log.append(("call", name, args[-1]))  # the stream is the last argument
+            if self._args is not None:
+                self._args.append((len(self._log) - 1, name, args))
             return 0
         return call
 
@@ -159,7 +161,7 @@ LINK_S = 55  # the shared link stream of the link-stream cases
 
 
 def _schedule(hip, *, layers, G, n_mb, schedule, speculate, append, turns, share, steps,
-              handover=0, link=False):
+              handover=0, link=False, dturns=None, turn_slots=1, args_log=None):
     from types import SimpleNamespace
     w = SimpleNamespace(num_layers=layers, record_bytes=1152)
     groups = [(a, list(range(a + 1, min(a + G, layers)))) for a in range(0, layers, G)]
@@ -180,10 +182,11 @@ def _schedule(hip, *, layers, G, n_mb, schedule, speculate, append, turns, share
             link=[hip.event() for _ in groups], rdone=[hip.event() for _ in groups]))
     return bench.DecodeSchedule(
         w=w, k=2048, groups=groups, mbs=mbs, n_mb=n_mb, n_qv=2, ad_ref=None,
-        lib=_FakeLib(hip.log), rec=hip.rec, wait=hip.wait, root_s=1, fork_ev=hip.event(),
-        join_evs=[hip.event() for _ in mbs], schedule=schedule, turns=turns,
+        lib=_FakeLib(hip.log, args_log), rec=hip.rec, wait=hip.wait, root_s=1,
+        fork_ev=hip.event(), join_evs=[hip.event() for _ in mbs], schedule=schedule, turns=turns,
         speculate=speculate, append=append, share=share, status_string=str, handover=handover,
-        link_s=LINK_S if link else None, link_join=hip.event() if link else None)
+        link_s=LINK_S if link else None, link_join=hip.event() if link else None, dturns=dturns,
+        turn_slots=turn_slots, turn_share=192)
 
 
 TRANSFERS = ("hisparse_fetch", "hisparse_fetch_group", "hisparse_fetch_part")
@@ -323,3 +326,96 @@ def test_decode_schedule_link_stream():
         with pytest.raises(ValueError):
             _schedule(hip, layers=4, G=1, schedule="overlap", speculate=False, append=False,
                       share=0, steps=2, link=True, **bad)
+
+
+DTURNS = 4242  # the device turn array of the device-turn cases
+
+
+def test_decode_schedule_device_turns():
+    """Link turns taken on the device: every micro-batch's transfer is a hisparse_fetch_turn on
+    its own stream (no event between the micro-batches' streams for the link), waiting for the
+    turn the previous transfer (in group and micro-batch order) signals, within one window of
+    turns reset on the root stream before the fork that starts it (every step when enqueued
+    one by one, the first of the steps captured to a graph). Turn indices stay inside the
+    array, each is signalled once per window and waited for at most once, and only after its
+    signalling call was enqueued. Options it cannot combine with are refused."""
+    cases = [dict(layers=8, G=1, n_mb=2, schedule="overlap", speculate=False, append=False,
+                  turns="all"),
+             dict(layers=8, G=1, n_mb=3, schedule="overlap", speculate=False, append=True,
+                  turns="all"),
+             dict(layers=6, G=1, n_mb=2, schedule="overlap", speculate=True, append=False,
+                  turns="all"),
+             dict(layers=8, G=1, n_mb=2, schedule="overlap", speculate=False, append=False,
+                  turns="first"),
+             dict(layers=8, G=4, n_mb=2, schedule="overlap", speculate=False, append=False,
+                  turns="all"),
+             dict(layers=8, G=4, n_mb=2, schedule="side", speculate=False, append=False,
+                  turns="all")]
+    steps, S = 8, 3
+    for case in cases:
+        hip, args_log = _FakeHip(), []
+        sched = _schedule(hip, steps=steps, share=0, dturns=DTURNS, turn_slots=S,
+                          args_log=args_log, **case)
+        budget = sched.events_per_step()
+        windows = [[0], [1]]  # steps of each window of turns
+        sched.step(0)
+        sched.step(1)
+        for t0 in (2, 5):  # a graph of 3 steps, twice: fork at the first, join at the last
+            windows.append([t0, t0 + 1, t0 + 2])
+            for j in range(S):
+                ev = [hip.event() for _ in range(budget)]
+                sched.step(t0 + j, ev, [], fork=(j == 0), join=(j == S - 1))
+                for e in ev:
+                    hip.destroy(e)
+        mbs, n_mb, n_groups = sched.mbs, case["n_mb"], len(sched.groups)
+        n_turns = S * n_groups * n_mb
+        assert sched.n_turns() == n_turns
+        streams = {mb.main: i for i, mb in enumerate(mbs)}
+        links = {e for mb in mbs for e in mb.link}
+        assert not [x for x in hip.log if x[0] == "wait" and x[2] in links], case
+        ordered = n_groups if case["turns"] == "all" else 1  # groups that take turns
+        plain = [a for a in args_log if a[1] in TRANSFERS]
+        assert len(plain) == steps * (n_groups - ordered) * n_mb, case
+        assert all(a[1] == "hisparse_fetch" for a in plain), case
+        resets = [a for a in args_log if a[1] == "hisparse_link_turns_reset"]
+        fetches = [a for a in args_log if a[1] == "hisparse_fetch_turn"]
+        # the eager steps 0 and 1 reset once each; each graph once
+        assert len(resets) == 2 + 2, case
+        for i, _, args in resets:
+            assert args == (DTURNS, n_turns, 1), case
+            assert hip.log[i + 1] == ("rec", sched.fork_ev, 1), case  # before the fork
+        assert len(fetches) == steps * ordered * n_mb, case
+        bounds = [i for i, _, _ in resets] + [len(hip.log)]
+        for w in range(len(resets)):  # one window of turns
+            win = [f for f in fetches if bounds[w] < f[0] < bounds[w + 1]]
+            signalled = set()
+            chain = []
+            for i, _, args in win:
+                h, layer, dt, nt, wt, sg, share, stream = args
+                assert dt == DTURNS and nt == n_turns, case
+                assert share == 192 and stream in streams, case
+                assert 0 <= sg < n_turns and sg not in signalled, case
+                assert wt == -1 or (0 <= wt < n_turns and wt in signalled), case
+                signalled.add(sg)
+                chain.append((wt, sg, streams[stream]))
+            # within each step of the window: transfers in group-major, micro-batch order,
+            # each (after the first of the step) waiting for the one before it
+            per_step = ordered * n_mb
+            assert len(chain) == len(windows[w]) * per_step, case
+            for q, (wt, sg, m) in enumerate(chain):
+                j, r = divmod(q, per_step)
+                g, i = divmod(r, n_mb)
+                t = windows[w][j]
+                assert m == i and sg == sched.turn_index(t, g, i), case
+                assert wt == (chain[q - 1][1] if r else -1), case
+            # each micro-batch's transfer follows its own resolve on its stream
+        for i, name, args in fetches:
+            prev = [x for x in hip.log[:i] if x[0] == "call" and x[2] == args[-1]]
+            assert prev[-1][1] == "hisparse_resolve_tables", case
+    hip = _FakeHip()
+    for bad in (dict(n_mb=1, schedule="overlap"), dict(n_mb=2, schedule="overlap", handover=64),
+                dict(n_mb=2, schedule="serial", G=4), dict(n_mb=2, schedule="overlap", link=True)):
+        bad.setdefault("G", 1)
+        with pytest.raises(ValueError):
+            _schedule(hip, layers=4, speculate=False, append=False, turns="all", share=0,
+                      steps=2, dturns=DTURNS, **bad)

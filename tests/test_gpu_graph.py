@@ -11,7 +11,7 @@ import pytest
 import torch
 
 import workload as W
-from hs_harness import Run, attn_desc, layer_cache_host, log
+from hs_harness import Run, attn_desc, layer_cache_host, log, turn_step
 from paper_2608_07009_amd import hisparse as hs
 
 pytestmark = pytest.mark.gpu
@@ -362,3 +362,66 @@ def test_graph_replay_speculate():
         torch.cuda.synchronize()
         eager.close()
         graph.close()
+
+
+def test_graph_replay_with_device_link_turns():
+    """Two micro-batches taking device link turns, captured to a graph with the turns' reset
+    (a fill kernel, no memset node) at its start, the micro-batches forked from and joined back
+    into the capturing stream; every replay (eager work and synchronisations between them)
+    leaves slots, counts and caches identical to hisparse_resolve on twin caches."""
+    w = W.workload(2, num_requests=2, num_layers=2)
+    steps = 5
+    runs = [Run(w, steps), Run(w, steps)]
+    twins = [Run(w, steps), Run(w, steps)]
+    dev = runs[0].dev
+    n_turns = w.num_layers * len(runs)
+    turns = torch.zeros(2 * n_turns, dtype=torch.int32, device=dev)
+    try:
+        turn_step(runs, [torch.cuda.Stream(), torch.cuda.Stream()], turns, 0, w.num_layers)
+        for r in twins:
+            r.resolve_step(0)
+        torch.cuda.synchronize()
+        sel_bufs = [torch.empty_like(r.sel[0]) for r in runs]
+        step = torch.ones(1, dtype=torch.int64, device=dev)
+        g = torch.cuda.CUDAGraph()
+        s0, s1 = torch.cuda.Stream(), torch.cuda.Stream()
+        s0.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s0):
+            with torch.cuda.graph(g, stream=s0):
+                for r, b in zip(runs, sel_bufs):
+                    b.copy_(r.sel.index_select(0, step).squeeze(0))
+                step.add_(1)
+                n_mb = len(runs)
+                hs.hisparse_link_turns_reset(turns, n_turns, s0)
+                fork = torch.cuda.Event()
+                fork.record(s0)
+                s1.wait_event(fork)
+                for l in range(w.num_layers):
+                    for i, (r, b, s) in enumerate(zip(runs, sel_bufs, (s0, s1))):
+                        hs.hisparse_resolve_tables(r.cache.handle, l,
+                                                   b[l * w.units:(l + 1) * w.units],
+                                                   r.slots[l], r.counts[l], s)
+                        ti = l * n_mb + i
+                        hs.hisparse_fetch_turn(r.cache.handle, l, turns, n_turns, ti - 1, ti,
+                                               256, s)
+                join = torch.cuda.Event()
+                join.record(s1)
+                s0.wait_event(join)
+        torch.cuda.synchronize()
+        for t in range(1, steps):
+            g.replay()
+            for r in twins:
+                r.resolve_step(t)
+            torch.cuda.synchronize()
+            scratch = torch.randn(1 << 16, device=dev).sum()  # eager work between replays
+            for r, tw in zip(runs, twins):
+                assert torch.equal(r.slots, tw.slots), f"slots differ at replay {t}"
+                assert torch.equal(r.counts, tw.counts), f"counts differ at replay {t}"
+                for l in range(w.num_layers):
+                    assert (layer_cache_host(r, l) == layer_cache_host(tw, l)).all(), (t, l)
+            assert (turns.view(n_turns, 2)[:, 1] == 1).all(), f"a turn unsignalled at {t}"
+            del scratch
+    finally:
+        torch.cuda.synchronize()
+        for r in runs + twins:
+            r.close()

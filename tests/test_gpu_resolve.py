@@ -9,7 +9,7 @@ import torch
 
 import oracle
 import workload as W
-from hs_harness import Run, expected_order, layer_cache_host, log
+from hs_harness import Run, expected_order, layer_cache_host, log, turn_step
 from paper_2608_07009_amd import HiSparseCache, hisparse as hs
 
 pytestmark = pytest.mark.gpu
@@ -367,3 +367,73 @@ def test_staged_fetches_on_two_streams():
                     assert (img[u, res] == host[u, orc.slot_pos[u, res]]).all(), (t, layer, u)
     finally:
         run.close()
+
+
+def test_fetch_turns_on_two_streams_equal_fetch():
+    """Two micro-batches (two caches, two streams) taking turns on the host link on the device
+    (hisparse_fetch_turn, each transfer waiting for the previous one's signal): slots, counts and
+    every layer's cache byte-identical to hisparse_resolve on a twin cache, every step; a turn
+    that is never signalled only delays its launch (the wait ends by itself after about 4 ms)
+    and changes nothing; argument errors and the unsupported fetch paths are refused."""
+    w = W.workload(2, num_requests=2, num_layers=2)
+    steps = 4
+    runs = [Run(w, steps), Run(w, steps)]
+    twins = [Run(w, steps), Run(w, steps)]
+    none = Run(w, 1, fill=False, fetch=hs.HISPARSE_FETCH_NONE)
+    dev = runs[0].dev
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    n_turns = w.num_layers * len(runs)
+    turns = torch.zeros(2 * n_turns, dtype=torch.int32, device=dev)
+    try:
+        torch.cuda.synchronize()
+        for t in range(steps):
+            log(f"fetch turns step {t}")
+            turn_step(runs, streams, turns, t, w.num_layers)
+            for r in twins:
+                r.resolve_step(t)
+            torch.cuda.synchronize()
+            for r, tw in zip(runs, twins):
+                assert torch.equal(r.slots, tw.slots) and torch.equal(r.counts, tw.counts), t
+                for l in range(w.num_layers):
+                    assert (layer_cache_host(r, l) == layer_cache_host(tw, l)).all(), (t, l)
+            # every turn was signalled by all of its launch's workgroups
+            tv = turns.view(n_turns, 2).cpu()
+            assert (tv[:, 1] == 1).all() and (tv[:, 0] > 0).all(), tv
+        # a wait on a turn never signalled (just reset): bounded, then the same copy
+        s = streams[0]
+        r, tw = runs[0], twins[0]
+        hs.hisparse_link_turns_reset(turns, n_turns, s)
+        hs.hisparse_resolve_tables(r.cache.handle, 0, r.sel_ptr(0, 0), r.slots[0], r.counts[0], s)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        hs.hisparse_fetch_turn(r.cache.handle, 0, turns, n_turns, 1, 0, 256, s)
+        e1.record(s)
+        hs.hisparse_resolve(tw.cache.handle, 0, tw.sel_ptr(0, 0), tw.slots[0], tw.counts[0],
+                            tw.stream)
+        torch.cuda.synchronize()
+        waited = e0.elapsed_time(e1)
+        log(f"fetch waiting on an unsignalled turn: {waited:.2f} ms")
+        assert 3.0 <= waited <= 1000.0, waited
+        assert torch.equal(r.slots[0], tw.slots[0]) and torch.equal(r.counts[0], tw.counts[0])
+        assert (layer_cache_host(r, 0) == layer_cache_host(tw, 0)).all()
+        h = r.cache.handle
+        N = n_turns
+        for bad in ((h, 0, turns, N, 2, 2, 256), (h, 0, turns, N, -2, 0, 256),
+                    (h, 0, turns, N, 0, 1, 0), (h, 0, turns, N, 0, 1, 257),
+                    (h, 0, None, N, 0, 1, 256), (h, 0, turns, 0, -1, -1, 256),
+                    (h, 0, turns, N, N, 0, 256), (h, 0, turns, N, 0, N, 256)):
+            with pytest.raises(hs.HisparseError) as e:
+                hs.hisparse_fetch_turn(*bad, s)
+            assert e.value.status == hs.HISPARSE_ERR_INVALID_ARG, bad
+        with pytest.raises(hs.HisparseError) as e:
+            hs.hisparse_fetch_turn(none.cache.handle, 0, turns, N, -1, 0, 256, s)
+        assert e.value.status == hs.HISPARSE_ERR_UNSUPPORTED
+        for n in (0, 1 << 25):
+            with pytest.raises(hs.HisparseError) as e:
+                hs.hisparse_link_turns_reset(turns, n, s)
+            assert e.value.status == hs.HISPARSE_ERR_INVALID_ARG
+        torch.cuda.synchronize()
+    finally:
+        torch.cuda.synchronize()
+        for r in runs + twins + [none]:
+            r.close()
