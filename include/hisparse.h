@@ -291,9 +291,11 @@ hisparse_status_t hisparse_fetch_part(hisparse_cache_t cache, int32_t layer, int
  *   signal_turn: -1, or the turn this launch signals once signal_share / 256 (1..256) of its
  *     workgroups have finished their copies (256: all of them, the link free).
  * The copies and results equal hisparse_fetch's whatever the order of the launches: a turn
- * orders only the use of the link, never data, and a wait ends by itself after about 4 ms,
- * so a turn never signalled (reset missing, its launch on a stream that waits for this one)
- * costs time, not correctness. For a sequence issued on streams that may run concurrently.
+ * orders only the use of the link, never data. A wait ends by itself after about 4 ms once
+ * the signalling launch has started, or after about 50 us if it has not (not yet issued, or
+ * queued behind this launch), so a turn that cannot be signalled in time (reset missing, its
+ * launch on a stream that waits for this one, launches serialised by a tool) costs time, not
+ * correctness. For a sequence issued on streams that may run concurrently.
  * HISPARSE_ERR_UNSUPPORTED unless the cache fetches zero-copy (the host-issued paths and
  * HISPARSE_FETCH_NONE launch no kernel); INVALID_ARG for a shared layer, a null d_turns,
  * n_turns < 1, indices outside [-1, n_turns), wait_turn == signal_turn, or a share outside

@@ -111,7 +111,8 @@ hipError_t read_resolve_phase_stamps(uint64_t* host, int32_t units);
 hipError_t launch_scatter(const ScatterArgs& a, hipStream_t stream);
 // Host-link turns between fetch launches on different streams (hisparse_fetch_turn): turn i
 // is the word pair turns[2i] (finished workgroups of the launch that signals it) and
-// turns[2i + 1] (non-zero once the launch that waits for it may start reading).
+// turns[2i + 1] (1 once that launch has started, 2 once the launch that waits for it may
+// start reading).
 struct LinkTurn {
   int32_t* turns;  // null: no turn taking
   int32_t wait;    // turn to wait for before the first host read (-1: none)

@@ -447,17 +447,23 @@ __global__ __launch_bounds__(NT) void resolve_kernel(ResolveArgs a) {
   RESOLVE_STAMP(8);
 }
 
-// Link turns as the fetch kernel sees them: the word to poll before reading (null: none), the
-// pair to count finished workgroups into (null: none), and the count that opens the next turn.
+// Link turns as the fetch kernel sees them: the turn to wait for before reading and the turn
+// to signal (null: none), and the count of finished workgroups that opens the next turn. A
+// turn's word 0 counts the signalling launch's finished workgroups; word 1 is 0 until that
+// launch has started, 1 once it has, 2 once the waiting launch may read.
 struct TurnDev {
-  const int32_t* wait_flag;
+  const int32_t* wait_pair;
   int32_t* signal_pair;
   int32_t go;
 };
 
 // A turn only orders the launches' use of the host link; no launch reads what another writes,
-// so a wait that outlasts this bound simply proceeds.
+// so a wait that outlasts its bound simply proceeds: a signalling launch that has started is
+// waited for up to kTurnWaitTicks, one that has not (not yet dispatched, or queued behind the
+// waiter) up to kTurnStartTicks. Issued in turn order, a signalling launch starts before its
+// waiter or within microseconds of it.
 constexpr uint64_t kTurnWaitTicks = 400000;  // 4 ms of the constant 100 MHz clock
+constexpr uint64_t kTurnStartTicks = 5000;   // 50 us
 
 template <int U>
 __global__ __launch_bounds__(kFetchThreads) void fetch_kernel(FetchArgs a, FastDiv div_cpr,
@@ -465,14 +471,21 @@ __global__ __launch_bounds__(kFetchThreads) void fetch_kernel(FetchArgs a, FastD
   // The fetch shares its CUs with other streams' kernels (the other micro-batch's attention and
   // merge); its waves issue little but each issue keeps the host link fed, so they go first.
   __builtin_amdgcn_s_setprio(3);
-  if (turn.wait_flag) {
-    // Waves of a launch that waits for its turn are resident already and poll the flag (an
+  if (turn.signal_pair && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 &&
+      threadIdx.x == 0)
+    __hip_atomic_fetch_max(turn.signal_pair + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (turn.wait_pair) {
+    // Waves of a launch that waits for its turn are resident already and poll its state (an
     // uncached device-scope read every few hundred cycles), so the link passes from one launch
     // to the next without a dependency through the command processor.
     const uint64_t t0 = wall_clock64();
-    while (__hip_atomic_load(turn.wait_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0 &&
-           wall_clock64() - t0 < kTurnWaitTicks)
+    for (;;) {
+      const int32_t st =
+          __hip_atomic_load(turn.wait_pair + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint64_t dt = wall_clock64() - t0;
+      if (st >= 2 || dt >= kTurnWaitTicks || (st == 0 && dt >= kTurnStartTicks)) break;
       __builtin_amdgcn_s_sleep(8);
+    }
   }
   // grid z: the target layers (one plan, each layer's own host records and cache)
   fetch_slice<U>(a, div_cpr, blockIdx.y, blockIdx.z,
@@ -483,7 +496,7 @@ __global__ __launch_bounds__(kFetchThreads) void fetch_kernel(FetchArgs a, FastD
     const int32_t n = __hip_atomic_fetch_add(turn.signal_pair, 1, __ATOMIC_RELAXED,
                                              __HIP_MEMORY_SCOPE_AGENT) + 1;
     if (n == turn.go)
-      __hip_atomic_store(turn.signal_pair + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_fetch_max(turn.signal_pair + 1, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -674,7 +687,7 @@ hipError_t launch_fetch(const FetchArgs& a, int transfer_block_bytes, int workgr
   TurnDev t{nullptr, nullptr, 0};
   if (turn && turn->turns) {
     const int64_t wgs = x * a.units * a.n_layers;
-    if (turn->wait >= 0) t.wait_flag = turn->turns + 2 * (int64_t)turn->wait + 1;
+    if (turn->wait >= 0) t.wait_pair = turn->turns + 2 * (int64_t)turn->wait;
     if (turn->signal >= 0) t.signal_pair = turn->turns + 2 * (int64_t)turn->signal;
     t.go = (int32_t)std::max<int64_t>(1, (wgs * turn->share + 255) / 256);
   }

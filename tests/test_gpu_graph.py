@@ -419,7 +419,7 @@ def test_graph_replay_with_device_link_turns():
                 assert torch.equal(r.counts, tw.counts), f"counts differ at replay {t}"
                 for l in range(w.num_layers):
                     assert (layer_cache_host(r, l) == layer_cache_host(tw, l)).all(), (t, l)
-            assert (turns.view(n_turns, 2)[:, 1] == 1).all(), f"a turn unsignalled at {t}"
+            assert (turns.view(n_turns, 2)[:, 1] == 2).all(), f"a turn unsignalled at {t}"
             del scratch
     finally:
         torch.cuda.synchronize()

@@ -373,8 +373,8 @@ def test_fetch_turns_on_two_streams_equal_fetch():
     """Two micro-batches (two caches, two streams) taking turns on the host link on the device
     (hisparse_fetch_turn, each transfer waiting for the previous one's signal): slots, counts and
     every layer's cache byte-identical to hisparse_resolve on a twin cache, every step; a turn
-    that is never signalled only delays its launch (the wait ends by itself after about 4 ms)
-    and changes nothing; argument errors and the unsupported fetch paths are refused."""
+    that is never signalled only delays its launch (the wait ends by itself, after about 50 us
+    when the signalling launch never started, about 4 ms when it did) and changes nothing; argument errors and the unsupported fetch paths are refused."""
     w = W.workload(2, num_requests=2, num_layers=2)
     steps = 4
     runs = [Run(w, steps), Run(w, steps)]
@@ -398,24 +398,32 @@ def test_fetch_turns_on_two_streams_equal_fetch():
                     assert (layer_cache_host(r, l) == layer_cache_host(tw, l)).all(), (t, l)
             # every turn was signalled by all of its launch's workgroups
             tv = turns.view(n_turns, 2).cpu()
-            assert (tv[:, 1] == 1).all() and (tv[:, 0] > 0).all(), tv
-        # a wait on a turn never signalled (just reset): bounded, then the same copy
+            assert (tv[:, 1] == 2).all() and (tv[:, 0] > 0).all(), tv
+        # waits on turns never signalled: one whose launch never started (just reset) ends
+        # after the start bound, one marked started from the host after the full bound; the
+        # copies are the same
         s = streams[0]
         r, tw = runs[0], twins[0]
-        hs.hisparse_link_turns_reset(turns, n_turns, s)
-        hs.hisparse_resolve_tables(r.cache.handle, 0, r.sel_ptr(0, 0), r.slots[0], r.counts[0], s)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(s)
-        hs.hisparse_fetch_turn(r.cache.handle, 0, turns, n_turns, 1, 0, 256, s)
-        e1.record(s)
-        hs.hisparse_resolve(tw.cache.handle, 0, tw.sel_ptr(0, 0), tw.slots[0], tw.counts[0],
-                            tw.stream)
-        torch.cuda.synchronize()
-        waited = e0.elapsed_time(e1)
-        log(f"fetch waiting on an unsignalled turn: {waited:.2f} ms")
-        assert 3.0 <= waited <= 1000.0, waited
-        assert torch.equal(r.slots[0], tw.slots[0]) and torch.equal(r.counts[0], tw.counts[0])
-        assert (layer_cache_host(r, 0) == layer_cache_host(tw, 0)).all()
+        for started, lo, hi in ((0, 0.04, 2.0), (1, 3.0, 1000.0)):
+            hs.hisparse_link_turns_reset(turns, n_turns, s)
+            with torch.cuda.stream(s):
+                turns[3].fill_(started)  # turn 1's state word
+            hs.hisparse_resolve_tables(r.cache.handle, 0, r.sel_ptr(started, 0), r.slots[0],
+                                       r.counts[0], s)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            hs.hisparse_fetch_turn(r.cache.handle, 0, turns, n_turns, 1, 0, 256, s)
+            e1.record(s)
+            hs.hisparse_resolve(tw.cache.handle, 0, tw.sel_ptr(started, 0), tw.slots[0],
+                                tw.counts[0], tw.stream)
+            torch.cuda.synchronize()
+            waited = e0.elapsed_time(e1)
+            log(f"fetch waiting on an unsignalled turn (state {started}): {waited:.3f} ms")
+            assert lo <= waited <= hi, (started, waited)
+            assert torch.equal(r.slots[0], tw.slots[0]) and torch.equal(r.counts[0],
+                                                                        tw.counts[0])
+            assert (layer_cache_host(r, 0) == layer_cache_host(tw, 0)).all()
+            assert int(turns[1].item()) == 2  # turn 0 signalled by the launch
         h = r.cache.handle
         N = n_turns
         for bad in ((h, 0, turns, N, 2, 2, 256), (h, 0, turns, N, -2, 0, 256),
