@@ -305,7 +305,8 @@ hisparse_status_t hisparse_fetch_turn(hisparse_cache_t cache, int32_t layer, int
                                       int32_t signal_share, void* stream);
 
 /* [async] Zero n_turns (1..2^24) link turns, d_turns[0 .. 2 * n_turns), with a fill kernel on
- * `stream` (capturable; no memset node). See hisparse_fetch_turn. */
+ * `stream` (capturable; no memset node), launched on the calling thread's current HIP device,
+ * which must hold d_turns and `stream`. See hisparse_fetch_turn. */
 hisparse_status_t hisparse_link_turns_reset(int32_t* d_turns, int32_t n_turns, void* stream);
 
 /* [async] Phase 4 for units [unit_begin, unit_begin + unit_count) of an anchor layer only
