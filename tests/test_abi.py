@@ -159,7 +159,12 @@ def test_entry_points_reject_a_null_handle_on_the_host():
         lambda: L.hisparse_append(None, 0, 1, dummy, dummy, dummy, None),
         lambda: L.hisparse_resolve(None, 0, dummy, dummy, None, None),
         lambda: L.hisparse_prefetch_layer(None, 0, 1, None),
+        lambda: L.hisparse_fetch_turn(None, 0, dummy, 4, -1, 0, 256, None),
         lambda: L.hisparse_reset(None, None),
+        # the link turns' reset checks its array and count before launching anything
+        lambda: L.hisparse_link_turns_reset(None, 4, None),
+        lambda: L.hisparse_link_turns_reset(dummy, 0, None),
+        lambda: L.hisparse_link_turns_reset(dummy, (1 << 24) + 1, None),
     ]
     for call in calls:
         assert call() == hs.HISPARSE_ERR_INVALID_ARG
