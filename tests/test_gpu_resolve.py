@@ -369,14 +369,16 @@ def test_staged_fetches_on_two_streams():
         run.close()
 
 
-def test_fetch_turns_on_two_streams_equal_fetch():
+@pytest.mark.parametrize("cfg", [2, 3, 4])
+def test_fetch_turns_on_two_streams_equal_fetch(cfg):
     """Two micro-batches (two caches, two streams) taking turns on the host link on the device
     (hisparse_fetch_turn, each transfer waiting for the previous one's signal): slots, counts and
     every layer's cache byte-identical to hisparse_resolve on a twin cache, every step; a turn
     that is never signalled only delays its launch (the wait ends by itself, after about 50 us
     when the signalling launch never started, about 4 ms when it did) and changes nothing; argument errors and the unsupported fetch paths are refused."""
-    w = W.workload(2, num_requests=2, num_layers=2)
+    w = W.workload(cfg, num_requests=2, num_layers=2)
     steps = 4
+    log(f"test_fetch_turns_on_two_streams_equal_fetch {w.name}")
     runs = [Run(w, steps), Run(w, steps)]
     twins = [Run(w, steps), Run(w, steps)]
     none = Run(w, 1, fill=False, fetch=hs.HISPARSE_FETCH_NONE)
