@@ -1082,7 +1082,12 @@ def main() -> int:
 
     share = max(0, min(256, args.merge_replay_share))
     dturns = dturns_t = None
-    if args.link_turns == "device" and n_mb > 1 and fetch == hs.HISPARSE_FETCH_ZERO_COPY:
+    # device turns take the anchors' own zero-copy fetches; the options that issue the link's
+    # transfers otherwise (a hand-over share, group fetches of shared layers) keep event turns
+    device_ok = not args.handover_share and not (
+        args.schedule in ("serial", "batched") and any(sh for _, sh in groups))
+    if (args.link_turns == "device" and n_mb > 1 and fetch == hs.HISPARSE_FETCH_ZERO_COPY
+            and device_ok):
         n_t = max(1, args.graph_steps) * len(groups) * n_mb
         dturns_t = torch.zeros(2 * n_t, dtype=torch.int32, device=dev)
         dturns = dturns_t.data_ptr()
